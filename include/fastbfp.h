@@ -1,0 +1,171 @@
+/*
+ * fastbfp.h -- C ABI of the MI355X (gfx950) block-floating-point hot path of
+ * FAST (Zhang, McDanel, Kung, "FAST: DNN Training Under Variable Precision
+ * Block Floating Point with Stochastic Rounding", HPCA 2022).
+ *
+ * Two operations sit behind this boundary:
+ *   bfp_quantize  FP32 -> BFP conversion (section III-A; converter of
+ *                 section V-C): one shared exponent per group of g values,
+ *                 sign-magnitude mantissas of m bits, nearest, stochastic or
+ *                 truncating rounding.
+ *   bfp_gemm      the variable-precision BFP dot product / GEMM (section III-B,
+ *                 fMAC of section V-B): per-group integer dot products, one
+ *                 exponent addition per group pair, FP32 accumulation across
+ *                 groups, and a pass count that grows with the mantissa widths.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named x, y, C, P, mant, exp, status_word are DEVICE pointers
+ *     (hipMalloc'd or torch CUDA tensors); pointers to size_t outputs are HOST
+ *     pointers.  The caller owns every buffer; the library allocates nothing
+ *     and keeps no state besides a per-device properties cache.
+ *   - stream is a hipStream_t passed as void* (NULL = the default stream).
+ *     Calls enqueue work on it and return without synchronising.
+ *   - Every argument and shape check happens on the host before any launch;
+ *     a failed check returns a non-zero bfp_status_t and enqueues nothing.
+ *     A failed launch returns BFP_E_HIP.
+ *   - All entry points are thread-safe.
+ *
+ * BFP tensor layout (rows x len values, groups of g consecutive values along
+ * len; g in {16, 32}; len % g == 0)
+ *   exp  : uint8 [rows][len/g]   shared exponent E = the largest FP32 biased
+ *          exponent field in the group (0 for a group of zeros/subnormals).
+ *          One unit in the last place of the group is 2^(E - 127 - (m-1)).
+ *   mant : chunk planes.  A magnitude q in [0, 2^m - 1] is split into 4-bit
+ *          chunks, most significant first: one chunk (q itself) when m <= 4,
+ *          two (hi = q >> 4, lo = q & 15) when 5 <= m <= 8.  Plane c holds
+ *          chunk c of every value, with the value's sign, as the OCP FP6 E2M3
+ *          code of (+-chunk / 2): every integer 0..15 halved is exact in E2M3.
+ *          Codes are packed little-endian, 6 bits per value (value t of a
+ *          group at bits 6t..6t+5), so a group takes 3g/4 bytes per plane:
+ *            plane c, row r, group G at byte offset
+ *            ((c * rows + r) * (len/g) + G) * (3g/4).
+ *          A zero magnitude is stored as code 0 (no sign).
+ *          This is the paper's chunk-plane storage (section V-D) with a chunk
+ *          width of 4 bits, the width that gfx950's block-scaled MFMA consumes
+ *          at its full FP6 rate; the lower chunk's scale is 2^4 below the upper
+ *          chunk's, as the paper decrements the lower 2-bit chunk's exponent.
+ */
+#ifndef FASTBFP_H
+#define FASTBFP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FASTBFP_ABI_VERSION 1
+
+typedef enum {
+  BFP_ROUND_NEAREST = 0,    /* add half an LSB, then truncate (ties away from zero) */
+  BFP_ROUND_STOCHASTIC = 1, /* add an 8-bit Philox noise byte below the LSB, then truncate */
+  BFP_ROUND_TRUNCATE = 2    /* drop the low-order bits (the converter without noise) */
+} bfp_round_t;
+
+typedef enum {
+  BFP_OK = 0,
+  BFP_E_ARG = 1,         /* null pointer, negative size, bad enum value */
+  BFP_E_SHAPE = 2,       /* g does not divide the grouped axis, K mismatch, ldc < N */
+  BFP_E_UNSUPPORTED = 3, /* a valid but unimplemented combination (e.g. g not in {16,32}) */
+  BFP_E_PRECISION = 4,   /* m outside 1..8, or a GEMM precision the stored planes cannot give */
+  BFP_E_HIP = 5          /* the HIP runtime reported an error at launch */
+} bfp_status_t;
+
+/* ABI version of the loaded library (FASTBFP_ABI_VERSION it was built with). */
+int bfp_abi_version(void);
+
+/* Static, NUL-terminated description of a status code. */
+const char* bfp_status_str(int status);
+
+/* Number of 4-bit chunk planes for an m-bit magnitude: 1 if m <= 4, 2 if
+ * 5 <= m <= 8, 0 if m is outside 1..8. */
+int bfp_chunks(int m_bits);
+
+/* Host-side sizes of the two BFP arrays for a rows x len tensor.
+ * Returns BFP_E_ARG for null outputs or negative sizes, BFP_E_SHAPE if
+ * len % g != 0, BFP_E_UNSUPPORTED for g not in {16, 32}, BFP_E_PRECISION for m
+ * outside 1..8. */
+int bfp_quantized_sizes(int64_t rows, int64_t len, int g, int m_bits, size_t* mant_bytes, size_t* exp_bytes);
+
+/*
+ * bfp_quantize -- FP32 -> BFP (section III-A, steps (a)-(d); converter of
+ * section V-C).
+ *   x           : FP32 [R][C], row-major, contiguous.
+ *   group_axis  : 1 -> groups of g consecutive values along each row; the
+ *                 output tensor has rows = R, len = C.
+ *                 0 -> groups of g consecutive values down each column; the
+ *                 output is written with the group axis last, i.e. rows = C,
+ *                 len = R (transpose-on-quantize: every GEMM operand is then
+ *                 K-contiguous, which serves the transposed operands of the
+ *                 backward GEMMs of section II-B).
+ *   g           : 16 or 32; must divide the grouped axis.
+ *   m_bits      : magnitude width 1..8 (a sign bit is kept besides).
+ *   round_mode  : bfp_round_t.
+ *   seed        : stochastic rounding only.  The noise byte of output value t
+ *                 of group gid (gid = the flat index into exp) is byte (t mod 4)
+ *                 of word ((t div 4) mod 4) of Philox4x32-10 with key =
+ *                 (seed mod 2^32, seed div 2^32) and counter = (gid mod 2^32,
+ *                 gid div 2^32, t div 16, 0) (Salmon et al., SC'11), so it does
+ *                 not depend on the launch shape.  The magnitude is then
+ *                 floor(a + U/256), a being the magnitude in units of the LSB.
+ *   mant, exp   : outputs in the layout above, sized by bfp_quantized_sizes.
+ *   status_word : optional device uint32; bit 0 is OR-ed in if any input was
+ *                 Inf or NaN (a precondition violation: those groups' outputs
+ *                 are unspecified).  May be NULL.
+ * Subnormal inputs are flushed to zero.  A group maximum that rounds up to
+ * 2^m saturates at 2^m - 1.
+ */
+int bfp_quantize(const float* x, int64_t R, int64_t C, int group_axis, int g, int m_bits, int round_mode,
+                 uint64_t seed, uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream);
+
+/*
+ * bfp_dequantize -- BFP -> FP32: y[r][k] = +-q * 2^(E - 127 - (m-1)), the value
+ * the BFP element stands for (section III-A).  Exact whenever the result is a
+ * normal FP32 number.  y is FP32 [rows][len].
+ */
+int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int g, int m_bits, float* y,
+                   void* stream);
+
+/*
+ * bfp_gemm -- C[M][N] = A[M][K] * B[N][K]^T for BFP operands grouped along K
+ * (section III-B and the fMAC of section V-B):
+ *   C[i][j] = sum over groups G of P_G * 2^(ea + eb - 254 - (m_a-1) - (m_b-1)),
+ *   P_G     = sum_{k in G} qa[i][k] * qb[j][k]   (exact integer products).
+ * The products are exact; the cross-group sum is accumulated in FP32.
+ *   a_mant/a_exp : A stored with a_m_bits (rows M, len K); likewise B (rows N).
+ *   m_a, m_b     : the precisions the product is taken at.  Either the stored
+ *                  width, or, for a two-chunk operand, the stored width minus
+ *                  4: the low chunk plane is then skipped, i.e. the magnitude is
+ *                  truncated to its top m - 4 bits (the paper's discard of a
+ *                  low-order chunk, section V-D).  Anything else returns
+ *                  BFP_E_PRECISION.
+ *   Passes: the kernel issues chunks(m_a) * chunks(m_b) block-scaled MFMA
+ *   passes per group pair (1 for m_a, m_b <= 4), the counterpart of the
+ *   paper's (m_a/2)(m_b/2) fMAC rounds.
+ *   C            : FP32 with row stride ldc >= N (elements).
+ * Preconditions for the stated accuracy: every group exponent E is at most 250,
+ * and every scaled group sum, partial sum and |C| stays in the FP32 normal range.
+ */
+int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+             int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, float* C, int64_t ldc,
+             void* stream);
+
+/*
+ * bfp_gemm_group_partials -- the exact integer group dot products
+ *   P[G][i][j] = sum_{k in G} qa'[i][k] * qb'[j][k]
+ * (parts M and A of section III-B), qa' and qb' being the magnitudes at m_a and
+ * m_b bits with their signs, computed with int8 MFMA and combined across chunk
+ * planes in integers (sum of 2^(4(ca+cb)) * P_{ca,cb}).  P is int32
+ * [K/g][M][N].  Meant for verification: it writes K/g times more output than
+ * bfp_gemm.  Same operand and precision rules as bfp_gemm (the exponents do not
+ * enter P, so only the mantissa planes are passed).
+ */
+int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* b_mant, int b_m_bits, int64_t M,
+                            int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASTBFP_H */

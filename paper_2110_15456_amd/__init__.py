@@ -1,0 +1,166 @@
+"""MI355X (gfx950) BFP hot path of FAST: FP32 -> BFP quantization and the
+variable-precision BFP GEMM.
+
+This module is a thin binding over the C ABI of ``include/fastbfp.h``
+(``libfastbfp.so``): it checks tensor arguments, allocates outputs with torch
+(device memory is torch's), passes raw pointers and torch's current stream,
+and turns non-zero statuses into exceptions.  Every step of the computation
+runs in the library's HIP kernels; there is no CPU path.
+
+    A = quantize(x, group_axis=-1, g=16, m=4, rounding="nearest")
+    W = quantize(w, group_axis=0, g=16, m=2)        # K-contiguous, transposed
+    y = gemm(A, W)                                   # FP32 [M, N] = x . w
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import torch
+
+from ._lib import BFPError, check, load
+
+__all__ = ["BFPTensor", "BFPError", "quantize", "dequantize", "gemm", "gemm_group_partials", "chunks",
+           "quantized_sizes", "ROUNDING"]
+
+ROUNDING = {"nearest": 0, "stochastic": 1, "truncate": 2}
+
+
+def chunks(m: int) -> int:
+    """4-bit chunk planes used for an m-bit magnitude (1 if m <= 4, else 2)."""
+    return int(load().bfp_chunks(int(m)))
+
+
+def quantized_sizes(rows: int, length: int, g: int, m: int):
+    """(mantissa bytes, exponent bytes) of a rows x length BFP tensor."""
+    mb, eb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    check(load().bfp_quantized_sizes(rows, length, g, m, ctypes.byref(mb), ctypes.byref(eb)), "bfp_quantized_sizes")
+    return mb.value, eb.value
+
+
+@dataclass
+class BFPTensor:
+    """A rows x len BFP tensor, groups of g along len (see include/fastbfp.h).
+
+    mant: uint8 chunk planes (flat, chunks(m) * rows * len * 3/4 bytes);
+    exp: uint8 [rows, len // g] shared exponents.
+    """
+    mant: torch.Tensor
+    exp: torch.Tensor
+    rows: int
+    len: int
+    g: int
+    m: int
+
+    @property
+    def planes(self) -> int:
+        return chunks(self.m)
+
+    @property
+    def device(self) -> torch.device:
+        return self.mant.device
+
+    @staticmethod
+    def empty(rows: int, length: int, g: int, m: int, device) -> "BFPTensor":
+        mb, eb = quantized_sizes(rows, length, g, m)
+        return BFPTensor(torch.empty(mb, dtype=torch.uint8, device=device),
+                         torch.empty((rows, length // g), dtype=torch.uint8, device=device), rows, length, g, m)
+
+
+def _stream(dev: torch.device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _need_cuda(t: torch.Tensor, name: str, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must have dtype %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rounding: str = "nearest",
+             seed: int = 0, status: torch.Tensor | None = None, out: BFPTensor | None = None) -> BFPTensor:
+    """FP32 -> BFP with groups of g along ``group_axis``.
+
+    group_axis -1 (or the last axis): groups along the last axis; leading axes
+    are flattened into rows.  group_axis 0 of a 2-D [R, C] tensor: groups down
+    the columns, written transposed as a [C, R] BFP tensor (K-contiguous for
+    the GEMM).  ``status``: optional int32/uint32 CUDA scalar whose bit 0 is set
+    on Inf/NaN input.  ``out``: optional preallocated BFPTensor of the result
+    shape (no allocation happens then).
+    """
+    _need_cuda(x, "x", torch.float32)
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    if x.dim() < 1:
+        raise ValueError("x must have at least one dimension")
+    nd = x.dim()
+    ax = group_axis % nd
+    if ax == nd - 1:
+        C = x.shape[-1]
+        R = x.numel() // C if C else 0
+        axis_flag, rows, length = 1, R, C
+    elif nd == 2 and ax == 0:
+        R, C = x.shape
+        axis_flag, rows, length = 0, C, R
+    else:
+        raise ValueError("group_axis must be the last axis, or 0 of a 2-D tensor")
+    t = out if out is not None else BFPTensor.empty(rows, length, g, m, x.device)
+    if (t.rows, t.len, t.g, t.m) != (rows, length, g, m):
+        raise ValueError("out has the wrong shape or format")
+    st_ptr = None
+    if status is not None:
+        _need_cuda(status, "status")
+        st_ptr = ctypes.c_void_p(status.data_ptr())
+    lib = load()
+    check(lib.bfp_quantize(ctypes.c_void_p(x.data_ptr()), R, C, axis_flag, g, m, ROUNDING[rounding],
+                           ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(t.mant.data_ptr()),
+                           ctypes.c_void_p(t.exp.data_ptr()), st_ptr, _stream(x.device)), "bfp_quantize")
+    return t
+
+
+def dequantize(t: BFPTensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """BFP -> FP32 [rows, len]: +-q * 2^(E - 127 - (m-1))."""
+    y = out if out is not None else torch.empty((t.rows, t.len), dtype=torch.float32, device=t.device)
+    _need_cuda(y, "out", torch.float32)
+    check(load().bfp_dequantize(ctypes.c_void_p(t.mant.data_ptr()), ctypes.c_void_p(t.exp.data_ptr()), t.rows,
+                                t.len, t.g, t.m, ctypes.c_void_p(y.data_ptr()), _stream(t.device)), "bfp_dequantize")
+    return y
+
+
+def _gemm_args(A: BFPTensor, B: BFPTensor, m_a, m_b):
+    if A.len != B.len or A.g != B.g:
+        raise ValueError("A and B must share K and the group size (A: K=%d g=%d, B: K=%d g=%d)"
+                         % (A.len, A.g, B.len, B.g))
+    return (A.m if m_a is None else int(m_a)), (B.m if m_b is None else int(m_b))
+
+
+def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = None,
+         out: torch.Tensor | None = None) -> torch.Tensor:
+    """C = A . B^T in FP32 [A.rows, B.rows] for BFP A [M, K] and B [N, K].
+
+    m_a / m_b: precision of each operand in the product (default: stored m;
+    for a two-chunk operand, m - 4 drops the low chunk plane).
+    """
+    m_a, m_b = _gemm_args(A, B, m_a, m_b)
+    C = out if out is not None else torch.empty((A.rows, B.rows), dtype=torch.float32, device=A.device)
+    _need_cuda(C, "out", torch.float32)
+    if C.dim() != 2 or C.shape[0] != A.rows or C.shape[1] != B.rows:
+        raise ValueError("out must be [%d, %d]" % (A.rows, B.rows))
+    check(load().bfp_gemm(ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
+                          ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows, B.rows,
+                          A.len, A.g, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0), _stream(A.device)),
+          "bfp_gemm")
+    return C
+
+
+def gemm_group_partials(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = None) -> torch.Tensor:
+    """Exact int32 group partials P [K/g, M, N] (int8 MFMA)."""
+    m_a, m_b = _gemm_args(A, B, m_a, m_b)
+    P = torch.empty((A.len // A.g, A.rows, B.rows), dtype=torch.int32, device=A.device)
+    check(load().bfp_gemm_group_partials(ctypes.c_void_p(A.mant.data_ptr()), A.m, ctypes.c_void_p(B.mant.data_ptr()),
+                                         B.m, A.rows, B.rows, A.len, A.g, m_a, m_b, ctypes.c_void_p(P.data_ptr()),
+                                         _stream(A.device)), "bfp_gemm_group_partials")
+    return P

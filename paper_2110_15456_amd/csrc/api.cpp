@@ -1,0 +1,131 @@
+// api.cpp -- the C ABI declared in include/fastbfp.h: argument validation on
+// the host, then a launch on the caller's stream.  No exception, allocation or
+// synchronisation happens here.
+#include <hip/hip_runtime.h>
+
+#include "../../include/fastbfp.h"
+#include "launch.h"
+
+namespace {
+
+bool group_supported(int g) { return g == 16 || g == 32; }
+
+int check_tensor(int64_t rows, int64_t len, int g, int m) {
+  if (rows < 0 || len < 0) return BFP_E_ARG;
+  if (m < 1 || m > 8) return BFP_E_PRECISION;
+  if (g <= 0) return BFP_E_ARG;
+  if (!group_supported(g)) return BFP_E_UNSUPPORTED;
+  if (len % g != 0) return BFP_E_SHAPE;
+  return BFP_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Planes the GEMM reads for an operand stored at m_stored and used at m_use:
+// every stored plane, or only the high plane when the low chunk is dropped.
+int planes_used(int m_stored, int m_use) {
+  if (m_use == m_stored) return m_stored > 4 ? 2 : 1;
+  if (m_stored > 4 && m_use == m_stored - 4) return 1;
+  return 0;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? BFP_OK : BFP_E_HIP; }
+
+int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, int64_t M, int64_t N, int64_t K, int g,
+               int m_a, int m_b) {
+  if (M < 0 || N < 0 || K < 0) return BFP_E_ARG;
+  if ((M > 0 && K > 0 && !a_mant) || (N > 0 && K > 0 && !b_mant)) return BFP_E_ARG;
+  if (a_m < 1 || a_m > 8 || b_m < 1 || b_m > 8) return BFP_E_PRECISION;
+  if (g <= 0) return BFP_E_ARG;
+  if (!group_supported(g)) return BFP_E_UNSUPPORTED;
+  if (K % g != 0) return BFP_E_SHAPE;
+  if (planes_used(a_m, m_a) == 0 || planes_used(b_m, m_b) == 0) return BFP_E_PRECISION;
+  if (M > 0x7fffffff || N > 0x7fffffff || K / g > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  if (!aligned(a_mant, 4) || !aligned(b_mant, 4)) return BFP_E_ARG;
+  return BFP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bfp_abi_version(void) { return FASTBFP_ABI_VERSION; }
+
+const char* bfp_status_str(int status) {
+  switch (status) {
+    case BFP_OK: return "ok";
+    case BFP_E_ARG: return "invalid argument (null or misaligned pointer, negative size, bad enum)";
+    case BFP_E_SHAPE: return "shape mismatch (group size must divide the grouped axis; K and ldc must agree)";
+    case BFP_E_UNSUPPORTED: return "unsupported configuration (group size must be 16 or 32)";
+    case BFP_E_PRECISION: return "unsupported precision (m in 1..8; GEMM precision must be the stored width or drop "
+                                 "the low 4-bit chunk)";
+    case BFP_E_HIP: return "HIP runtime error at launch";
+    default: return "unknown status";
+  }
+}
+
+int bfp_chunks(int m_bits) { return (m_bits < 1 || m_bits > 8) ? 0 : (m_bits > 4 ? 2 : 1); }
+
+int bfp_quantized_sizes(int64_t rows, int64_t len, int g, int m_bits, size_t* mant_bytes, size_t* exp_bytes) {
+  if (!mant_bytes || !exp_bytes) return BFP_E_ARG;
+  const int st = check_tensor(rows, len, g, m_bits);
+  if (st != BFP_OK) return st;
+  *mant_bytes = (size_t)bfp_chunks(m_bits) * (size_t)rows * (size_t)len * 3 / 4;
+  *exp_bytes = (size_t)rows * (size_t)(len / g);
+  return BFP_OK;
+}
+
+int bfp_quantize(const float* x, int64_t R, int64_t C, int group_axis, int g, int m_bits, int round_mode,
+                 uint64_t seed, uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream) {
+  if (group_axis != 0 && group_axis != 1) return BFP_E_ARG;
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  const int64_t rows = group_axis == 1 ? R : C, len = group_axis == 1 ? C : R;
+  const int st = check_tensor(rows, len, g, m_bits);
+  if (st != BFP_OK) return st;
+  if (R == 0 || C == 0) return BFP_OK;
+  if (!x || !mant || !exp) return BFP_E_ARG;
+  if (!aligned(x, group_axis == 1 ? 16 : 4) || !aligned(mant, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (group_axis == 1)
+    return status_of(fastbfp::launch_quantize_rows(x, R, C, g, m_bits, round_mode, seed, mant, exp, status_word, s));
+  return status_of(fastbfp::launch_quantize_cols(x, R, C, g, m_bits, round_mode, seed, mant, exp, status_word, s));
+}
+
+int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int g, int m_bits, float* y,
+                   void* stream) {
+  const int st = check_tensor(rows, len, g, m_bits);
+  if (st != BFP_OK) return st;
+  if (rows == 0 || len == 0) return BFP_OK;
+  if (!mant || !exp || !y) return BFP_E_ARG;
+  if (!aligned(mant, 4) || !aligned(y, 16)) return BFP_E_ARG;
+  return status_of(fastbfp::launch_dequantize(mant, exp, rows, len, g, m_bits, y, static_cast<hipStream_t>(stream)));
+}
+
+int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+             int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, float* C, int64_t ldc,
+             void* stream) {
+  int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
+  if (st != BFP_OK) return st;
+  if (ldc < N) return BFP_E_SHAPE;
+  if (M == 0 || N == 0) return BFP_OK;
+  if (!C || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
+  if (g != 16) return BFP_E_UNSUPPORTED;
+  const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
+  return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, bfp_chunks(a_m_bits), na, b_mant, b_exp,
+                                           bfp_chunks(b_m_bits), nb, M, N, K, g, 4 - m_a - m_b, C, ldc,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* b_mant, int b_m_bits, int64_t M,
+                            int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream) {
+  int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
+  if (st != BFP_OK) return st;
+  if (M == 0 || N == 0 || K == 0) return BFP_OK;
+  if (!P) return BFP_E_ARG;
+  if ((M + 31) / 32 > 65535 || K / g > 65535) return BFP_E_UNSUPPORTED;
+  const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
+  return status_of(fastbfp::launch_group_partials(a_mant, bfp_chunks(a_m_bits), na, b_mant, bfp_chunks(b_m_bits), nb,
+                                                  M, N, K, g, P, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,27 @@
+// launch.h -- internal launchers behind the C ABI (host side).  Arguments are
+// validated by the callers in api.cpp; these functions only pick a kernel
+// specialisation and launch it on the given stream.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fastbfp {
+
+// Rounding modes, numerically equal to bfp_round_t.
+enum { kNearest = 0, kStochastic = 1, kTruncate = 2 };
+
+hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,
+                                uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
+hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
+                                uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
+hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
+                             float* y, hipStream_t s);
+// na / nb: chunk planes used (1 or 2); a_off / b_off: the stored operand's plane
+// count, which sets the plane stride.  scale_log2 = 4 - m_a - m_b.
+hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_planes, int na, const uint8_t* b_mant,
+                          const uint8_t* b_exp, int b_planes, int nb, int64_t M, int64_t N, int64_t K, int g,
+                          int scale_log2, float* C, int64_t ldc, hipStream_t s);
+hipError_t launch_group_partials(const uint8_t* a_mant, int a_planes, int na, const uint8_t* b_mant, int b_planes,
+                                 int nb, int64_t M, int64_t N, int64_t K, int g, int32_t* P, hipStream_t s);
+
+}  // namespace fastbfp

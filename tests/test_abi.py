@@ -1,0 +1,146 @@
+"""The C-ABI library: it loads without a GPU, exports every symbol the header
+declares, and rejects bad arguments on the host before any launch.  CPU only:
+every call here returns before touching the HIP runtime."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+from paper_2110_15456_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fastbfp.h")
+OK, E_ARG, E_SHAPE, E_UNSUP, E_PREC, E_HIP = range(6)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bfp_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("libfastbfp.so is not built; run __graft_entry__.build()")
+    return _lib.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(lib, n), n
+    # and the binding's signature table covers exactly the header
+    assert sorted(_lib.SIGNATURES) == names
+
+
+def test_version_and_status_strings(lib):
+    assert lib.bfp_abi_version() == 1
+    for s in range(6):
+        assert len(lib.bfp_status_str(s)) > 0
+    assert lib.bfp_status_str(99) == b"unknown status"
+
+
+def test_chunks(lib):
+    assert [lib.bfp_chunks(m) for m in range(0, 10)] == [0, 1, 1, 1, 1, 2, 2, 2, 2, 0]
+
+
+def test_quantized_sizes(lib):
+    mb, eb = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.bfp_quantized_sizes(8192, 8192, 16, 4, ctypes.byref(mb), ctypes.byref(eb)) == OK
+    assert (mb.value, eb.value) == (8192 * 8192 * 3 // 4, 8192 * 512)
+    assert lib.bfp_quantized_sizes(3, 64, 32, 8, ctypes.byref(mb), ctypes.byref(eb)) == OK
+    assert (mb.value, eb.value) == (2 * 3 * 64 * 3 // 4, 6)
+    assert lib.bfp_quantized_sizes(3, 40, 16, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_SHAPE
+    assert lib.bfp_quantized_sizes(3, 64, 8, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_UNSUP
+    assert lib.bfp_quantized_sizes(3, 64, 16, 9, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC
+    assert lib.bfp_quantized_sizes(3, 64, 16, 0, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC
+    assert lib.bfp_quantized_sizes(-1, 64, 16, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_ARG
+    assert lib.bfp_quantized_sizes(3, 64, 16, 4, None, ctypes.byref(eb)) == E_ARG
+
+
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: every call below fails validation first
+
+
+def q(lib, x=FAKE, R=4, C=64, axis=1, g=16, m=4, mode=0, mant=FAKE, exp=FAKE, st=None):
+    return lib.bfp_quantize(x, R, C, axis, g, m, mode, 0, mant, exp, st, None)
+
+
+def test_quantize_validation(lib):
+    assert q(lib, x=None) == E_ARG
+    assert q(lib, mant=None) == E_ARG
+    assert q(lib, axis=2) == E_ARG
+    assert q(lib, mode=3) == E_ARG
+    assert q(lib, mode=-1) == E_ARG
+    assert q(lib, C=40) == E_SHAPE
+    assert q(lib, R=40, axis=0) == E_SHAPE
+    assert q(lib, g=8) == E_UNSUP
+    assert q(lib, g=0) == E_ARG
+    assert q(lib, m=9) == E_PREC
+    assert q(lib, m=0) == E_PREC
+    assert q(lib, R=-1) == E_ARG
+    assert q(lib, x=ctypes.c_void_p(0x100004)) == E_ARG  # FP32 rows must be 16-byte aligned
+    assert q(lib, R=0) == OK  # empty: nothing to launch
+    assert q(lib, x=None, C=0, R=0) == OK
+
+
+def gm(lib, a=FAKE, ae=FAKE, am=4, b=FAKE, be=FAKE, bm=4, M=8, N=8, K=64, g=16, ma=4, mb=4, C=FAKE, ldc=8):
+    return lib.bfp_gemm(a, ae, am, b, be, bm, M, N, K, g, ma, mb, C, ldc, None)
+
+
+def test_gemm_validation(lib):
+    assert gm(lib, a=None) == E_ARG
+    assert gm(lib, C=None) == E_ARG
+    assert gm(lib, ae=None) == E_ARG
+    assert gm(lib, K=40) == E_SHAPE
+    assert gm(lib, ldc=7) == E_SHAPE
+    assert gm(lib, g=8) == E_UNSUP
+    assert gm(lib, M=-1) == E_ARG
+    assert gm(lib, am=9) == E_PREC
+    assert gm(lib, ma=3) == E_PREC          # m=4 is one chunk: nothing to drop
+    assert gm(lib, am=8, ma=5) == E_PREC    # only whole 4-bit chunks can be dropped
+    assert gm(lib, am=4, ma=5) == E_PREC    # cannot raise precision
+    assert gm(lib, bm=6, mb=1) == E_PREC
+    assert gm(lib, a=ctypes.c_void_p(0x100001)) == E_ARG
+    assert gm(lib, M=0) == OK and gm(lib, N=0, ldc=0) == OK
+
+
+def test_group_partials_validation(lib):
+    f = lib.bfp_gemm_group_partials
+    assert f(None, 4, FAKE, 4, 8, 8, 64, 16, 4, 4, FAKE, None) == E_ARG
+    assert f(FAKE, 4, FAKE, 4, 8, 8, 64, 16, 4, 4, None, None) == E_ARG
+    assert f(FAKE, 4, FAKE, 4, 8, 8, 60, 16, 4, 4, FAKE, None) == E_SHAPE
+    assert f(FAKE, 8, FAKE, 4, 8, 8, 64, 16, 3, 4, FAKE, None) == E_PREC
+    assert f(FAKE, 4, FAKE, 4, 0, 8, 64, 16, 4, 4, FAKE, None) == OK
+
+
+def test_dequantize_validation(lib):
+    f = lib.bfp_dequantize
+    assert f(None, FAKE, 4, 64, 16, 4, FAKE, None) == E_ARG
+    assert f(FAKE, FAKE, 4, 60, 16, 4, FAKE, None) == E_SHAPE
+    assert f(FAKE, FAKE, 4, 64, 16, 10, FAKE, None) == E_PREC
+    assert f(FAKE, FAKE, 0, 64, 16, 4, None, None) == OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    """No CPU fallback: a missing library is an ImportError at first use."""
+    code = ("import paper_2110_15456_amd._lib as L; L.LIB_PATH = %r\n"
+            "try:\n    L.load()\nexcept ImportError as e:\n    print('raised', e)\n" % str(tmp_path / "missing.so"))
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
+    assert "raised" in out.stdout, out.stderr
+
+
+def test_product_path_does_not_touch_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2110_15456_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                pat = r"^\s*(import|from)\s+oracle\b|liboracle|\boracle\.\w+\s*\(|oracle\.c\b"
+                assert not re.search(pat, text, flags=re.M), os.path.join(dirpath, f)

@@ -1,0 +1,157 @@
+"""GPU parity of bfp_gemm (block-scaled MFMA) and bfp_gemm_group_partials
+(int8 MFMA) with the oracle.  Group partials must be bit-exact; every FP32
+output must satisfy |C_gpu - C_oracle| <= 1e-6 * sum_G |T_G| (the oracle sums
+in double).  Operands are quantized on both sides from the same FP32 inputs,
+and their quantized bytes are checked bit-exact first."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2110_15456_amd as fb
+from paper_2110_15456_amd import synth
+from gpu_util import announce, check_quantize, THREADS
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-6
+
+
+def operands(xa, xb, m_a_st, m_b_st, a_axis=-1, b_axis=-1, mode_a="nearest", mode_b="nearest", seed=0,
+             rows=None):
+    """GPU BFP tensors plus the oracle's own quantization of the same inputs."""
+    A, qa, ea = check_quantize(xa, a_axis, 16, m_a_st, mode_a, seed=seed, rows=None)
+    B, qb, eb = check_quantize(xb, b_axis, 16, m_b_st, mode_b, seed=seed + 1)
+    return A, B, (qa, ea), (qb, eb)
+
+
+def check_gemm(A, B, oa, ob, m_a=None, m_b=None, rows=None, partials=False):
+    m_a = A.m if m_a is None else m_a
+    m_b = B.m if m_b is None else m_b
+    C = fb.gemm(A, B, m_a, m_b)
+    torch.cuda.synchronize()
+    Cg = C.cpu().numpy().astype(np.float64)
+    idx = np.arange(A.rows) if rows is None else np.asarray(rows)
+    Co, S = oracle.gemm(oa[0], oa[1], A.m, ob[0], ob[1], B.m, g=16, m_a=m_a, m_b=m_b, rows=idx, threads=THREADS)
+    err = np.abs(Cg[idx] - Co)
+    ratio = err / np.maximum(S, 1e-300)
+    worst = np.unravel_index(np.argmax(ratio), ratio.shape)
+    assert np.all(err <= TOL * S), "max err/sum|T| = %.3g at %s (gpu %r oracle %r)" % (
+        ratio[worst], worst, Cg[idx][worst], Co[worst])
+    if partials:
+        P = fb.gemm_group_partials(A, B, m_a, m_b).cpu().numpy()
+        Po = oracle.group_partials(oa[0], A.m, ob[0], B.m, g=16, m_a=m_a, m_b=m_b, rows=idx)
+        assert np.array_equal(P[:, idx, :].astype(np.int64), Po)
+    return float(ratio.max())
+
+
+@pytest.mark.parametrize("K", [16, 32])
+def test_tiny_all_precisions(K):
+    """M = N = 4, K = 16 and 32: every stored (m_a, m_b) in 1..8, and the
+    low-chunk drop where an operand has two chunks; C and the int32 partials."""
+    x = synth.draw("normal", (8, K), 300 + K)
+    for am in range(1, 9):
+        for bm in range(1, 9):
+            announce("gemm tiny K=%d stored (%d,%d)" % (K, am, bm))
+            A, B, oa, ob = operands(x[:4], x[4:], am, bm)
+            for m_a in sorted({am, am - 4} - {-3, -2, -1, 0}):
+                for m_b in sorted({bm, bm - 4} - {-3, -2, -1, 0}):
+                    check_gemm(A, B, oa, ob, m_a, m_b, partials=True)
+
+
+def test_config1_256():
+    """A 256x256 and B 256x256 from N(0,1) (seed 0, one stream); A at m=2
+    along K, B [K, N] quantized along axis 0 (its K) at m=4; round to nearest."""
+    a, b = synth.gemm_pair_normal(256, 256, 256, seed=0)
+    announce("gemm config 256^3 (2,4)")
+    A, B, oa, ob = operands(a, b, 2, 4, a_axis=-1, b_axis=0)
+    check_gemm(A, B, oa, ob, partials=True)
+
+
+SHAPES = [(300, 200, 592), (257, 129, 576), (129, 257, 144), (1, 1, 16), (5, 300, 4096), (64, 64, 2048)]
+PAIRS = [(2, 2), (2, 4), (4, 4), (4, 6), (6, 8), (8, 8), (3, 7), (1, 5)]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_ragged_shapes(shape):
+    M, N, K = shape
+    xa = synth.draw("half_normal", (M, K), M + K)
+    xb = synth.draw("weights", (N, K), N + 2 * K)
+    for pa, pb in PAIRS:
+        announce("gemm %dx%dx%d (%d,%d)" % (M, N, K, pa, pb))
+        A, B, oa, ob = operands(xa, xb, pa, pb)
+        check_gemm(A, B, oa, ob, partials=(M * N * K <= 64 * 64 * 2048))
+
+
+def test_precision_lowering():
+    xa = synth.draw("half_normal", (130, 320), 5)
+    xb = synth.draw("grads", (70, 320), 6)
+    announce("gemm stored (8,6) used at (4,2) and mixed")
+    A, B, oa, ob = operands(xa, xb, 8, 6, mode_b="stochastic", seed=3)
+    for m_a, m_b in [(4, 2), (8, 2), (4, 6), (8, 6)]:
+        check_gemm(A, B, oa, ob, m_a, m_b, partials=True)
+
+
+def test_gradient_operands_wide_exponents():
+    """Laplace gradients with outliers on both sides, stochastic rounding."""
+    xa = synth.draw("grads", (256, 1024), 51)
+    xb = synth.draw("grads", (192, 1024), 52)
+    for pair in [(2, 2), (4, 4), (6, 8)]:
+        announce("gemm grads x grads %s" % (pair,))
+        A, B, oa, ob = operands(xa, xb, *pair, mode_a="stochastic", mode_b="stochastic", seed=17)
+        check_gemm(A, B, oa, ob)
+
+
+def sampled_rows(M, n, seed):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([[0, M - 1], rng.choice(M, n, replace=False)]))
+
+
+def big_case(M, N, K, pa, pb, dist_a, dist_b, seed, b_axis=-1, nrows=24):
+    xa = synth.draw(dist_a, (M, K), seed)
+    xb = synth.draw(dist_b, (N, K) if b_axis == -1 else (K, N), seed + 1)
+    rows = sampled_rows(M, nrows, seed)
+    announce("gemm %dx%dx%d (%d,%d) %s x %s sampled rows" % (M, N, K, pa, pb, dist_a, dist_b))
+    A = fb.quantize(torch.from_numpy(xa).cuda(), g=16, m=pa)
+    B = fb.quantize(torch.from_numpy(xb).cuda(), group_axis=b_axis, g=16, m=pb)
+    # oracle operands: A only on the sampled rows, B in full
+    qa = np.zeros((M, K), np.int16)
+    ea = np.zeros((M, K // 16), np.uint8)
+    for r in rows:
+        q1, e1, _ = oracle.quantize(xa, g=16, m=pa, rows=(int(r), int(r) + 1))
+        qa[r], ea[r] = q1[0], e1[0]
+    qb, eb, _ = oracle.quantize(xb, axis=b_axis, g=16, m=pb, threads=THREADS)
+    return check_gemm(A, B, (qa, ea), (qb, eb), rows=rows)
+
+
+@pytest.mark.parametrize("shape", [(8192, 12288, 4096), (8192, 4096, 4096), (8192, 16384, 4096),
+                                   (8192, 4096, 16384)])
+def test_transformer_shapes_sampled(shape):
+    M, N, K = shape
+    for pa, pb in [(2, 4), (8, 8)]:
+        big_case(M, N, K, pa, pb, "normal", "weights", seed=41)
+
+
+@pytest.mark.parametrize("shape", [(802816, 64, 576), (200704, 128, 1152), (50176, 256, 2304),
+                                   (12544, 512, 4608)])
+def test_resnet_im2col_shapes_sampled(shape):
+    M, N, K = shape
+    big_case(M, N, K, 2, 4, "half_normal", "weights", seed=61)
+
+
+def test_ffn_backward_shapes_sampled():
+    """dX = dY . W^T (K = 16384) and dW = X^T . dY (operands regrouped along
+    the token axis by transpose-on-quantize)."""
+    big_case(8192, 4096, 16384, 4, 4, "grads", "weights", seed=53)
+    # dW[4096, 16384] = X^T [4096, 8192] . dY [8192, 16384]: quantize X and dY
+    # along axis 0 (tokens); the oracle does the same from the untransposed arrays
+    x = synth.draw("half_normal", (8192, 4096), 51)
+    dy = synth.draw("grads", (8192, 16384), 54)
+    rows = sampled_rows(4096, 16, 9)
+    announce("gemm dW 4096x16384x8192 regrouped operands")
+    A = fb.quantize(torch.from_numpy(x).cuda(), group_axis=0, g=16, m=6)
+    B = fb.quantize(torch.from_numpy(dy).cuda(), group_axis=0, g=16, m=6, rounding="stochastic", seed=7)
+    qa, ea, _ = oracle.quantize(x, axis=0, g=16, m=6, threads=THREADS)
+    qb, eb, _ = oracle.quantize(dy, axis=0, g=16, m=6, mode="stochastic", seed=7, threads=THREADS)
+    check_gemm(A, B, (qa, ea), (qb, eb), rows=rows)

@@ -1,0 +1,133 @@
+"""GPU parity of bfp_quantize / bfp_dequantize with the oracle: exponents and
+packed mantissas bit-exact, on small ragged shapes, edge values, both group
+axes, every m and rounding mode, and the full 64M-element quantize sweep."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import bfp_codec
+import paper_2110_15456_amd as fb
+from paper_2110_15456_amd import synth
+from gpu_util import announce, check_quantize, gpu_quantize, THREADS
+
+pytestmark = pytest.mark.gpu
+MODES = ("nearest", "stochastic", "truncate")
+
+
+@pytest.mark.parametrize("g", [16, 32])
+@pytest.mark.parametrize("m", range(1, 9))
+@pytest.mark.parametrize("dist", ["normal", "grads"])
+def test_rows_small_ragged(g, m, dist):
+    # 37 x 768: 1776 groups at g=16 (7 workgroups, the last one partial)
+    x = synth.draw(dist, (37, 768), 1000 + m)
+    for mode in MODES:
+        announce("quantize rows 37x768 g=%d m=%d %s %s" % (g, m, dist, mode))
+        check_quantize(x, -1, g, m, mode, seed=77 + m)
+
+
+@pytest.mark.parametrize("shape", [(16 * 37, 100), (512, 64), (32 * 9, 130), (16, 1)])
+@pytest.mark.parametrize("g", [16, 32])
+def test_cols_transposed(shape, g):
+    R, C = shape
+    if R % g:
+        pytest.skip("group size must divide R")
+    x = synth.draw("grads", shape, 2000 + R + C)
+    for m in (1, 2, 4, 6, 8):
+        for mode in MODES:
+            announce("quantize cols %dx%d g=%d m=%d %s" % (R, C, g, m, mode))
+            t, q_o, _ = check_quantize(x, 0, g, m, mode, seed=5)
+            # the same bytes as quantizing the transposed copy along rows
+            t2, _ = gpu_quantize(np.ascontiguousarray(x.T), -1, g, m, mode, seed=5)
+            assert torch.equal(t.mant, t2.mant) and torch.equal(t.exp, t2.exp)
+
+
+def test_special_values():
+    x = synth.special_values(64 * 256, seed=3).reshape(64, 256)
+    for m in range(1, 9):
+        for mode in MODES:
+            announce("quantize special values m=%d %s" % (m, mode))
+            check_quantize(x, -1, 16, m, mode, seed=11)
+            check_quantize(np.ascontiguousarray(x.T), 0, 16, m, mode, seed=11)
+
+
+def test_nonfinite_sets_status():
+    x = synth.draw("normal", (8, 64), 1)
+    x[3, 17] = np.inf
+    announce("quantize with an Inf input")
+    _, st = gpu_quantize(x, -1, 16, 4, "nearest")
+    assert st == 1
+    x[3, 17] = np.nan
+    _, st = gpu_quantize(np.ascontiguousarray(x.T), 0, 16, 4, "nearest")
+    assert st == 1
+
+
+def test_empty_inputs():
+    announce("quantize empty tensors")
+    t, st = gpu_quantize(np.zeros((0, 64), np.float32), -1, 16, 4, "nearest")
+    assert t.rows == 0 and st == 0
+    y = fb.dequantize(t)
+    assert y.shape == (0, 64)
+
+
+@pytest.mark.parametrize("m", [1, 2, 4, 5, 8])
+def test_dequantize_matches_oracle(m):
+    x = synth.draw("grads", (33, 512), 7)
+    announce("dequantize m=%d" % m)
+    t, _ = gpu_quantize(x, -1, 16, m, "stochastic", seed=9)
+    y = fb.dequantize(t).cpu().numpy().astype(np.float64)
+    q_o, E_o, _ = oracle.quantize(x, g=16, m=m, mode="stochastic", seed=9)
+    assert np.array_equal(y, oracle.dequantize(q_o, E_o, 16, m))
+
+
+@pytest.mark.parametrize("dist,seed", [("half_normal", 21), ("weights", 22), ("grads", 23)])
+def test_full_size_sweep(dist, seed):
+    """The 64M-element quantize sweep (8192 x 8192, g=16 along the last axis):
+    m in {2,4,6,8}, nearest and stochastic (Philox seed 1234); full parity for
+    one mode per m, the other on a 1024-row slice."""
+    x = synth.draw(dist, (8192, 8192), seed)
+    for m in (2, 4, 6, 8):
+        for mode in ("nearest", "stochastic"):
+            full = (mode == "nearest") == (m % 4 == 0)
+            rows = None if full else (8192 - 1024, 8192)
+            announce("quantize 8192x8192 %s m=%d %s rows=%s" % (dist, m, mode, rows))
+            check_quantize(x, -1, 16, m, mode, seed=1234, rows=rows)
+
+
+def test_stochastic_unbiased_over_1000_seeds():
+    """First 4096 values of the gradient tensor, Philox seeds 1234..2233.  For
+    each value the exact expectation of the magnitude is the average over all
+    256 noise bytes (taken from the oracle); the GPU's average over 1000 seeds
+    must match it within sampling error (per-value and pooled z scores)."""
+    x = synth.draw("grads", (8192, 8192), 23)[:1, :4096].copy()
+    m = 2
+    announce("SR unbiasedness, 1000 seeds, 4096 values")
+    xt = torch.from_numpy(x).cuda()
+    out = fb.BFPTensor.empty(1, 4096, 16, m, "cuda")
+    acc = torch.zeros(4096, dtype=torch.float64)
+    accsq = torch.zeros(4096, dtype=torch.float64)
+    for s in range(1234, 2234):
+        fb.quantize(xt, g=16, m=m, rounding="stochastic", seed=s, out=out)
+        qv = torch.from_numpy(bfp_codec.decode(out.mant.cpu().numpy(), 1, 4096, m).astype(np.float64))[0]
+        acc += qv.abs()
+        accsq += qv.abs() ** 2
+    mean = (acc / 1000).numpy()
+    # exact expectation per value from the oracle, enumerating the noise byte
+    expect = np.zeros(4096)
+    for G in range(256):
+        grp = x[0, 16 * G:16 * G + 16]
+        tot = np.zeros(16)
+        for u in range(256):
+            qg, _, _ = oracle.quantize_group(grp, m, "stochastic", np.full(16, u))
+            tot += np.abs(qg)
+        expect[16 * G:16 * G + 16] = tot / 256
+    p = expect - np.floor(expect)
+    var = p * (1 - p)
+    live = var > 0
+    z = (mean[live] - expect[live]) / np.sqrt(var[live] / 1000)
+    assert np.all(mean[~live] == expect[~live])
+    assert np.max(np.abs(z)) < 5.5
+    pooled = (mean[live] - expect[live]).sum() / np.sqrt((var[live] / 1000).sum())
+    assert abs(pooled) < 4.0
