@@ -1,0 +1,316 @@
+#!/usr/bin/env python3
+"""Benchmark of the BFP hot path on one MI355X.
+
+A step is one BFP training step of one FFN layer (M = 8192 tokens, 4096 ->
+16384, groups of 16): six quantizations -- X and W for the forward GEMM (W
+regrouped along its rows, i.e. transposed on quantize), dY (stochastic
+rounding) and W for dX = dY . W^T, X and dY regrouped along the token axis for
+dW = X^T . dY -- and the three GEMMs.  The mantissa width follows the schedule
+2 -> 4 -> 6 bits over consecutive steps.  Inputs are resident in HBM before
+timing (three dY tensors rotate with the schedule).
+
+Printed: one JSON line with the step's effective BFP throughput
+(2 M N K summed over the three GEMMs, divided by the step time including the
+quantizations), the roofline of the dominant kernel measured with HIP events
+inside the timed region, per-kernel figures, a sweep of the GEMM over the
+transformer-block shapes and every mantissa pair, the quantize sweep over
+64M-element tensors, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "BFP GEMM effective TOPS per (m_a,m_b) + % int8 MFMA peak; quantize GB/s % HBM"
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+PEAK_FP6_TFLOPS = 10100.0    # dense FP6/FP4 MFMA (the instruction the GEMM issues)
+PEAK_INT8_TOPS = 5000.0      # dense int8 MFMA (the metric's reference)
+M_TOK, D_IN, D_FF, G = 8192, 4096, 16384, 16
+SCHEDULE = (2, 4, 6)
+
+
+def planes(m):
+    return 1 if m <= 4 else 2
+
+
+def q_bytes(n_elems, m, g=G):
+    """Algorithmic HBM bytes of one quantization: read FP32, write the chunk
+    planes (6 bits per value each) and one exponent byte per group."""
+    return n_elems * (4 + 0.75 * planes(m) + 1.0 / g)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=30)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--no-sweeps", action="store_true", help="skip the GEMM and quantize sweeps")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--quiet", action="store_true")
+    return p.parse_args()
+
+
+def log(args, *a):
+    if not args.quiet:
+        print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class Step:
+    """Buffers and launches of one FFN training step."""
+
+    def __init__(self, torch, fb, synth, dev):
+        self.torch, self.fb = torch, fb
+        t0 = time.time()
+        self.X = torch.from_numpy(synth.draw("half_normal", (M_TOK, D_IN), 51)).to(dev)
+        self.W = torch.from_numpy(synth.draw("weights", (D_IN, D_FF), 52)).to(dev)
+        self.dY = [torch.from_numpy(synth.draw("grads", (M_TOK, D_FF), 53 + i)).to(dev) for i in range(3)]
+        self.gen_s = time.time() - t0
+        self.q = {}
+        for m in SCHEDULE:
+            e = fb.BFPTensor.empty
+            self.q[m] = dict(
+                xa=e(M_TOK, D_IN, G, m, dev),      # X grouped along features (fwd A)
+                wb=e(D_FF, D_IN, G, m, dev),       # W regrouped: rows = output features (fwd B)
+                dya=e(M_TOK, D_FF, G, m, dev),     # dY along features (dX A)
+                wk=e(D_IN, D_FF, G, m, dev),       # W along its columns (dX B)
+                xt=e(D_IN, M_TOK, G, m, dev),      # X regrouped along tokens (dW A)
+                dyt=e(D_FF, M_TOK, G, m, dev),     # dY regrouped along tokens (dW B)
+            )
+        self.Y = torch.empty((M_TOK, D_FF), dtype=torch.float32, device=dev)
+        self.dX = torch.empty((M_TOK, D_IN), dtype=torch.float32, device=dev)
+        self.dW = torch.empty((D_IN, D_FF), dtype=torch.float32, device=dev)
+
+    def run(self, s, ev=None):
+        """Enqueue step s.  ev: optional list collecting (name, start, end) events."""
+        fb, torch = self.fb, self.torch
+        m = SCHEDULE[s % 3]
+        b = self.q[m]
+        dy = self.dY[s % 3]
+        seed = 1000 + 2 * s
+
+        def rec(name, fn):
+            if ev is None:
+                fn()
+                return
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            z.record()
+            ev.append((name, m, a, z))
+
+        rec("quantize_rows", lambda: fb.quantize(self.X, g=G, m=m, out=b["xa"]))
+        rec("quantize_cols", lambda: fb.quantize(self.W, group_axis=0, g=G, m=m, out=b["wb"]))
+        rec("gemm", lambda: fb.gemm(b["xa"], b["wb"], out=self.Y))
+        rec("quantize_rows", lambda: fb.quantize(dy, g=G, m=m, rounding="stochastic", seed=seed, out=b["dya"]))
+        rec("quantize_rows", lambda: fb.quantize(self.W, g=G, m=m, out=b["wk"]))
+        rec("gemm", lambda: fb.gemm(b["dya"], b["wk"], out=self.dX))
+        rec("quantize_cols", lambda: fb.quantize(self.X, group_axis=0, g=G, m=m, out=b["xt"]))
+        rec("quantize_cols", lambda: fb.quantize(dy, group_axis=0, g=G, m=m, rounding="stochastic", seed=seed + 1,
+                                                 out=b["dyt"]))
+        rec("gemm", lambda: fb.gemm(b["xt"], b["dyt"], out=self.dW))
+
+
+STEP_OPS = 3 * 2.0 * M_TOK * D_FF * D_IN
+GEMM_OPS = 2.0 * M_TOK * D_FF * D_IN  # every one of the three GEMMs has M*N*K = 8192*16384*4096
+
+
+def gemm_sweep(torch, fb, synth, dev, args):
+    """Transformer-block GEMMs at every mantissa pair (effective TOPS)."""
+    shapes = {"qkv": (8192, 12288, 4096), "out_proj": (8192, 4096, 4096), "ffn_up": (8192, 16384, 4096),
+              "ffn_down": (8192, 4096, 16384)}
+    pairs = [(2, 2), (2, 4), (4, 4), (4, 6), (6, 8), (8, 8)]
+    X = torch.from_numpy(synth.bf16_round(synth.draw("normal", (8192, 16384), 41))).to(dev)
+    Wt = torch.from_numpy(synth.bf16_round(synth.draw("weights", (16384, 16384), 42))).to(dev)
+    out = {}
+    for name, (M, N, K) in shapes.items():
+        xa = X[:M, :K].contiguous()
+        wb = Wt[:N, :K].contiguous()
+        C = torch.empty((M, N), dtype=torch.float32, device=dev)
+        for pa, pb in pairs:
+            A = fb.quantize(xa, g=G, m=pa)
+            B = fb.quantize(wb, g=G, m=pb)
+            fb.gemm(A, B, out=C)
+            torch.cuda.synchronize()
+            reps = 5
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fb.gemm(A, B, out=C)
+            z.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(z) / reps
+            tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+            issued = tops * planes(pa) * planes(pb) * 2  # zero-padded half blocks, chunk passes
+            out["%s(%d,%d)" % (name, pa, pb)] = {
+                "M": M, "N": N, "K": K, "ms": round(ms, 4), "eff_tops": round(tops, 1),
+                "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4),
+                "mfma_issued_tflops": round(issued, 1), "frac_fp6_peak_issued": round(issued / PEAK_FP6_TFLOPS, 4)}
+            log(args, "gemm %s (%d,%d): %.3f ms, %.0f eff TOPS" % (name, pa, pb, ms, tops))
+        del C
+    del X, Wt
+    return out
+
+
+def quantize_sweep(torch, fb, synth, dev, args):
+    """64M-element quantize (8192 x 8192, g=16, last axis), three distributions
+    rotated so that consecutive launches read different 256 MB buffers."""
+    xs = [torch.from_numpy(synth.draw(d, (8192, 8192), s)).to(dev)
+          for d, s in (("half_normal", 21), ("weights", 22), ("grads", 23))]
+    out = {}
+    n = 8192 * 8192
+    for m in (2, 4, 6, 8):
+        for mode in ("nearest", "stochastic"):
+            outs = [fb.BFPTensor.empty(8192, 8192, G, m, dev) for _ in range(3)]
+            for i in range(3):
+                fb.quantize(xs[i], g=G, m=m, rounding=mode, seed=1234, out=outs[i])
+            torch.cuda.synchronize()
+            reps = 12
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for r in range(reps):
+                fb.quantize(xs[r % 3], g=G, m=m, rounding=mode, seed=1234, out=outs[r % 3])
+            z.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(z) / reps
+            gbs = q_bytes(n, m) / (ms * 1e-3) / 1e9
+            out["m%d_%s" % (m, mode)] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
+                                         "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+            log(args, "quantize m=%d %s: %.1f us, %.0f GB/s" % (m, mode, ms * 1e3, gbs))
+            del outs
+    del xs
+    return out
+
+
+def cpu_baseline(args):
+    """The oracle, untuned, on the host cores: every quantization of one m=4
+    step in full, plus the first 32 output rows of each GEMM; the GEMM time is
+    scaled to all rows and the step rate reported in the bench's unit."""
+    import numpy as np
+    import oracle
+    from paper_2110_15456_amd import synth
+    threads = max(1, min(os.cpu_count() or 1, 64))
+    X = synth.draw("half_normal", (M_TOK, D_IN), 51)
+    W = synth.draw("weights", (D_IN, D_FF), 52)
+    dY = synth.draw("grads", (M_TOK, D_FF), 53)
+    m = 4
+    t0 = time.time()
+    xa = oracle.quantize(X, axis=-1, g=G, m=m, threads=threads)
+    wb = oracle.quantize(W, axis=0, g=G, m=m, threads=threads)
+    dya = oracle.quantize(dY, axis=-1, g=G, m=m, mode="stochastic", seed=1000, threads=threads)
+    wk = oracle.quantize(W, axis=-1, g=G, m=m, threads=threads)
+    xt = oracle.quantize(X, axis=0, g=G, m=m, threads=threads)
+    dyt = oracle.quantize(dY, axis=0, g=G, m=m, mode="stochastic", seed=1001, threads=threads)
+    tq = time.time() - t0
+    rows = np.arange(32)
+    t1 = time.time()
+    oracle.gemm(xa[0], xa[1], m, wb[0], wb[1], m, g=G, rows=rows, threads=threads)
+    oracle.gemm(dya[0], dya[1], m, wk[0], wk[1], m, g=G, rows=rows, threads=threads)
+    oracle.gemm(xt[0], xt[1], m, dyt[0], dyt[1], m, g=G, rows=rows, threads=threads)
+    tg = time.time() - t1
+    # rows sampled: 32 of 8192 (fwd, dX) and 32 of 4096 (dW)
+    full_gemm_s = tg / 3 * (M_TOK / 32 + M_TOK / 32 + D_IN / 32)
+    step_s = tq + full_gemm_s
+    return {"value": round(STEP_OPS / step_s / 1e12, 6), "unit": "TOPS", "cores": threads, "kind": "oracle",
+            "sample": ("one m=4 FFN step: all six quantizations in full (%.1f s) and the first 32 output rows of "
+                       "each GEMM (%.1f s), GEMM time scaled by rows to the full step (est. %.0f s per step)"
+                       % (tq, tg, step_s)),
+            "cpu_seconds": round(tq + tg, 1)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (--gpus %d requested)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2110_15456_amd as fb
+    from paper_2110_15456_amd import synth
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    fb._lib.load()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    step = Step(torch, fb, synth, dev)
+    log(args, "inputs generated in %.1f s" % step.gen_s)
+    for s in range(args.warmup):
+        step.run(s)
+    torch.cuda.synchronize()
+
+    events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for s in range(args.steps):
+        step.run(args.warmup + s, events)
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+    value = STEP_OPS / (ms_step * 1e-3) / 1e12
+
+    # per-kernel table from the events recorded inside the timed region
+    table = {}
+    sizes = [M_TOK * D_IN, D_IN * D_FF, 0, M_TOK * D_FF, D_IN * D_FF, 0, M_TOK * D_IN, M_TOK * D_FF, 0]
+    for i, (name, m, a, z) in enumerate(events):
+        k = i % 9
+        r = table.setdefault("%s_m%d" % (name, m), {"launches": 0, "ms": 0.0, "work": 0.0})
+        r["launches"] += 1
+        r["ms"] += a.elapsed_time(z)
+        r["work"] += GEMM_OPS if name == "gemm" else q_bytes(sizes[k], m)
+    kernels = {}
+    for key, r in table.items():
+        avg = r["ms"] / r["launches"]
+        per = r["work"] / r["launches"]
+        if key.startswith("gemm"):
+            ach = per / (avg * 1e-3) / 1e12
+            kernels[key] = {"launches": r["launches"], "avg_ms": round(avg, 4), "achieved": round(ach, 1),
+                            "unit": "TFLOP/s", "share": 0.0}
+        else:
+            ach = per / (avg * 1e-3) / 1e9
+            kernels[key] = {"launches": r["launches"], "avg_ms": round(avg, 4), "achieved": round(ach, 1),
+                            "unit": "GB/s", "frac_hbm": round(ach / PEAK_HBM_GBS, 4), "share": 0.0}
+    total = sum(r["ms"] for r in table.values())
+    for key, r in table.items():
+        kernels[key]["share"] = round(r["ms"] / total, 4)
+    dom = max(table, key=lambda k: table[k]["ms"])
+    d = kernels[dom]
+    if dom.startswith("gemm"):
+        roof = {"bound": "mfma", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_FP6_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(d["achieved"] / PEAK_FP6_TFLOPS, 4), "traffic": None,
+                "work_per_launch": "2*M*N*K = %.4g FLOP (BFP MACs, algorithmic)" % GEMM_OPS}
+    else:
+        roof = {"bound": "hbm", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(d["achieved"] / PEAK_HBM_GBS, 4), "traffic": None}
+    log(args, "step %.3f ms, %.1f eff TOPS, wall %.2f s" % (ms_step, value, wall))
+
+    result = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp6", "data": "synthetic",
+        "config": {"workload": "BFP FFN training step: tokens 8192, 4096->16384, g=16, fwd+dX+dW GEMMs with six "
+                               "quantizations (two regrouped along tokens, SR on dY), mantissa schedule 2->4->6",
+                   "M": M_TOK, "d_in": D_IN, "d_ff": D_FF, "g": G, "schedule": list(SCHEDULE)},
+        "roofline": roof, "kernels": kernels,
+    }
+    del step
+    torch.cuda.empty_cache()
+    if not args.no_sweeps:
+        result["gemm_sweep"] = gemm_sweep(torch, fb, synth, dev, args)
+        torch.cuda.empty_cache()
+        result["quantize_sweep"] = quantize_sweep(torch, fb, synth, dev, args)
+    if not args.no_cpu:
+        log(args, "timing the CPU oracle on a sample ...")
+        result["cpu_baseline"] = cpu_baseline(args)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
