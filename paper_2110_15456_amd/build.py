@@ -20,6 +20,9 @@ LIB = os.path.join(HERE, "libfastbfp.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 SOURCES = ["quantize.hip", "gemm_mx.hip", "gemm_i8.hip", "api.cpp"]
+# Per-source extra flags: the quantizer aligns values with ldexp and relies on
+# FP32 denormal flushing to read subnormal inputs as zero.
+SOURCE_FLAGS = {"quantize.hip": ["-fgpu-flush-denormals-to-zero"]}
 HIPFLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
     # CDNA packed-FP32 instructions stay off: ordinary float code only.
@@ -41,23 +44,27 @@ def _torch_lib_dir() -> str | None:
     return None
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [os.path.join(ROCM, "bin", "hipcc"), *HIPFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, build_dir: str = BUILD, defines=()) -> str:
+    obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
+    cmd = [os.path.join(ROCM, "bin", "hipcc"), *HIPFLAGS, *SOURCE_FLAGS.get(src, []), *["-D" + d for d in defines], "-c",
+           os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), res.stderr))
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libfastbfp.so next to this file."""
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile every source and link the library (default: libfastbfp.so next
+    to this file).  ``defines``: extra preprocessor definitions (NAME=VALUE)
+    that select kernel tile shapes."""
+    build_dir = BUILD if not defines else BUILD + "_" + "_".join(d.replace("=", "") for d in defines)
+    os.makedirs(build_dir, exist_ok=True)
     with ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 1)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        objs = list(ex.map(lambda src: _compile(src, build_dir, defines), SOURCES))
     tlib = _torch_lib_dir()
     rpath = ":".join([p for p in (tlib, os.path.join(ROCM, "lib")) if p])
-    link = [os.path.join(ROCM, "llvm", "bin", "clang++"), "-shared", "-fPIC", "-o", LIB + ".tmp", *objs]
+    link = [os.path.join(ROCM, "llvm", "bin", "clang++"), "-shared", "-fPIC", "-o", out + ".tmp", *objs]
     if tlib:
         link += ["-L" + tlib]
     else:
@@ -66,10 +73,10 @@ def build(verbose: bool = False) -> str:
     res = subprocess.run(link, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (" ".join(link), res.stderr))
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(out + ".tmp", out)
     if verbose:
-        print("built", LIB)
-    return LIB
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":

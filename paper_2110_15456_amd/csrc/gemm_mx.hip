@@ -26,206 +26,368 @@
 // The one remaining constant factor, 2^(4 - m_a - m_b) (the E2M3 halving of
 // both operands and the (m-1) in the LSB), is applied exactly in the epilogue.
 //
-// Tiling: a 256-thread workgroup computes a 128x128 tile of C with four waves
-// of 64x64 (4x4 MFMA tiles of 16x16, 64 FP32 accumulators per lane).  K is
-// walked in slabs of 8 groups (128 values); each slab's codes and exponents
-// are staged global -> registers -> LDS, and the next slab's global loads are
-// in flight while the current slab's MFMAs run.
+// Tiling: a 512-thread workgroup (eight waves in a 2x4 grid, two per SIMD)
+// computes a 256x256 tile of C (smaller along an operand with two chunk
+// planes); each wave holds its B fragments in registers for the slab and
+// streams its A fragments.  K is walked in slabs of 8 groups (128 values).  Slabs are double-buffered in LDS:
+// while the MFMAs of slab s read one buffer, the global loads of slab s+1 are
+// in flight into registers and are written to the other buffer afterwards, so
+// each slab costs one barrier.  Workgroups are ordered so that the tiles that
+// share an A row panel run on the same XCD (each XCD has its own L2).
 #include "bfp_device.h"
 #include "launch.h"
 
 namespace fastbfp {
 
 namespace mx {
-constexpr int BM = 128, BN = 128;
-constexpr int KG = 8;            // groups per K slab
-constexpr int ROWB = KG * 12;    // code bytes per row per plane per slab
-constexpr int PITCH = 112;       // LDS row pitch: conflict-free 8-byte reads
-constexpr int NT = 256;          // threads per workgroup
+#ifndef FASTBFP_MX_WGM
+#define FASTBFP_MX_WGM 2
+#endif
+#ifndef FASTBFP_MX_WGN
+#define FASTBFP_MX_WGN 2
+#endif
+#ifndef FASTBFP_MX_BM
+#define FASTBFP_MX_BM 256
+#endif
+#ifndef FASTBFP_MX_BN
+#define FASTBFP_MX_BN 256
+#endif
+constexpr int WGM = FASTBFP_MX_WGM, WGN = FASTBFP_MX_WGN;  // wave grid along M and N
+constexpr int NT = 64 * WGM * WGN;                        // threads per workgroup
+// A rows in LDS: each group in a 16-byte slot, the even group of a pair as
+// [c0 c1 c2 0] and the odd one as [0 c0 c1 c2] (dwords), so that the two
+// halves of the zero-padded MFMA operand are single aligned 16-byte reads.
+// Pitch = 32 B per pair + 16: the 16-byte reads of 16 consecutive rows then
+// hit 64 distinct banks.
+// B rows in LDS: the 24 code bytes of a pair back to back (one 6-dword
+// operand); pitch 24 B per pair + 16 keeps its 8-byte reads conflict-free.
+template <int BM_, int BN_, int KG_>
+struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, KG = KG_;
+  static constexpr int PAIRS = KG / 2;                 // group pairs per row per slab
+  static constexpr int WM = BM / WGM, WN = BN / WGN;   // wave tile
+  static constexpr int TM = WM / 16, TN = WN / 16;     // 16x16 MFMA tiles per wave
+  static constexpr int PITCH_A = PAIRS * 32 + 16;
+  static constexpr int PITCH_B = PAIRS * 24 + 16;
+  static constexpr int PLANE_A = BM * PITCH_A;
+  static constexpr int PLANE_B = BN * PITCH_B;
+  static constexpr int EXP_A = BM * KG, EXP_B = BN * KG;
+  static constexpr int stage_bytes(int na, int nb) { return na * PLANE_A + nb * PLANE_B + EXP_A + EXP_B; }
+  static constexpr int A_PAIRS_PER_T = BM * PAIRS / NT;  // pairs each thread stages per plane per slab
+  static constexpr int B_PAIRS_PER_T = BN * PAIRS / NT;
+  static_assert(A_PAIRS_PER_T * NT == BM * PAIRS && B_PAIRS_PER_T * NT == BN * PAIRS,
+                "every thread stages the same whole number of group pairs");
+  static_assert(TM >= 1 && TN >= 1 && TM * 16 * WGM == BM && TN * 16 * WGN == BN, "wave tiles cover the tile");
+};
 }  // namespace mx
 
-// Staging registers for one operand tile of one slab.
-template <int NP, int VEC>
-struct TileRegs {
-  static constexpr int CHUNKS = mx::BM * mx::ROWB / VEC;  // VEC-byte pieces per plane
-  static constexpr int PER_T = CHUNKS / mx::NT;
-  uint32_t v[NP][PER_T][VEC / 4];
-  uint32_t e;  // 4 exponent bytes
+// Staging registers: PPT group pairs (6 dwords each) per plane.
+template <int NP, int PPT>
+struct PairRegs {
+  uint32_t v[NP][PPT][6];
 };
 
-// Load one slab of a 128-row operand tile: codes of planes [0, NP) and the
-// exponents, zero-filled past row_end / past the last group.
-template <int NP, int VEC>
-__device__ __forceinline__ void load_tile(TileRegs<NP, VEC>& r, const uint8_t* __restrict__ mant,
-                                          const uint8_t* __restrict__ exps, int64_t plane_stride, int row0,
-                                          int row_end, int ng, int slab, int tid) {
-  constexpr int PIECES_PER_ROW = mx::ROWB / VEC;
-  const int gvalid = min(mx::KG, ng - slab * mx::KG);
-  const int bvalid = gvalid * 12;
+// Global -> registers for one slab of an operand tile (PAIRS pairs per row).
+// Pair index id = tid + u*NT covers row id / PAIRS, pair id % PAIRS.
+// Out-of-range pairs (past the last row or group) read a valid address
+// instead, so no lane branches around a load and nothing waits on a load
+// before the stores.  Their codes are never zeroed: rows past M (or N) only
+// feed outputs that are not stored, and groups past K carry exponent 0 on
+// both sides, so their block scale 2^-254 takes any FP6 product (at most 2^11
+// per block) below the smallest FP32 subnormal, i.e. to zero.
+// VEC: 8 -> three 8-byte loads per pair (ng even, so rows are 8-byte aligned
+// and groups come in whole pairs), 4 -> six 4-byte loads, the odd group's
+// clamped to the pair start when it does not exist.
+template <int NP, int PPT, int PAIRS, int KG, int VEC>
+__device__ __forceinline__ void load_pairs(PairRegs<NP, PPT>& r, const uint8_t* __restrict__ mant,
+                                           int64_t plane_stride, int row0, int row_end, int ng, int slab, int tid) {
+  const int gvalid = ng - slab * KG;  // groups left in this row from the slab start
   const int64_t row_bytes = (int64_t)ng * 12;
 #pragma unroll
-  for (int u = 0; u < TileRegs<NP, VEC>::PER_T; ++u) {
+  for (int u = 0; u < PPT; ++u) {
     const int id = tid + u * mx::NT;
-    const int row = id / PIECES_PER_ROW, part = id % PIECES_PER_ROW;
-    const bool ok = (row0 + row < row_end) && (part * VEC < bvalid);
-    const int64_t off = (int64_t)(row0 + row) * row_bytes + slab * mx::ROWB + part * VEC;
+    const int row = id / PAIRS, pr = id % PAIRS;
+    const bool rok = row0 + row < row_end;
+    const bool g0 = rok && 2 * pr < gvalid, g1 = rok && 2 * pr + 1 < gvalid;
+    const int64_t off = g0 ? (int64_t)(row0 + row) * row_bytes + (slab * KG + 2 * pr) * 12 : 0;
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-      if (VEC == 16) {
-        uint4 x = make_uint4(0, 0, 0, 0);
-        if (ok) x = *reinterpret_cast<const uint4*>(mant + p * plane_stride + off);
-        r.v[p][u][0] = x.x;
-        r.v[p][u][1] = x.y;
-        r.v[p][u][2] = x.z;
-        r.v[p][u][3] = x.w;
+      const uint8_t* src = mant + p * plane_stride + off;
+      if (VEC == 8) {
+        const uint2 x0 = *reinterpret_cast<const uint2*>(src);
+        const uint2 x1 = *reinterpret_cast<const uint2*>(src + 8);
+        const uint2 x2 = *reinterpret_cast<const uint2*>(src + 16);
+        r.v[p][u][0] = x0.x; r.v[p][u][1] = x0.y; r.v[p][u][2] = x1.x;
+        r.v[p][u][3] = x1.y; r.v[p][u][4] = x2.x; r.v[p][u][5] = x2.y;
       } else {
-        r.v[p][u][0] = ok ? *reinterpret_cast<const uint32_t*>(mant + p * plane_stride + off) : 0u;
-      }
-    }
-  }
-  // Exponents: 128 rows x 8 groups = 1024 bytes, 4 per thread.
-  {
-    const int row = tid >> 1, j0 = (tid & 1) * 4;
-    uint32_t e = 0;
-    if (row0 + row < row_end) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int gidx = slab * mx::KG + j0 + j;
-        if (j0 + j < gvalid) e |= (uint32_t)exps[(int64_t)(row0 + row) * ng + gidx] << (8 * j);
+        for (int k = 0; k < 6; ++k)
+          r.v[p][u][k] = *reinterpret_cast<const uint32_t*>(src + ((k < 3 || g1) ? 4 * k : 0));
       }
     }
-    r.e = e;
   }
 }
 
-template <int NP, int VEC>
-__device__ __forceinline__ void store_tile(const TileRegs<NP, VEC>& r, uint8_t* sm, uint8_t* se, int tid) {
-  constexpr int PIECES_PER_ROW = mx::ROWB / VEC;
+template <int NP, int PPT, int PAIRS, int PITCH, int PLANE>
+__device__ __forceinline__ void store_pairs_a(const PairRegs<NP, PPT>& r, uint8_t* sm, int tid) {
 #pragma unroll
-  for (int u = 0; u < TileRegs<NP, VEC>::PER_T; ++u) {
+  for (int u = 0; u < PPT; ++u) {
     const int id = tid + u * mx::NT;
-    const int row = id / PIECES_PER_ROW, part = id % PIECES_PER_ROW;
+    const int row = id / PAIRS, pr = id % PAIRS;
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-      uint8_t* dst = sm + p * (mx::BM * mx::PITCH) + row * mx::PITCH + part * VEC;
-      if (VEC == 16)
-        *reinterpret_cast<uint4*>(dst) = make_uint4(r.v[p][u][0], r.v[p][u][1], r.v[p][u][2], r.v[p][u][3]);
-      else
-        *reinterpret_cast<uint32_t*>(dst) = r.v[p][u][0];
+      uint8_t* dst = sm + p * PLANE + row * PITCH + pr * 32;
+      const uint32_t* v = r.v[p][u];
+      *reinterpret_cast<u32x4*>(dst) = u32x4{v[0], v[1], v[2], 0u};
+      *reinterpret_cast<u32x4*>(dst + 16) = u32x4{0u, v[3], v[4], v[5]};
     }
   }
-  *reinterpret_cast<uint32_t*>(se + (tid >> 1) * mx::KG + (tid & 1) * 4) = r.e;
 }
 
-// 24 code bytes (groups 2b and 2b+1 of one row) as six dwords.
-__device__ __forceinline__ void read_frag(const uint8_t* p, uint32_t (&d)[6]) {
-  const uint2 x0 = *reinterpret_cast<const uint2*>(p);
-  const uint2 x1 = *reinterpret_cast<const uint2*>(p + 8);
-  const uint2 x2 = *reinterpret_cast<const uint2*>(p + 16);
-  d[0] = x0.x; d[1] = x0.y; d[2] = x1.x; d[3] = x1.y; d[4] = x2.x; d[5] = x2.y;
+template <int NP, int PPT, int PAIRS, int PITCH, int PLANE>
+__device__ __forceinline__ void store_pairs_b(const PairRegs<NP, PPT>& r, uint8_t* sm, int tid) {
+#pragma unroll
+  for (int u = 0; u < PPT; ++u) {
+    const int id = tid + u * mx::NT;
+    const int row = id / PAIRS, pr = id % PAIRS;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      uint8_t* dst = sm + p * PLANE + row * PITCH + pr * 24;
+      const uint32_t* v = r.v[p][u];
+      *reinterpret_cast<uint2*>(dst) = make_uint2(v[0], v[1]);
+      *reinterpret_cast<uint2*>(dst + 8) = make_uint2(v[2], v[3]);
+      *reinterpret_cast<uint2*>(dst + 16) = make_uint2(v[4], v[5]);
+    }
+  }
 }
 
-template <int NA, int NB, int VEC>
-__global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
+// Exponents of one slab for one row (KG bytes, KG = 8).  EXP_FULL:
+// every slab is full and the rows are KG-byte aligned, so one load; otherwise
+// byte loads with a clamp and zeros past the last group.
+template <int KG, bool EXP_FULL>
+__device__ __forceinline__ uint2 load_exps(const uint8_t* __restrict__ exps, int row, int row_end, int ng, int slab) {
+  const bool rok = row < row_end;
+  const int64_t base = (int64_t)(rok ? row : 0) * ng + slab * KG;
+  static_assert(KG == 8, "one slab's exponents are one 8-byte word");
+  if (EXP_FULL) {
+    // rows past the end only feed outputs that are not stored
+    return *reinterpret_cast<const uint2*>(exps + base);
+  } else {
+    const int gvalid = min(KG, ng - slab * KG);
+    uint32_t w[2] = {0u, 0u};
+#pragma unroll
+    for (int j = 0; j < KG; ++j) {
+      const uint32_t b = exps[base + min(j, gvalid - 1)];
+      w[j >> 2] |= ((rok && j < gvalid) ? b : 0u) << (8 * (j & 3));
+    }
+    return make_uint2(w[0], w[1]);
+  }
+}
+
+// Workgroup id -> (tile_m, tile_n).  Dispatch places consecutive workgroup ids
+// on consecutive XCDs; the remap gives each XCD a contiguous run of logical
+// tiles, and logical tiles are walked in column-major groups of GROUP_M tile
+// rows so that concurrently running workgroups share A and B panels in L2.
+__device__ __forceinline__ void tile_of(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
+  constexpr int NXCD = 8, GROUP_M = 8;
+  int lid = bid;
+  if (nblocks % NXCD == 0) lid = (bid % NXCD) * (nblocks / NXCD) + bid / NXCD;
+  const int per_group = GROUP_M * tiles_n;
+  const int grp = lid / per_group;
+  const int first_m = grp * GROUP_M;
+  const int rows_in_group = min(tiles_m - first_m, GROUP_M);
+  const int in = lid % per_group;
+  tm = first_m + in % rows_in_group;
+  tn = in / rows_in_group;
+}
+
+template <class CF, int NA, int NB, int VEC, bool EXP_FULL>
+__global__ __launch_bounds__(mx::NT) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
                                                  int64_t a_plane_stride, const uint8_t* __restrict__ b_mant,
                                                  const uint8_t* __restrict__ b_exp, int64_t b_plane_stride, int M,
                                                  int N, int ng, float scale, float* __restrict__ C, int64_t ldc,
-                                                 int tiles_n) {
-  __shared__ __attribute__((aligned(16))) uint8_t sA[NA * mx::BM * mx::PITCH];
-  __shared__ __attribute__((aligned(16))) uint8_t sB[NB * mx::BN * mx::PITCH];
-  __shared__ __attribute__((aligned(16))) uint8_t sEA[mx::BM * mx::KG];
-  __shared__ __attribute__((aligned(16))) uint8_t sEB[mx::BN * mx::KG];
-
+                                                 int tiles_m, int tiles_n) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  constexpr int KG = CF::KG, TM = CF::TM, TN = CF::TN;
+  constexpr int STAGE = CF::stage_bytes(NA, NB);
+  constexpr int OFF_B = NA * CF::PLANE_A;
+  constexpr int OFF_EA = OFF_B + NB * CF::PLANE_B;
+  constexpr int OFF_EB = OFF_EA + CF::EXP_A;
   const int tid = threadIdx.x;
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
-  const int row0 = tm * mx::BM, col0 = tn * mx::BN;
+  int tm, tn;
+  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  const int row0 = tm * CF::BM, col0 = tn * CF::BN;
   const int wave = tid >> 6, lane = tid & 63;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / mx::WGN, wc = wave % mx::WGN;
   const int lr = lane & 15, lb = lane >> 4;
 
-  v4f acc[4][4];
+  v4f acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  const int nslabs = (ng + mx::KG - 1) / mx::KG;
-  TileRegs<NA, VEC> ra;
-  TileRegs<NB, VEC> rb;
-  load_tile<NA, VEC>(ra, a_mant, a_exp, a_plane_stride, row0, M, ng, 0, tid);
-  load_tile<NB, VEC>(rb, b_mant, b_exp, b_plane_stride, col0, N, ng, 0, tid);
+  const int nslabs = (ng + KG - 1) / KG;
+  PairRegs<NA, CF::A_PAIRS_PER_T> ra;
+  PairRegs<NB, CF::B_PAIRS_PER_T> rb;
+  // Exponent staging: rows 0..BM-1 are A's, BM..BM+BN-1 are B's; thread t
+  // handles rows t, t + NT, ... (EPT of them).
+  constexpr int EPT = (CF::BM + CF::BN + mx::NT - 1) / mx::NT;
+  static_assert((CF::BM + CF::BN) % 64 == 0, "whole waves skip the rows past BM + BN");
+  auto exp_row_info = [&](int k, const uint8_t*& src, int& grow, int& gend, int& lds) {
+    const int r = tid + k * mx::NT;
+    const bool is_a = r < CF::BM;
+    const int rr = is_a ? r : r - CF::BM;
+    src = is_a ? a_exp : b_exp;
+    grow = (is_a ? row0 : col0) + rr;
+    gend = is_a ? M : N;
+    lds = (is_a ? OFF_EA : OFF_EB) + rr * KG;
+  };
+
+  auto stage_in = [&](uint8_t* dst, const uint2 (&e)[EPT]) {
+    store_pairs_a<NA, CF::A_PAIRS_PER_T, CF::PAIRS, CF::PITCH_A, CF::PLANE_A>(ra, dst, tid);
+    store_pairs_b<NB, CF::B_PAIRS_PER_T, CF::PAIRS, CF::PITCH_B, CF::PLANE_B>(rb, dst + OFF_B, tid);
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      if (tid + k * mx::NT >= CF::BM + CF::BN) break;
+      const uint8_t* src;
+      int grow, gend, lds;
+      exp_row_info(k, src, grow, gend, lds);
+      *reinterpret_cast<uint2*>(dst + lds) = e[k];
+    }
+  };
+  auto fetch = [&](int slab, uint2 (&e)[EPT]) {
+    load_pairs<NA, CF::A_PAIRS_PER_T, CF::PAIRS, KG, VEC>(ra, a_mant, a_plane_stride, row0, M, ng, slab, tid);
+    load_pairs<NB, CF::B_PAIRS_PER_T, CF::PAIRS, KG, VEC>(rb, b_mant, b_plane_stride, col0, N, ng, slab, tid);
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      e[k] = make_uint2(0u, 0u);
+      if (tid + k * mx::NT >= CF::BM + CF::BN) break;
+      const uint8_t* src;
+      int grow, gend, lds;
+      exp_row_info(k, src, grow, gend, lds);
+      e[k] = load_exps<KG, EXP_FULL>(src, grow, gend, ng, slab);
+    }
+  };
+
+  if (nslabs > 0) {
+    uint2 e0[EPT];
+    fetch(0, e0);
+    stage_in(smem, e0);
+  }
+  __syncthreads();
 
   for (int s = 0; s < nslabs; ++s) {
-    store_tile<NA, VEC>(ra, sA, sEA, tid);
-    store_tile<NB, VEC>(rb, sB, sEB, tid);
-    __syncthreads();
-    if (s + 1 < nslabs) {
-      load_tile<NA, VEC>(ra, a_mant, a_exp, a_plane_stride, row0, M, ng, s + 1, tid);
-      load_tile<NB, VEC>(rb, b_mant, b_exp, b_plane_stride, col0, N, ng, s + 1, tid);
-    }
+    const uint8_t* cur = smem + (s & 1) * STAGE;
+    uint8_t* nxt = smem + ((s + 1) & 1) * STAGE;
+    // Next slab's global loads (the last slab re-reads itself: harmless, unused),
+    // issued before this slab's MFMAs.
+    uint2 e_next[EPT];
+    fetch(min(s + 1, nslabs - 1), e_next);
+    __builtin_amdgcn_sched_barrier(0);
+
 #pragma unroll
-    for (int ca = 0; ca < NA; ++ca) {
-      // A fragments of this wave's four 16-row tiles, with their exponent pairs.
-      uint32_t af[4][6];
-      int ea[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int rl = wr * 64 + i * 16 + lr;
-        read_frag(sA + ca * (mx::BM * mx::PITCH) + rl * mx::PITCH + lb * 24, af[i]);
-        // +4 per chunk of significance, applied to both packed exponent bytes
-        // (no carry: E <= 250).
-        ea[i] = (int)*reinterpret_cast<const uint16_t*>(sEA + rl * mx::KG + 2 * lb) + 0x0404 * (NA - 1 - ca);
-      }
+    for (int kp = 0; kp < CF::PAIRS / 4; ++kp) {  // MFMA K-steps: 4 group pairs each (one per lane block)
+      static_assert(CF::PAIRS % 4 == 0, "a slab is a whole number of MFMA K-steps");
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
+        // This wave's TN B fragments stay in registers across the A loop.
+        v8i bv[TN];
+        int eb[TN];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int cl = wc * 64 + j * 16 + lr;
-          uint32_t bf[6];
-          read_frag(sB + cb * (mx::BN * mx::PITCH) + cl * mx::PITCH + lb * 24, bf);
-          const int eb = (int)*reinterpret_cast<const uint16_t*>(sEB + cl * mx::KG + 2 * lb) + 0x0404 * (NB - 1 - cb);
-          const v8i bv = {(int)bf[0], (int)bf[1], (int)bf[2], (int)bf[3], (int)bf[4], (int)bf[5], 0, 0};
+        for (int j = 0; j < TN; ++j) {
+          const int cl = wc * CF::WN + j * 16 + lr;
+          const uint8_t* p = cur + OFF_B + cb * CF::PLANE_B + cl * CF::PITCH_B + (kp * 4 + lb) * 24;
+          const uint2 y0 = *reinterpret_cast<const uint2*>(p);
+          const uint2 y1 = *reinterpret_cast<const uint2*>(p + 8);
+          const uint2 y2 = *reinterpret_cast<const uint2*>(p + 16);
+          bv[j] = v8i{(int)y0.x, (int)y0.y, (int)y1.x, (int)y1.y, (int)y2.x, (int)y2.y, 0, 0};
+          eb[j] = (int)*reinterpret_cast<const uint16_t*>(cur + OFF_EB + cl * KG + 2 * (kp * 4 + lb)) +
+                  0x0404 * (NB - 1 - cb);
+        }
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const v8i a_even = {(int)af[i][0], (int)af[i][1], (int)af[i][2], 0, 0, 0, 0, 0};
-            const v8i a_odd = {0, 0, 0, (int)af[i][3], (int)af[i][4], (int)af[i][5], 0, 0};
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a_even, bv, acc[i][j], 2, 2, 0, ea[i], 0, eb);
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a_odd, bv, acc[i][j], 2, 2, 1, ea[i], 1, eb);
+        for (int ca = 0; ca < NA; ++ca) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int rl = wr * CF::WM + i * 16 + lr;
+            const uint8_t* p = cur + ca * CF::PLANE_A + rl * CF::PITCH_A + (kp * 4 + lb) * 32;
+            const u32x4 e4 = *reinterpret_cast<const u32x4*>(p);       // [c0 c1 c2 0] of the even group
+            const u32x4 o4 = *reinterpret_cast<const u32x4*>(p + 16);  // [0 c0 c1 c2] of the odd group
+            const v8i a_even = {(int)e4[0], (int)e4[1], (int)e4[2], (int)e4[3], 0, 0, 0, 0};
+            const v8i a_odd = {0, 0, (int)o4[0], (int)o4[1], (int)o4[2], (int)o4[3], 0, 0};
+            // +4 per chunk of significance on both packed exponent bytes (E <= 250: no carry)
+            const int ea = (int)*reinterpret_cast<const uint16_t*>(cur + OFF_EA + rl * KG + 2 * (kp * 4 + lb)) +
+                           0x0404 * (NA - 1 - ca);
+            // all even-group MFMAs first, then the odd ones: consecutive MFMAs
+            // write different accumulators and never wait on each other
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a_even, bv[j], acc[i][j], 2, 2, 0, ea, 0,
+                                                                          eb[j]);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a_odd, bv[j], acc[i][j], 2, 2, 1, ea, 1,
+                                                                          eb[j]);
           }
         }
       }
     }
+    // Keep the next slab's LDS writes (which wait for its global loads) after
+    // this slab's MFMAs, so the loads' latency hides behind the math.
+    __builtin_amdgcn_sched_barrier(0);
+    stage_in(nxt, e_next);
     __syncthreads();
   }
 
   // Epilogue: lane holds rows 4*lb + r, column lr of each 16x16 tile.
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = col0 + wc * 64 + j * 16 + lr;
+    for (int j = 0; j < TN; ++j) {
+      const int col = col0 + wc * CF::WN + j * 16 + lr;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = row0 + wr * 64 + i * 16 + lb * 4 + r;
+        const int row = row0 + wr * CF::WM + i * 16 + lb * 4 + r;
         if (row < M && col < N) C[(int64_t)row * ldc + col] = acc[i][j][r] * scale;
       }
     }
+}
+
+template <class CF, int NA, int NB, int VEC, bool EXP_FULL>
+static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
+                              const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
+                              int64_t ldc, hipStream_t s) {
+  const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
+  constexpr int lds = 2 * CF::stage_bytes(NA, NB);
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  auto kern = k_gemm_mx<CF, NA, NB, VEC, EXP_FULL>;
+  static bool attr_set = false;  // benign race: every caller sets the same value
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_m * tiles_n)), dim3(mx::NT), lds, s, a_mant, a_exp, a_ps, b_mant,
+                     b_exp, b_ps, M, N, ng, scale, C, ldc, tiles_m, tiles_n);
+  return hipGetLastError();
 }
 
 template <int NA, int NB>
 static hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
                               const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
                               int64_t ldc, hipStream_t s) {
-  const int tiles_m = (M + mx::BM - 1) / mx::BM, tiles_n = (N + mx::BN - 1) / mx::BN;
-  const dim3 grid((unsigned)(tiles_m * tiles_n));
-  const bool al16 = (reinterpret_cast<uintptr_t>(a_mant) % 16 == 0) && (reinterpret_cast<uintptr_t>(b_mant) % 16 == 0);
-  if (ng % 4 == 0 && al16)  // every row starts 16-byte aligned: 16-byte global loads
-    hipLaunchKernelGGL((k_gemm_mx<NA, NB, 16>), grid, dim3(mx::NT), 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps,
-                       M, N, ng, scale, C, ldc, tiles_n);
-  else
-    hipLaunchKernelGGL((k_gemm_mx<NA, NB, 4>), grid, dim3(mx::NT), 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M,
-                       N, ng, scale, C, ldc, tiles_n);
-  return hipGetLastError();
+  // Slabs of 8 groups (one MFMA K-step); the tile shrinks along an operand
+  // with two chunk planes so that two LDS stages fit in 160 KB.
+  using CF = mx::Cfg<NA == 1 ? FASTBFP_MX_BM : FASTBFP_MX_BM / 2, NB == 1 ? FASTBFP_MX_BN : FASTBFP_MX_BN / 2, 8>;
+  auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
+  // 8-byte code loads need every row (ng * 12 bytes) and both bases 8-byte aligned.
+  const bool v8 = ng % 2 == 0 && al(a_mant, 8) && al(b_mant, 8);
+  // single exponent loads need full slabs and KG-byte aligned exponent rows.
+  const bool ef = ng % CF::KG == 0 && al(a_exp, CF::KG) && al(b_exp, CF::KG);
+  if (v8 && ef) return launch_mx_v<CF, NA, NB, 8, true>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
+  if (v8) return launch_mx_v<CF, NA, NB, 8, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
+  return launch_mx_v<CF, NA, NB, 4, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
 }
 
 hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_planes, int na, const uint8_t* b_mant,

@@ -14,9 +14,29 @@
 
 namespace fastbfp {
 
+// Signed chunk value as the float the FP6 converter takes: +-c * 0.5 (the
+// E2M3 code of c/2), with a zero magnitude as +0.0 so that it packs as code 0.
+// neg_half is -0.5 or +0.5 carrying the sign of the input value.
+__device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
+  return __builtin_fmaf((float)c, neg_half, 0.0f);  // 0 * -0.5 + 0 = +0
+}
+
 // Quantize one group whose FP32 bit patterns are in b[].  Writes the packed
 // chunk planes to w[plane][...] and the shared exponent to E_out; nonfinite is
 // set if any input was Inf/NaN.
+//
+// Alignment is done in floating point, exactly: with the shared exponent E,
+// one LSB is 2^(E-127-(m-1)), so a = |x| / LSB = ldexp(|x|, 127 + (m-1) - E)
+// is a power-of-two scaling of an FP32 value into [0, 2^m) and has no
+// rounding.  Truncating conversions to integer then implement the three
+// rounding rules exactly:
+//   truncate:   q = floor(a)
+//   nearest:    q = (floor(2a) + 1) >> 1           (half an LSB added, ties up)
+//   stochastic: q = (floor(256a) + U) >> 8         (U = the noise byte)
+// Subnormal inputs flush to zero (this file is compiled with FP32 denormal
+// flushing, so ldexp reads them as zero).  Codes are produced by the gfx950
+// FP6 converter, which interleaves its two 16-value inputs: output value 2i is
+// a[i] / scale and 2i+1 is b[i] / scale.
 template <int G, int MODE, int NCH>
 __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
                                                uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
@@ -40,49 +60,53 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
     }
   }
 
+  const uint32_t qmax = (1u << m) - 1u;
+  // (b) the exponent that aligns a value to the group's LSB (times 2 for
+  // nearest, 256 for stochastic rounding).
+  const int align = 127 + (int)m - 1 - (int)E + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
+  typedef float v16f __attribute__((ext_vector_type(16)));
+  v16f ev[NCH][G / 32 + (G % 32 != 0)], od[NCH][G / 32 + (G % 32 != 0)];
 #pragma unroll
   for (int p = 0; p < NCH; ++p)
 #pragma unroll
-    for (int i = 0; i < G * 6 / 32; ++i) w[p][i] = 0u;
-
-  const uint32_t qmax = (1u << m) - 1u;
-  // The value's 24-bit significand S is worth S * 2^(ef-150); one LSB of the
-  // group is 2^(E-127-(m-1)); so the magnitude in LSBs is S >> sh with
-  // sh = E - ef + 24 - m (>= 16 because m <= 8).
-  const uint32_t base = E + 24u - m;
+    for (int h = 0; h < G / 32 + (G % 32 != 0); ++h) {
+      ev[p][h] = v16f{};
+      od[p][h] = v16f{};
+    }
 #pragma unroll
   for (int t = 0; t < G; ++t) {
-    const uint32_t ef = (b[t] >> 23) & 0xFFu;
-    const uint32_t S = ef ? ((b[t] & 0x7FFFFFu) | 0x800000u) : 0u;  // subnormals flush to zero
-    const uint32_t sh = base - ef;
+    const float mag = __builtin_ldexpf(__uint_as_float(b[t] & 0x7FFFFFFFu), align);
+    const uint32_t fl = (uint32_t)mag;  // truncating conversion: floor
     uint32_t q;
     if (MODE == kNearest) {
-      // (c)+(d): add half an LSB, truncate.
-      q = ((S >> min(sh - 1u, 31u)) + 1u) >> 1;
+      q = (fl + 1u) >> 1;
     } else if (MODE == kTruncate) {
-      q = S >> min(sh, 31u);
+      q = fl;
     } else {
-      // (b) keep 8 bits below the LSB, (c) add the noise byte, (d) truncate.
-      const uint32_t u = (noise[t >> 2] >> (8 * (t & 3))) & 0xFFu;
-      q = ((S >> min(sh - 8u, 31u)) + u) >> 8;
+      // (c) add the noise byte below the LSB, (d) truncate.
+      q = (fl + ((noise[t >> 2] >> (8 * (t & 3))) & 0xFFu)) >> 8;
     }
     q = min(q, qmax);  // a group maximum that rounds up to 2^m saturates
-    const uint32_t sbit = (b[t] >> 26) & 0x20u;
-    uint32_t code[NCH];
+    const float nh = __uint_as_float((b[t] & 0x80000000u) | 0x3F000000u);  // +-0.5
+    const int h = t / 32, k = (t % 32) / 2;
     if (NCH == 1) {
-      code[0] = e2m3_half_code(q) | (q ? sbit : 0u);
+      const float f = signed_half(q, nh);
+      if (t % 2 == 0) ev[0][h][k] = f; else od[0][h][k] = f;
     } else {
-      const uint32_t hi = q >> 4, lo = q & 15u;
-      code[0] = e2m3_half_code(hi) | (hi ? sbit : 0u);
-      code[NCH - 1] = e2m3_half_code(lo) | (lo ? sbit : 0u);
-    }
-    const int bit = 6 * t, wi = bit / 32, bs = bit % 32;
-#pragma unroll
-    for (int p = 0; p < NCH; ++p) {
-      w[p][wi] |= code[p] << bs;
-      if (bs > 26) w[p][wi + 1] |= code[p] >> (32 - bs);
+      const float fh = signed_half(q >> 4, nh), fl2 = signed_half(q & 15u, nh);
+      if (t % 2 == 0) { ev[0][h][k] = fh; ev[NCH - 1][h][k] = fl2; }
+      else { od[0][h][k] = fh; od[NCH - 1][h][k] = fl2; }
     }
   }
+  typedef uint32_t v6u __attribute__((ext_vector_type(6)));
+#pragma unroll
+  for (int p = 0; p < NCH; ++p)
+#pragma unroll
+    for (int h = 0; h < G / 32 + (G % 32 != 0); ++h) {
+      const v6u c = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev[p][h], od[p][h], 1.0f);
+#pragma unroll
+      for (int i = 0; i < 6 && 6 * h + i < G * 6 / 32; ++i) w[p][6 * h + i] = c[i];
+    }
 }
 
 template <int G, int NCH>
@@ -97,22 +121,50 @@ __device__ __forceinline__ void store_group(uint8_t* __restrict__ mant, int64_t 
 }
 
 // Groups along the contiguous last axis: group gid covers x[gid*G, gid*G+G).
+// Each wave owns 64 consecutive groups.  Their FP32 values are brought into
+// the wave's LDS region by direct global->LDS 16-byte loads, each of which
+// reads 1 KB contiguous (one lane per 16-byte chunk), and every lane then reads
+// its own group back.  The chunk j of group l lands in 16-byte slot
+// CPG*l + (j ^ swz(l)): the XOR spreads the 16 lanes served together across
+// all 64 banks on the read-back.  (Reading 64 contiguous bytes per lane
+// straight from global memory instead leaves each load instruction touching
+// 64 scattered 16-byte pieces, which costs about a third of HBM bandwidth.)
 template <int G, int MODE, int NCH>
 __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__ x, int64_t ngroups, uint32_t m,
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant,
                                                        uint8_t* __restrict__ exps, uint32_t* status) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (gid >= ngroups) return;
-  uint32_t b[G];
-  const u32x4* src = reinterpret_cast<const u32x4*>(x) + gid * (G / 4);
+  constexpr int CPG = G / 4;             // 16-byte chunks per group
+  constexpr int LANES_PER_SWZ = 16 / CPG;
+  __shared__ __attribute__((aligned(16))) uint32_t stage[4][64 * G];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g0 = ((int64_t)blockIdx.x * 4 + wave) * 64;  // first group of this wave
+  if (g0 >= ngroups) return;
+  const int64_t nvalid = min((int64_t)64, ngroups - g0);
+  typedef __attribute__((address_space(3))) void lds_void;
+  const uint8_t* base = reinterpret_cast<const uint8_t*>(x) + g0 * (G * 4);
 #pragma unroll
-  for (int i = 0; i < G / 4; ++i) {
-    const u32x4 v = __builtin_nontemporal_load(src + i);  // read once: bypass cache retention
-    b[4 * i + 0] = v[0];
-    b[4 * i + 1] = v[1];
-    b[4 * i + 2] = v[2];
-    b[4 * i + 3] = v[3];
+  for (int k = 0; k < CPG; ++k) {
+    const int slot = 64 * k + lane;
+    const int l = slot / CPG;
+    const int j = (slot % CPG) ^ ((l / LANES_PER_SWZ) % CPG);
+    // chunks of groups past the end read the wave's first chunk instead (unused)
+    const int64_t off = (l < nvalid) ? (int64_t)(l * CPG + j) * 16 : 0;
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + off),
+                                     (lds_void*)(&stage[wave][64 * 4 * k]), 16, 0, 0);
   }
+  __builtin_amdgcn_s_waitcnt(0);  // the wave reads back what its own loads wrote
+  if (lane >= nvalid) return;
+  uint32_t b[G];
+#pragma unroll
+  for (int j = 0; j < CPG; ++j) {
+    const int slot = CPG * lane + (j ^ ((lane / LANES_PER_SWZ) % CPG));
+    const u32x4 v = *reinterpret_cast<const u32x4*>(&stage[wave][4 * slot]);
+    b[4 * j + 0] = v[0];
+    b[4 * j + 1] = v[1];
+    b[4 * j + 2] = v[2];
+    b[4 * j + 3] = v[3];
+  }
+  const int64_t gid = g0 + lane;
   uint32_t w[NCH][G * 6 / 32];
   uint32_t E;
   bool nonfinite;
@@ -124,36 +176,65 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
 
 // Groups down the columns of x[R][C] (transpose-on-quantize).  Output row c is
 // column c of x; its group j covers x[j*G .. j*G+G-1][c] and has
-// gid = c * (R/G) + j.  A block is 64 columns x 4 group slots; each thread
-// walks NGT consecutive groups of its column, so its output bytes are
-// contiguous and a wave's loads are 256 contiguous bytes.
+// gid = c * (R/G) + j.  A block takes 64 columns (one per lane: every load
+// instruction reads 256 contiguous bytes of a row of x) and JB = 4 * NGT
+// consecutive group rows (NGT per wave).  The packed codes and exponents of
+// the 64 x JB groups are gathered in LDS and then written row by row, so that
+// every store instruction writes contiguous bytes of one output row.
 template <int G, int MODE, int NCH, int NGT>
 __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__ x, int64_t R, int64_t C,
                                                        int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
                                                        uint8_t* __restrict__ mant, uint8_t* __restrict__ exps,
                                                        uint32_t* status) {
+  constexpr int JB = 4 * NGT;             // group rows per block
+  constexpr int WPG = G * 6 / 32;         // code dwords per group per plane
+  constexpr int ROWW = JB * WPG;          // code dwords per output row per plane in this block
+  __shared__ uint32_t sc[NCH][64][ROWW];
+  __shared__ uint8_t se[64][JB];
   const int64_t bx = blockIdx.x % nbx, by = blockIdx.x / nbx;
-  const int64_t c = bx * 64 + (threadIdx.x & 63);
-  if (c >= C) return;
+  const int lane = threadIdx.x & 63, slot = threadIdx.x >> 6;
+  const int64_t c0 = bx * 64, c = c0 + lane;
   const int64_t gpr = R / G;
-  const int64_t ngroups = C * gpr;
-  const int64_t j0 = (by * 4 + (threadIdx.x >> 6)) * NGT;
+  const int64_t jb = by * JB;
+  const int jn = (int)min((int64_t)JB, gpr - jb);  // group rows this block covers
   bool any_bad = false;
-  for (int i = 0; i < NGT; ++i) {
-    const int64_t j = j0 + i;
-    if (j >= gpr) break;
-    uint32_t b[G];
-    const float* src = x + (j * G) * C + c;
+  if (c < C) {
+    for (int i = 0; i < NGT; ++i) {
+      const int jl = slot * NGT + i;
+      if (jl >= jn) break;
+      const int64_t j = jb + jl;
+      uint32_t b[G];
+      const float* src = x + (j * G) * C + c;
 #pragma unroll
-    for (int t = 0; t < G; ++t) b[t] = __float_as_uint(__builtin_nontemporal_load(src + t * C));
-    uint32_t w[NCH][G * 6 / 32];
-    uint32_t E;
-    bool nonfinite;
-    const int64_t gid = c * gpr + j;
-    quantize_group<G, MODE, NCH>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite);
-    exps[gid] = (uint8_t)E;
-    store_group<G, NCH>(mant, ngroups * (G * 3 / 4), gid, w);
-    any_bad |= nonfinite;
+      for (int t = 0; t < G; ++t) b[t] = __float_as_uint(src[t * C]);
+      uint32_t w[NCH][WPG];
+      uint32_t E;
+      bool nonfinite;
+      quantize_group<G, MODE, NCH>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite);
+#pragma unroll
+      for (int p = 0; p < NCH; ++p)
+#pragma unroll
+        for (int k = 0; k < WPG; ++k) sc[p][lane][jl * WPG + k] = w[p][k];
+      se[lane][jl] = (uint8_t)E;
+      any_bad |= nonfinite;
+    }
+  }
+  __syncthreads();
+  // Write-out: output row c0 + r gets jn groups starting at group jb.
+  const int ncols = (int)min((int64_t)64, C - c0);
+  const int64_t plane_dw = C * gpr * WPG;  // dwords per plane
+  uint32_t* mw = reinterpret_cast<uint32_t*>(mant);
+  for (int d = threadIdx.x; d < ncols * ROWW; d += 256) {
+    const int r = d / ROWW, k = d % ROWW;
+    if (k < jn * WPG) {
+      const int64_t o = ((c0 + r) * gpr + jb) * WPG + k;
+#pragma unroll
+      for (int p = 0; p < NCH; ++p) mw[p * plane_dw + o] = sc[p][r][k];
+    }
+  }
+  for (int d = threadIdx.x; d < ncols * JB; d += 256) {
+    const int r = d / JB, k = d % JB;
+    if (k < jn) exps[(c0 + r) * gpr + jb + k] = se[r][k];
   }
   if (status && any_bad) atomicOr(status, 1u);
 }
