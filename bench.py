@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--no-sweeps", action="store_true", help="skip the GEMM and quantize sweeps")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--quiet", action="store_true")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="also run a plain 256 MiB device copy (torch) whose profiler counters calibrate HBM bytes")
     return p.parse_args()
 
 
@@ -187,14 +189,32 @@ def quantize_sweep(torch, fb, synth, dev, args):
     return out
 
 
+def measured_traffic(key):
+    """HBM bytes per launch of a bench kernel from the committed rocprofv3
+    counter runs (profiles/traffic.json), or None if the kernel sources have
+    changed since those counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    data = json.load(open(path))
+    for fn, sha in data.get("source_sha256", {}).items():
+        src = os.path.join(ROOT, "paper_2110_15456_amd", "csrc", fn)
+        if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != sha:
+            return None
+    entry = data.get("bench_keys", {}).get(key)
+    return round(entry["bytes_per_launch"]) if entry else None
+
+
 def cpu_baseline(args):
-    """The oracle, untuned, on the host cores: every quantization of one m=4
-    step in full, plus the first 32 output rows of each GEMM; the GEMM time is
-    scaled to all rows and the step rate reported in the bench's unit."""
+    """The oracle, untuned, on the host cores (at most the 16-thread CPU share
+    of one GPU): every quantization of one m=4 step in full, plus the first
+    SAMPLE_ROWS output rows of each GEMM; the GEMM time is scaled to all rows
+    and the step rate reported in the bench's unit."""
     import numpy as np
     import oracle
     from paper_2110_15456_amd import synth
-    threads = max(1, min(os.cpu_count() or 1, 64))
+    threads = max(1, min(os.cpu_count() or 1, 16))
     X = synth.draw("half_normal", (M_TOK, D_IN), 51)
     W = synth.draw("weights", (D_IN, D_FF), 52)
     dY = synth.draw("grads", (M_TOK, D_FF), 53)
@@ -207,19 +227,21 @@ def cpu_baseline(args):
     xt = oracle.quantize(X, axis=0, g=G, m=m, threads=threads)
     dyt = oracle.quantize(dY, axis=0, g=G, m=m, mode="stochastic", seed=1001, threads=threads)
     tq = time.time() - t0
-    rows = np.arange(32)
+    SAMPLE_ROWS = 384
+    rows = np.arange(SAMPLE_ROWS)
     t1 = time.time()
     oracle.gemm(xa[0], xa[1], m, wb[0], wb[1], m, g=G, rows=rows, threads=threads)
     oracle.gemm(dya[0], dya[1], m, wk[0], wk[1], m, g=G, rows=rows, threads=threads)
     oracle.gemm(xt[0], xt[1], m, dyt[0], dyt[1], m, g=G, rows=rows, threads=threads)
     tg = time.time() - t1
-    # rows sampled: 32 of 8192 (fwd, dX) and 32 of 4096 (dW)
-    full_gemm_s = tg / 3 * (M_TOK / 32 + M_TOK / 32 + D_IN / 32)
+    # rows sampled: SAMPLE_ROWS of 8192 (fwd, dX) and of 4096 (dW); the three
+    # GEMMs have the same N*K per output row, so each took about tg / 3
+    full_gemm_s = tg / 3 * (M_TOK + M_TOK + D_IN) / SAMPLE_ROWS
     step_s = tq + full_gemm_s
     return {"value": round(STEP_OPS / step_s / 1e12, 6), "unit": "TOPS", "cores": threads, "kind": "oracle",
-            "sample": ("one m=4 FFN step: all six quantizations in full (%.1f s) and the first 32 output rows of "
+            "sample": ("one m=4 FFN step: all six quantizations in full (%.1f s) and the first %d output rows of "
                        "each GEMM (%.1f s), GEMM time scaled by rows to the full step (est. %.0f s per step)"
-                       % (tq, tg, step_s)),
+                       % (tq, SAMPLE_ROWS, tg, step_s)),
             "cpu_seconds": round(tq + tg, 1)}
 
 
@@ -284,11 +306,11 @@ def main():
     d = kernels[dom]
     if dom.startswith("gemm"):
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_FP6_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(d["achieved"] / PEAK_FP6_TFLOPS, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(d["achieved"] / PEAK_FP6_TFLOPS, 4), "traffic": measured_traffic(dom),
                 "work_per_launch": "2*M*N*K = %.4g FLOP (BFP MACs, algorithmic)" % GEMM_OPS}
     else:
         roof = {"bound": "hbm", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(d["achieved"] / PEAK_HBM_GBS, 4), "traffic": None}
+                "frac": round(d["achieved"] / PEAK_HBM_GBS, 4), "traffic": measured_traffic(dom)}
     log(args, "step %.3f ms, %.1f eff TOPS, wall %.2f s" % (ms_step, value, wall))
 
     result = {
@@ -302,6 +324,14 @@ def main():
     }
     del step
     torch.cuda.empty_cache()
+    if args.calibrate_copy:
+        src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
+        del src, dst
     if not args.no_sweeps:
         result["gemm_sweep"] = gemm_sweep(torch, fb, synth, dev, args)
         torch.cuda.empty_cache()
