@@ -60,6 +60,11 @@ def _load():
             lib.oracle_gemm.argtypes = [P, P, i32, P, P, i32, i64, i64, i64, i32, i32, i32, P, i64, P, P]
             lib.oracle_group_partials.argtypes = [P, i32, P, i32, i64, i64, i32, i32, i32, P, i64, P]
             lib.oracle_relative_improvement.argtypes = [P, P, P, P, i64, i32, i64, i64, P, P]
+            lib.oracle_drop_low_chunk.argtypes = [P, i64, P]
+            lib.oracle_threshold.argtypes = [ctypes.c_double, ctypes.c_double, i64, i64, i64, i64]
+            lib.oracle_threshold.restype = ctypes.c_double
+            lib.oracle_select_mantissa.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double]
+            lib.oracle_select_mantissa.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -207,3 +212,36 @@ def relative_improvement(q4, e4, q2, e2, g: int = 16) -> float:
     den = np.zeros(1, np.float64)
     lib.oracle_relative_improvement(*[_ptr(a) for a in arrs], n, g, 0, rows, _ptr(num), _ptr(den))
     return float(num[0] / den[0]) if den[0] != 0 else 0.0
+
+
+def drop_low_chunk(q4) -> np.ndarray:
+    """BFP(X,2) mantissas from the stored 4-bit ones: sign * (|q4| >> 2) (section V-D)."""
+    lib = _load()
+    q4 = np.ascontiguousarray(q4, dtype=np.int16)
+    q2 = np.empty_like(q4)
+    lib.oracle_drop_low_chunk(_ptr(q4), q4.size, _ptr(q2))
+    return q2
+
+
+def improvement_sums(q4, e4, g: int = 16):
+    """Numerator and denominator of Eq. 2 with BFP(X,2) the chunk-dropped BFP(X,4)."""
+    lib = _load()
+    q4 = np.ascontiguousarray(q4, dtype=np.int16)
+    e4 = np.ascontiguousarray(e4, dtype=np.uint8)
+    q2 = drop_low_chunk(q4)
+    rows, n = q4.shape
+    num = np.zeros(1, np.float64)
+    den = np.zeros(1, np.float64)
+    lib.oracle_relative_improvement(_ptr(q4), _ptr(e4), _ptr(q2), _ptr(e4), n, g, 0, rows, _ptr(num), _ptr(den))
+    return float(num[0]), float(den[0])
+
+
+def threshold(alpha: float, beta: float, i: int, I: int, l: int, L: int) -> float:
+    """Eq. 1."""
+    return float(_load().oracle_threshold(alpha, beta, i, I, l, L))
+
+
+def select_mantissa(num: float, den: float, eps: float) -> int:
+    """Algorithm 1's per-tensor choice (2 or 4 bits)."""
+    return int(_load().oracle_select_mantissa(num, den, eps))
+

@@ -277,3 +277,35 @@ void oracle_relative_improvement(const int16_t* q4, const uint8_t* e4, const int
   num[0] += n;
   den[0] += d;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Adaptive precision (section IV-B: Algorithm 1 and Eqs. 1-2; section V-D).  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The 2-bit mantissa of the adaptive scheme, taken from the stored 4-bit one:
+ * the converter keeps 4-bit mantissas as two 2-bit chunks and, when 2 bits
+ * are selected, the low chunk is discarded (section V-D).  The shared
+ * exponent is unchanged, so BFP(X,2) = sign * (|q4| >> 2) * 2^(E-127-1).
+ */
+void oracle_drop_low_chunk(const int16_t* q4, int64_t n, int16_t* q2) {
+  for (int64_t i = 0; i < n; ++i) {
+    const int mag = q4[i] < 0 ? -q4[i] : q4[i];
+    q2[i] = (int16_t)(q4[i] < 0 ? -(mag >> 2) : (mag >> 2));
+  }
+}
+
+/* Eq. 1: the threshold at layer l of L and iteration i of I. */
+double oracle_threshold(double alpha, double beta, int64_t i, int64_t I, int64_t l, int64_t L) {
+  return alpha - beta * (double)i / (double)I - beta * (double)l / (double)L;
+}
+
+/*
+ * Algorithm 1's choice for one tensor: 2 bits when the relative improvement
+ * r(X) = num / den of 4 over 2 bits is below the threshold, else 4.  An
+ * all-zero tensor (den = 0) has no improvement and takes 2 bits.
+ */
+int oracle_select_mantissa(double num, double den, double eps) {
+  const double r = den > 0.0 ? num / den : 0.0;
+  return r < eps ? 2 : 4;
+}

@@ -350,3 +350,58 @@ def test_relative_improvement_eq2():
               for i in range(3) for k in range(64))
     den = sum(abs(brute_value(q2[i, k], e2[i, k // 16], 2)) for i in range(3) for k in range(64))
     assert abs(r - float(num / den)) <= 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Adaptive precision (Algorithm 1, Eqs. 1-2, section V-D chunk discard)
+# ---------------------------------------------------------------------------
+
+def test_low_chunk_drop_equals_direct_truncation():
+    """Discarding the low 2-bit chunk of a truncated 4-bit mantissa is the
+    truncated 2-bit mantissa of the same value (same shared exponent)."""
+    for seed, dist in ((3, "normal"), (4, "grads"), (5, "half_normal")):
+        x = synth.draw(dist, (8, 256), seed)
+        q4, e4, _ = oracle.quantize(x, g=16, m=4, mode="truncate")
+        q2, e2, _ = oracle.quantize(x, g=16, m=2, mode="truncate")
+        assert np.array_equal(e4, e2)
+        assert np.array_equal(oracle.drop_low_chunk(q4), q2)
+
+
+def test_improvement_hand_example():
+    """One group holding 1.75 and zeros: BFP(1.75, 4) = 14/8 = 1.75, the chunk
+    drop keeps 14 >> 2 = 3 at LSB 1/2, i.e. 1.5; r = 0.25 / 1.5 = 1/6."""
+    x = np.zeros((1, 16), np.float32)
+    x[0, 0] = 1.75
+    q4, e4, _ = oracle.quantize(x, g=16, m=4)
+    assert q4[0, 0] == 14 and e4[0, 0] == 127
+    num, den = oracle.improvement_sums(q4, e4, g=16)
+    assert num == 0.25 and den == 1.5
+    # sign is carried: -1.75 gives the same sums
+    q4n, e4n, _ = oracle.quantize(-x, g=16, m=4)
+    assert oracle.improvement_sums(q4n, e4n, g=16) == (0.25, 1.5)
+
+
+def test_improvement_zero_on_two_bit_grid():
+    """Values already on their group's 2-bit grid have no low chunk: r = 0."""
+    rng = np.random.default_rng(9)
+    k = rng.integers(-3, 4, size=(4, 64)).astype(np.float64)
+    k[:, ::16] = 3.0  # each group's maximum sits in the top chunk
+    scale = 2.0 ** rng.integers(-20, 20, size=(4, 4)).repeat(16, axis=1)
+    x = (k * scale).astype(np.float32)
+    q4, e4, _ = oracle.quantize(x, g=16, m=4)
+    num, den = oracle.improvement_sums(q4, e4, g=16)
+    assert num == 0.0 and den > 0.0
+
+
+def test_threshold_eq1_and_selection():
+    """Eq. 1 endpoints with the paper's alpha = 0.6, beta = 0.3, and the strict
+    inequality of Algorithm 1."""
+    a, b = 0.6, 0.3
+    assert oracle.threshold(a, b, 0, 100, 0, 10) == a
+    assert abs(oracle.threshold(a, b, 100, 100, 10, 10) - (a - 2 * b)) < 1e-15
+    eps = [oracle.threshold(a, b, i, 100, 3, 10) for i in range(0, 101, 10)]
+    assert all(e1 > e2 for e1, e2 in zip(eps, eps[1:]))
+    assert oracle.select_mantissa(1.0, 4.0, 0.25) == 4   # r == eps: not below
+    assert oracle.select_mantissa(1.0, 4.0, 0.2500001) == 2
+    assert oracle.select_mantissa(0.0, 0.0, 0.0) == 4    # r = 0, eps = 0: not below
+    assert oracle.select_mantissa(0.0, 0.0, 0.1) == 2
