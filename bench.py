@@ -185,6 +185,24 @@ def quantize_sweep(torch, fb, synth, dev, args):
                                          "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
             log(args, "quantize m=%d %s: %.1f us, %.0f GB/s" % (m, mode, ms * 1e3, gbs))
             del outs
+    # The adaptive converter (Algorithm 1, Eq. 2): one pass writes BFP(X,4),
+    # the 2-bit tensor left by discarding the low chunk, and the two sums.
+    for mode in ("nearest", "stochastic"):
+        for r in range(3):
+            fb.quantize_adaptive(xs[r], g=G, rounding=mode, seed=1234)
+        torch.cuda.synchronize()
+        reps = 12
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(reps):
+            fb.quantize_adaptive(xs[r % 3], g=G, rounding=mode, seed=1234)
+        z.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(z) / reps
+        gbs = n * (4 + 0.75 * 2 + 1.0 / G) / (ms * 1e-3) / 1e9
+        out["adaptive_m4m2_%s" % mode] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
+                                          "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+        log(args, "adaptive m=4/2 %s: %.1f us, %.0f GB/s" % (mode, ms * 1e3, gbs))
     del xs
     return out
 

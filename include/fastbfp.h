@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define FASTBFP_ABI_VERSION 1
+#define FASTBFP_ABI_VERSION 2
 
 typedef enum {
   BFP_ROUND_NEAREST = 0,    /* add half an LSB, then truncate (ties away from zero) */
@@ -163,6 +163,50 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
  */
 int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* b_mant, int b_m_bits, int64_t M,
                             int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream);
+
+/*
+ * bfp_quantize_adaptive -- the converter and improvement block of the adaptive
+ * scheme (Algorithm 1, Eq. 2, section V-C; section V-D for the chunk discard),
+ * in one pass over x: BFP(X, 4) is written as by bfp_quantize with m_bits = 4;
+ * BFP(X, 2) is that tensor with the low 2-bit chunk of every mantissa
+ * discarded (same shared exponents: value +-(q >> 2) * 2^(E - 128)); and
+ *   sums[0] = sum_n |BFP(X_n, 4) - BFP(X_n, 2)|,  sums[1] = sum_n |BFP(X_n, 2)|,
+ * so that r(X) = sums[0] / sums[1] (Eq. 2).
+ *   x, R, C, group_axis, g, round_mode, seed, status_word : as bfp_quantize.
+ *   mant4, exp  : the m = 4 tensor (layout of bfp_quantize, m_bits = 4).
+ *   mant2       : optional (may be NULL): the m = 2 tensor's mantissas, same
+ *                 size as mant4; it shares exp.  Either tensor can be handed to
+ *                 bfp_gemm (m_bits 4 or 2) without converting again.
+ *   sums        : device doubles, bfp_adaptive_sums_len(R, C, group_axis, g)
+ *                 of them (8-byte aligned): sums[0] and sums[1] receive the two
+ *                 sums, the rest is the workspace of their per-workgroup
+ *                 partials.  The partials are added in a fixed order, so the
+ *                 result is the same on every run.
+ */
+int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode, uint64_t seed,
+                          uint8_t* mant4, uint8_t* mant2, uint8_t* exp, double* sums, uint32_t* status_word,
+                          void* stream);
+
+/*
+ * bfp_adaptive_sums_len -- the number of doubles bfp_quantize_adaptive needs
+ * at `sums` for this shape (at least 2); -1 if group_axis or g is invalid.
+ */
+int64_t bfp_adaptive_sums_len(int64_t R, int64_t C, int group_axis, int g);
+
+/*
+ * bfp_adaptive_threshold -- Eq. 1: epsilon(l, i) = alpha - beta * i / I -
+ * beta * l / L for iteration i of I and layer l of L (the paper uses alpha =
+ * 0.6, beta = 0.3).  Host arithmetic; returns NaN if I or L is not positive.
+ */
+double bfp_adaptive_threshold(double alpha, double beta, int64_t i, int64_t I, int64_t l, int64_t L);
+
+/*
+ * bfp_adaptive_mantissa -- Algorithm 1's choice for one tensor: 2 if
+ * r(X) = num / den < eps, else 4 (r = 0 when den = 0: an all-zero tensor gains
+ * nothing from 4 bits).  Host arithmetic on the two sums read back from
+ * bfp_quantize_adaptive.
+ */
+int bfp_adaptive_mantissa(double num, double den, double eps);
 
 #ifdef __cplusplus
 }

@@ -121,6 +121,61 @@ def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rou
     return t
 
 
+def quantize_adaptive(x: torch.Tensor, group_axis: int = -1, g: int = 16, rounding: str = "nearest",
+                      seed: int = 0, with_m2: bool = True, status: torch.Tensor | None = None):
+    """One pass of the adaptive converter (Algorithm 1, Eq. 2): returns
+    ``(t4, t2, sums)`` with t4 = BFP(X, 4), t2 = BFP(X, 2) taken from t4 by
+    discarding the low 2-bit chunk (same exponent tensor; None unless
+    ``with_m2``), and sums a float64 CUDA tensor [sum |BFP4 - BFP2|,
+    sum |BFP2|], so that r(X) = sums[0] / sums[1]."""
+    _need_cuda(x, "x", torch.float32)
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    nd = x.dim()
+    if nd < 1:
+        raise ValueError("x must have at least one dimension")
+    ax = group_axis % nd
+    if ax == nd - 1:
+        C = x.shape[-1]
+        R = x.numel() // C if C else 0
+        axis_flag, rows, length = 1, R, C
+    elif nd == 2 and ax == 0:
+        R, C = x.shape
+        axis_flag, rows, length = 0, C, R
+    else:
+        raise ValueError("group_axis must be the last axis, or 0 of a 2-D tensor")
+    t4 = BFPTensor.empty(rows, length, g, 4, x.device)
+    t2 = BFPTensor(torch.empty_like(t4.mant), t4.exp, rows, length, g, 2) if with_m2 else None
+    lib = load()
+    n_sums = lib.bfp_adaptive_sums_len(R, C, axis_flag, g)
+    if n_sums < 2:
+        raise ValueError("unsupported shape or group size for the adaptive converter")
+    work = torch.empty(n_sums, dtype=torch.float64, device=x.device)
+    sums = work[:2]
+    st_ptr = None
+    if status is not None:
+        _need_cuda(status, "status")
+        st_ptr = ctypes.c_void_p(status.data_ptr())
+    check(lib.bfp_quantize_adaptive(ctypes.c_void_p(x.data_ptr()), R, C, axis_flag, g, ROUNDING[rounding],
+                                    ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(t4.mant.data_ptr()),
+                                    ctypes.c_void_p(t2.mant.data_ptr()) if t2 is not None else None,
+                                    ctypes.c_void_p(t4.exp.data_ptr()), ctypes.c_void_p(work.data_ptr()), st_ptr,
+                                    _stream(x.device)), "bfp_quantize_adaptive")
+    return t4, t2, sums
+
+
+def adaptive_threshold(alpha: float, beta: float, i: int, I: int, l: int, L: int) -> float:
+    """Eq. 1: epsilon(l, i) = alpha - beta i / I - beta l / L."""
+    return float(load().bfp_adaptive_threshold(alpha, beta, i, I, l, L))
+
+
+def adaptive_mantissa(sums, eps: float) -> int:
+    """Algorithm 1's choice (2 or 4 bits) from the two sums of quantize_adaptive
+    (reading them back synchronises with the stream)."""
+    num, den = (float(v) for v in (sums.tolist() if hasattr(sums, "tolist") else sums))
+    return int(load().bfp_adaptive_mantissa(num, den, eps))
+
+
 def dequantize(t: BFPTensor, out: torch.Tensor | None = None) -> torch.Tensor:
     """BFP -> FP32 [rows, len]: +-q * 2^(E - 127 - (m-1))."""
     y = out if out is not None else torch.empty((t.rows, t.len), dtype=torch.float32, device=t.device)

@@ -128,4 +128,39 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
                                                   M, N, K, g, P, static_cast<hipStream_t>(stream)));
 }
 
+int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode, uint64_t seed,
+                          uint8_t* mant4, uint8_t* mant2, uint8_t* exp, double* sums, uint32_t* status_word,
+                          void* stream) {
+  if (group_axis != 0 && group_axis != 1) return BFP_E_ARG;
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  const int64_t rows = group_axis == 1 ? R : C, len = group_axis == 1 ? C : R;
+  const int st = check_tensor(rows, len, g, 4);
+  if (st != BFP_OK) return st;
+  if (!sums || !aligned(sums, 8)) return BFP_E_ARG;
+  if (R != 0 && C != 0) {
+    if (!x || !mant4 || !exp) return BFP_E_ARG;
+    if (!aligned(x, group_axis == 1 ? 16 : 4) || !aligned(mant4, 4) || !aligned(mant2, 4) ||
+        !aligned(status_word, 4))
+      return BFP_E_ARG;
+  }
+  return status_of(fastbfp::launch_quantize_adaptive(x, R, C, group_axis, g, round_mode, seed, mant4, mant2, exp, sums,
+                                                     status_word, static_cast<hipStream_t>(stream)));
+}
+
+int64_t bfp_adaptive_sums_len(int64_t R, int64_t C, int group_axis, int g) {
+  if ((group_axis != 0 && group_axis != 1) || (g != 16 && g != 32) || R < 0 || C < 0) return -1;
+  if ((group_axis == 1 ? C : R) % g != 0) return -1;
+  return 2 + 2 * fastbfp::adaptive_parts(R, C, group_axis, g);
+}
+
+double bfp_adaptive_threshold(double alpha, double beta, int64_t i, int64_t I, int64_t l, int64_t L) {
+  if (I <= 0 || L <= 0) return __builtin_nan("");
+  return alpha - beta * (double)i / (double)I - beta * (double)l / (double)L;
+}
+
+int bfp_adaptive_mantissa(double num, double den, double eps) {
+  const double r = den > 0.0 ? num / den : 0.0;
+  return r < eps ? 2 : 4;
+}
+
 }  // extern "C"

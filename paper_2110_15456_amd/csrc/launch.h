@@ -14,6 +14,15 @@ hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
 hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
+// Adaptive precision (Algorithm 1, Eq. 2): quantize at m = 4 into mant4/exps,
+// optionally write the low-chunk-discarded 2-bit mantissas to mant2, and set
+// sums[0] = sum |BFP(X,4) - BFP(X,2)|, sums[1] = sum |BFP(X,2)| (sums holds
+// 2 + 2 * adaptive_parts(...) doubles; the rest is workspace).
+// Partial-sum pairs the adaptive kernel writes (one per workgroup).
+int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g);
+hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
+                                    uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
+                                    uint32_t* status, hipStream_t s);
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
                              float* y, hipStream_t s);
 // na / nb: chunk planes used (1 or 2); a_off / b_off: the stored operand's plane

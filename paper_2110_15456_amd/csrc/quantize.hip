@@ -37,10 +37,18 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
 // flushing, so ldexp reads them as zero).  Codes are produced by the gfx950
 // FP6 converter, which interleaves its two 16-value inputs: output value 2i is
 // a[i] / scale and 2i+1 is b[i] / scale.
-template <int G, int MODE, int NCH>
+//
+// ADAPT (m = 4 only; section V-D and Eq. 2): plane 0 gets the 4-bit magnitude
+// q as one code, plane 1 (if NCH = 2) the 2-bit mantissa left when the low
+// chunk is discarded, q >> 2; s_lo and s_hi return the group's sums of q & 3
+// and q >> 2 (the magnitudes BFP(X,4) - BFP(X,2) and BFP(X,2) in units of
+// 2^(E-130) and 2^(E-128)).
+template <int G, int MODE, int NCH, bool ADAPT = false>
 __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
                                                uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
-                                               bool& nonfinite) {
+                                               bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
+  s_lo = 0u;
+  s_hi = 0u;
   // (a) shared exponent: the largest biased exponent field in the group.
   uint32_t E = 0;
 #pragma unroll
@@ -89,7 +97,13 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
     q = min(q, qmax);  // a group maximum that rounds up to 2^m saturates
     const float nh = __uint_as_float((b[t] & 0x80000000u) | 0x3F000000u);  // +-0.5
     const int h = t / 32, k = (t % 32) / 2;
-    if (NCH == 1) {
+    if (ADAPT) {
+      s_lo += q & 3u;
+      s_hi += q >> 2;
+      const float f4 = signed_half(q, nh), f2 = signed_half(q >> 2, nh);
+      if (t % 2 == 0) { ev[0][h][k] = f4; ev[NCH - 1][h][k] = NCH == 2 ? f2 : f4; }
+      else { od[0][h][k] = f4; od[NCH - 1][h][k] = NCH == 2 ? f2 : f4; }
+    } else if (NCH == 1) {
       const float f = signed_half(q, nh);
       if (t % 2 == 0) ev[0][h][k] = f; else od[0][h][k] = f;
     } else {
@@ -109,14 +123,63 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
     }
 }
 
+// Plane p of the group goes to mant_p (plane 1 of a two-chunk tensor, or the
+// separate 2-bit tensor of the adaptive path).
 template <int G, int NCH>
-__device__ __forceinline__ void store_group(uint8_t* __restrict__ mant, int64_t plane_bytes, int64_t gid,
+__device__ __forceinline__ void store_group(uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1, int64_t gid,
                                             const uint32_t (&w)[NCH][G * 6 / 32]) {
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
-    uint3* dst = reinterpret_cast<uint3*>(mant + p * plane_bytes + gid * (G * 3 / 4));
+    uint3* dst = reinterpret_cast<uint3*>((p ? mant1 : mant0) + gid * (G * 3 / 4));
 #pragma unroll
     for (int i = 0; i < G / 16; ++i) dst[i] = make_uint3(w[p][3 * i], w[p][3 * i + 1], w[p][3 * i + 2]);
+  }
+}
+
+// Writes the block's Eq. 2 partial sums to part[2 * blockIdx.x + {0, 1}]:
+// a fixed-order reduction over the lanes of each wave, then over the four
+// waves.  Every thread of the block must call it.
+__device__ __forceinline__ void block_improvement(double num, double den, double* part) {
+  __shared__ double red[2][4];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    num += __shfl_xor(num, off);
+    den += __shfl_xor(den, off);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wave] = num;
+    red[1][wave] = den;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    part[2 * blockIdx.x + 1] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+  }
+}
+
+// sums[0..1] = the sums of the nparts partial pairs at sums + 2, in a fixed
+// order (one block): the result does not depend on scheduling.
+__global__ __launch_bounds__(256) void k_improvement_finalize(double* sums, int64_t nparts) {
+  __shared__ double red[2][256];
+  double num = 0.0, den = 0.0;
+  for (int64_t i = threadIdx.x; i < nparts; i += 256) {
+    num += sums[2 + 2 * i];
+    den += sums[3 + 2 * i];
+  }
+  red[0][threadIdx.x] = num;
+  red[1][threadIdx.x] = den;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + w];
+      red[1][threadIdx.x] += red[1][threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    sums[0] = red[0][0];
+    sums[1] = red[1][0];
   }
 }
 
@@ -129,17 +192,18 @@ __device__ __forceinline__ void store_group(uint8_t* __restrict__ mant, int64_t 
 // all 64 banks on the read-back.  (Reading 64 contiguous bytes per lane
 // straight from global memory instead leaves each load instruction touching
 // 64 scattered 16-byte pieces, which costs about a third of HBM bandwidth.)
-template <int G, int MODE, int NCH>
+template <int G, int MODE, int NCH, bool ADAPT>
 __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__ x, int64_t ngroups, uint32_t m,
-                                                       uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant,
-                                                       uint8_t* __restrict__ exps, uint32_t* status) {
+                                                       uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
+                                                       uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
+                                                       uint32_t* status, double* sums) {
   constexpr int CPG = G / 4;             // 16-byte chunks per group
   constexpr int LANES_PER_SWZ = 16 / CPG;
   __shared__ __attribute__((aligned(16))) uint32_t stage[4][64 * G];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t g0 = ((int64_t)blockIdx.x * 4 + wave) * 64;  // first group of this wave
-  if (g0 >= ngroups) return;
-  const int64_t nvalid = min((int64_t)64, ngroups - g0);
+  if (!ADAPT && g0 >= ngroups) return;  // (the adaptive path keeps every wave for its block sums)
+  const int64_t nvalid = max((int64_t)0, min((int64_t)64, ngroups - g0));
   typedef __attribute__((address_space(3))) void lds_void;
   const uint8_t* base = reinterpret_cast<const uint8_t*>(x) + g0 * (G * 4);
 #pragma unroll
@@ -148,12 +212,13 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
     const int l = slot / CPG;
     const int j = (slot % CPG) ^ ((l / LANES_PER_SWZ) % CPG);
     // chunks of groups past the end read the wave's first chunk instead (unused)
-    const int64_t off = (l < nvalid) ? (int64_t)(l * CPG + j) * 16 : 0;
+    const int64_t off = (l < nvalid) ? (int64_t)(l * CPG + j) * 16 : -g0 * (G * 4);  // x's first chunk
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + off),
                                      (lds_void*)(&stage[wave][64 * 4 * k]), 16, 0, 0);
   }
   __builtin_amdgcn_s_waitcnt(0);  // the wave reads back what its own loads wrote
-  if (lane >= nvalid) return;
+  const bool valid = lane < nvalid;
+  if (!ADAPT && !valid) return;  // (the adaptive path keeps every lane for its wave sums)
   uint32_t b[G];
 #pragma unroll
   for (int j = 0; j < CPG; ++j) {
@@ -166,12 +231,17 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   }
   const int64_t gid = g0 + lane;
   uint32_t w[NCH][G * 6 / 32];
-  uint32_t E;
+  uint32_t E, s_lo, s_hi;
   bool nonfinite;
-  quantize_group<G, MODE, NCH>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite);
-  exps[gid] = (uint8_t)E;
-  store_group<G, NCH>(mant, ngroups * (G * 3 / 4), gid, w);
-  if (status && nonfinite) atomicOr(status, 1u);
+  quantize_group<G, MODE, NCH, ADAPT>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
+  if (valid) {
+    exps[gid] = (uint8_t)E;
+    store_group<G, NCH>(mant0, mant1, gid, w);
+    if (status && nonfinite) atomicOr(status, 1u);
+  }
+  if (ADAPT)
+    block_improvement(valid ? ldexp((double)s_lo, (int)E - 130) : 0.0, valid ? ldexp((double)s_hi, (int)E - 128) : 0.0,
+                      sums + 2);
 }
 
 // Groups down the columns of x[R][C] (transpose-on-quantize).  Output row c is
@@ -181,11 +251,11 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
 // consecutive group rows (NGT per wave).  The packed codes and exponents of
 // the 64 x JB groups are gathered in LDS and then written row by row, so that
 // every store instruction writes contiguous bytes of one output row.
-template <int G, int MODE, int NCH, int NGT>
+template <int G, int MODE, int NCH, int NGT, bool ADAPT>
 __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__ x, int64_t R, int64_t C,
                                                        int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
-                                                       uint8_t* __restrict__ mant, uint8_t* __restrict__ exps,
-                                                       uint32_t* status) {
+                                                       uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1,
+                                                       uint8_t* __restrict__ exps, uint32_t* status, double* sums) {
   constexpr int JB = 4 * NGT;             // group rows per block
   constexpr int WPG = G * 6 / 32;         // code dwords per group per plane
   constexpr int ROWW = JB * WPG;          // code dwords per output row per plane in this block
@@ -198,6 +268,7 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
   const int64_t jb = by * JB;
   const int jn = (int)min((int64_t)JB, gpr - jb);  // group rows this block covers
   bool any_bad = false;
+  double num = 0.0, den = 0.0;
   if (c < C) {
     for (int i = 0; i < NGT; ++i) {
       const int jl = slot * NGT + i;
@@ -208,9 +279,13 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
 #pragma unroll
       for (int t = 0; t < G; ++t) b[t] = __float_as_uint(src[t * C]);
       uint32_t w[NCH][WPG];
-      uint32_t E;
+      uint32_t E, s_lo, s_hi;
       bool nonfinite;
-      quantize_group<G, MODE, NCH>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite);
+      quantize_group<G, MODE, NCH, ADAPT>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo, s_hi);
+      if (ADAPT) {
+        num += ldexp((double)s_lo, (int)E - 130);
+        den += ldexp((double)s_hi, (int)E - 128);
+      }
 #pragma unroll
       for (int p = 0; p < NCH; ++p)
 #pragma unroll
@@ -219,17 +294,16 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       any_bad |= nonfinite;
     }
   }
+  if (ADAPT) block_improvement(num, den, sums + 2);
   __syncthreads();
   // Write-out: output row c0 + r gets jn groups starting at group jb.
   const int ncols = (int)min((int64_t)64, C - c0);
-  const int64_t plane_dw = C * gpr * WPG;  // dwords per plane
-  uint32_t* mw = reinterpret_cast<uint32_t*>(mant);
   for (int d = threadIdx.x; d < ncols * ROWW; d += 256) {
     const int r = d / ROWW, k = d % ROWW;
     if (k < jn * WPG) {
       const int64_t o = ((c0 + r) * gpr + jb) * WPG + k;
 #pragma unroll
-      for (int p = 0; p < NCH; ++p) mw[p * plane_dw + o] = sc[p][r][k];
+      for (int p = 0; p < NCH; ++p) reinterpret_cast<uint32_t*>(p ? mant1 : mant0)[o] = sc[p][r][k];
     }
   }
   for (int d = threadIdx.x; d < ncols * JB; d += 256) {
@@ -276,23 +350,23 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
   }
 }
 
-template <int G, int MODE, int NCH>
-static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant, uint8_t* exps,
-                                uint32_t* status, hipStream_t s) {
+template <int G, int MODE, int NCH, bool ADAPT = false>
+static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
+                                uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
   const int64_t blocks = (ngroups + 255) / 256;
-  hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
-                     (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant, exps, status);
+  hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
+                     (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
   return hipGetLastError();
 }
 
-template <int G, int MODE, int NCH>
-static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant,
-                                uint8_t* exps, uint32_t* status, hipStream_t s) {
+template <int G, int MODE, int NCH, bool ADAPT = false>
+static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant0,
+                                uint8_t* mant1, uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
   constexpr int NGT = 8;
   const int64_t gpr = R / G;
   const int64_t nbx = (C + 63) / 64, nby = (gpr + 4 * NGT - 1) / (4 * NGT);
-  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R, C, nbx,
-                     (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant, exps, status);
+  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
+                     C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
   return hipGetLastError();
 }
 
@@ -314,13 +388,61 @@ hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s) {
   const int64_t ngroups = rows * (len / g);
   if (ngroups == 0) return hipSuccess;
-  FASTBFP_DISPATCH_QUANT(launch_rows_t, x, ngroups, m, seed, mant, exps, status, s);
+  uint8_t* mant1 = mant + ngroups * (g * 3 / 4);  // plane 1 when m > 4
+  FASTBFP_DISPATCH_QUANT(launch_rows_t, x, ngroups, m, seed, mant, mant1, exps, status, nullptr, s);
 }
 
 hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s) {
   if (R == 0 || C == 0) return hipSuccess;
-  FASTBFP_DISPATCH_QUANT(launch_cols_t, x, R, C, m, seed, mant, exps, status, s);
+  uint8_t* mant1 = mant + C * (R / g) * (g * 3 / 4);  // plane 1 when m > 4
+  FASTBFP_DISPATCH_QUANT(launch_cols_t, x, R, C, m, seed, mant, mant1, exps, status, nullptr, s);
+}
+
+#define FASTBFP_DISPATCH_ADAPT(FN, ...)                                                                    \
+  do {                                                                                                    \
+    if (g == 16) {                                                                                        \
+      if (mode == kNearest) return two ? FN<16, kNearest, 2, true>(__VA_ARGS__) : FN<16, kNearest, 1, true>(__VA_ARGS__); \
+      if (mode == kStochastic)                                                                            \
+        return two ? FN<16, kStochastic, 2, true>(__VA_ARGS__) : FN<16, kStochastic, 1, true>(__VA_ARGS__); \
+      return two ? FN<16, kTruncate, 2, true>(__VA_ARGS__) : FN<16, kTruncate, 1, true>(__VA_ARGS__);   \
+    } else {                                                                                              \
+      if (mode == kNearest) return two ? FN<32, kNearest, 2, true>(__VA_ARGS__) : FN<32, kNearest, 1, true>(__VA_ARGS__); \
+      if (mode == kStochastic)                                                                            \
+        return two ? FN<32, kStochastic, 2, true>(__VA_ARGS__) : FN<32, kStochastic, 1, true>(__VA_ARGS__); \
+      return two ? FN<32, kTruncate, 2, true>(__VA_ARGS__) : FN<32, kTruncate, 1, true>(__VA_ARGS__);   \
+    }                                                                                                     \
+  } while (0)
+
+int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g) {
+  if (R == 0 || C == 0) return 0;
+  if (group_axis == 1) return (R * (C / g) + 255) / 256;  // one partial pair per k_quantize_rows block
+  const int64_t gpr = R / g;
+  return ((C + 63) / 64) * ((gpr + 31) / 32);  // one per k_quantize_cols block (NGT = 8)
+}
+
+static hipError_t launch_adaptive_kernel(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
+                                         uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
+                                         uint32_t* status, hipStream_t s) {
+  const int m = 4;
+  const bool two = mant2 != nullptr;  // second output plane: the 2-bit mantissas
+  if (group_axis == 1) {
+    const int64_t ngroups = R * (C / g);
+    FASTBFP_DISPATCH_ADAPT(launch_rows_t, x, ngroups, m, seed, mant4, mant2, exps, status, sums, s);
+  }
+  FASTBFP_DISPATCH_ADAPT(launch_cols_t, x, R, C, m, seed, mant4, mant2, exps, status, sums, s);
+}
+
+hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
+                                    uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
+                                    uint32_t* status, hipStream_t s) {
+  const int64_t nparts = adaptive_parts(R, C, group_axis, g);
+  if (nparts > 0) {
+    const hipError_t e = launch_adaptive_kernel(x, R, C, group_axis, g, mode, seed, mant4, mant2, exps, sums, status, s);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_improvement_finalize, dim3(1), dim3(256), 0, s, sums, nparts);
+  return hipGetLastError();
 }
 
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,

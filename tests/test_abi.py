@@ -4,6 +4,7 @@ every call here returns before touching the HIP runtime."""
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import re
 import subprocess
@@ -40,8 +41,14 @@ def test_exports_every_declared_symbol(lib):
     assert sorted(_lib.SIGNATURES) == names
 
 
+def _header_abi_version():
+    import re
+    txt = open(os.path.join(ROOT, "include", "fastbfp.h")).read()
+    return int(re.search(r"#define FASTBFP_ABI_VERSION (\d+)", txt).group(1))
+
+
 def test_version_and_status_strings(lib):
-    assert lib.bfp_abi_version() == 1
+    assert lib.bfp_abi_version() == _header_abi_version()
     for s in range(6):
         assert len(lib.bfp_status_str(s)) > 0
     assert lib.bfp_status_str(99) == b"unknown status"
@@ -144,3 +151,46 @@ def test_product_path_does_not_touch_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 pat = r"^\s*(import|from)\s+oracle\b|liboracle|\boracle\.\w+\s*\(|oracle\.c\b"
                 assert not re.search(pat, text, flags=re.M), os.path.join(dirpath, f)
+
+
+def test_adaptive_argument_errors(lib):
+    """bfp_quantize_adaptive validates on the host before any launch."""
+    P = ctypes.c_void_p
+    dummy = P(4096)
+    sums = P(8192)
+    E_ARG, E_SHAPE = 1, 2
+    # bad group axis, bad rounding mode, missing sums, misaligned sums
+    assert lib.bfp_quantize_adaptive(dummy, 4, 32, 2, 16, 0, 0, dummy, None, dummy, sums, None, None) == E_ARG
+    assert lib.bfp_quantize_adaptive(dummy, 4, 32, 1, 16, 7, 0, dummy, None, dummy, sums, None, None) == E_ARG
+    assert lib.bfp_quantize_adaptive(dummy, 4, 32, 1, 16, 0, 0, dummy, None, dummy, None, None, None) == E_ARG
+    assert lib.bfp_quantize_adaptive(dummy, 4, 32, 1, 16, 0, 0, dummy, None, dummy, P(8196), None, None) == E_ARG
+    # g does not divide the grouped axis
+    assert lib.bfp_quantize_adaptive(dummy, 4, 40, 1, 16, 0, 0, dummy, None, dummy, sums, None, None) == E_SHAPE
+    assert lib.bfp_quantize_adaptive(dummy, 40, 32, 0, 16, 0, 0, dummy, None, dummy, sums, None, None) == E_SHAPE
+    # missing outputs, misaligned second tensor
+    assert lib.bfp_quantize_adaptive(dummy, 4, 32, 1, 16, 0, 0, None, None, dummy, sums, None, None) == E_ARG
+    assert lib.bfp_quantize_adaptive(dummy, 4, 32, 1, 16, 0, 0, dummy, P(4098), dummy, sums, None, None) == E_ARG
+
+
+def test_adaptive_host_helpers_match_oracle(lib):
+    """Eq. 1 and Algorithm 1's choice: the library's host arithmetic against
+    the oracle's."""
+    import oracle
+    for args in ((0.6, 0.3, 0, 100, 0, 12), (0.6, 0.3, 37, 100, 5, 12), (0.6, 0.3, 100, 100, 12, 12),
+                 (0.9, 0.1, 3, 7, 2, 5)):
+        assert lib.bfp_adaptive_threshold(*args) == oracle.threshold(*args)
+    assert math.isnan(lib.bfp_adaptive_threshold(0.6, 0.3, 1, 0, 1, 4))
+    for num, den, eps in ((1.0, 4.0, 0.25), (1.0, 4.0, 0.26), (0.0, 0.0, 0.0), (0.0, 0.0, 0.1), (3.0, 2.0, 0.6)):
+        assert lib.bfp_adaptive_mantissa(num, den, eps) == oracle.select_mantissa(num, den, eps)
+
+
+
+def test_adaptive_sums_len(lib):
+    """Workspace doubles for the adaptive converter: 2 results + 2 per workgroup."""
+    assert lib.bfp_adaptive_sums_len(4, 32, 2, 16) == -1
+    assert lib.bfp_adaptive_sums_len(4, 40, 1, 16) == -1
+    assert lib.bfp_adaptive_sums_len(4, 32, 1, 8) == -1
+    assert lib.bfp_adaptive_sums_len(0, 64, 1, 16) == 2
+    assert lib.bfp_adaptive_sums_len(4, 32, 1, 16) == 4          # 8 groups: one workgroup of 256 groups
+    assert lib.bfp_adaptive_sums_len(8192, 8192, 1, 16) == 2 + 2 * (8192 * 512 // 256)
+    assert lib.bfp_adaptive_sums_len(512, 100, 0, 16) == 2 + 2 * (2 * 1)  # 2 column blocks x 1 group-row block
