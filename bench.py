@@ -207,6 +207,44 @@ def quantize_sweep(torch, fb, synth, dev, args):
     return out
 
 
+def epilogue_sweep(torch, fb, synth, dev, args):
+    """The GEMM with its output converted to BFP in the epilogue (the layer
+    output handed to the next layer as BFP, section V-A) against the same work
+    unfused: the FP32 GEMM followed by a separate quantize of C (16384-wide
+    rows, groups of 16).  FFN up-projection shape, output at the input's
+    width."""
+    M, N, K = 8192, 16384, 4096
+    X = torch.from_numpy(synth.draw("normal", (M, K), 41)).to(dev)
+    W = torch.from_numpy(synth.draw("weights", (N, K), 42)).to(dev)
+    C = torch.empty((M, N), dtype=torch.float32, device=dev)
+    out = {}
+
+    def timed(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        z.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(z) / reps
+
+    for m in (2, 4, 6):
+        A, B = fb.quantize(X, g=G, m=m), fb.quantize(W, g=G, m=m)
+        T = fb.BFPTensor.empty(M, N, G, m, dev)
+        for mode in ("nearest", "stochastic"):
+            fused = timed(lambda: fb.gemm_bfp(A, B, m, rounding=mode, seed=77, out=T))
+            sep = timed(lambda: (fb.gemm(A, B, out=C), fb.quantize(C, g=G, m=m, rounding=mode, seed=77, out=T)))
+            out["ffn_up(%d,%d)->m%d_%s" % (m, m, m, mode)] = {
+                "fused_ms": round(fused, 4), "unfused_ms": round(sep, 4), "speedup": round(sep / fused, 3),
+                "fused_eff_tops": round(2.0 * M * N * K / (fused * 1e-3) / 1e12, 1)}
+            log(args, "gemm_bfp ffn_up m=%d %s: fused %.3f ms, unfused %.3f ms" % (m, mode, fused, sep))
+        del A, B, T
+    del X, W, C
+    return out
+
+
 def measured_traffic(key):
     """HBM bytes per launch of a bench kernel from the committed rocprofv3
     counter runs (profiles/traffic.json), or None if the kernel sources have
@@ -354,6 +392,7 @@ def main():
         result["gemm_sweep"] = gemm_sweep(torch, fb, synth, dev, args)
         torch.cuda.empty_cache()
         result["quantize_sweep"] = quantize_sweep(torch, fb, synth, dev, args)
+        result["epilogue_sweep"] = epilogue_sweep(torch, fb, synth, dev, args)
     if not args.no_cpu:
         log(args, "timing the CPU oracle on a sample ...")
         result["cpu_baseline"] = cpu_baseline(args)

@@ -152,6 +152,25 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
              void* stream);
 
 /*
+ * bfp_gemm_bfp -- bfp_gemm with its output converted to BFP in the epilogue,
+ * from the FP32 results, by the converter of section V-C (the paper's
+ * converter sits at the output of the systolic array, section V-A): C is
+ * written as a BFP tensor of rows = M, len = N with groups of 16 along each
+ * row (the K axis of a GEMM that consumes C as its left operand) at c_m_bits,
+ * in the layout of bfp_quantize.  The result is exactly bfp_quantize(C, group
+ * axis 1, g = 16, c_m_bits, round_mode, seed) of the FP32 C that bfp_gemm
+ * computes: the same values, the same noise addressing (gid = the index into
+ * c_exp), without writing or re-reading FP32 C.
+ *   Operands and precisions : as bfp_gemm (g = 16).
+ *   c_m_bits    : 1..8.  round_mode, seed, status_word : as bfp_quantize.
+ *   c_mant, c_exp : outputs sized by bfp_quantized_sizes(M, N, 16, c_m_bits).
+ * N must be a multiple of 16 (BFP_E_SHAPE otherwise).
+ */
+int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+                 int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int c_m_bits, int round_mode,
+                 uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status_word, void* stream);
+
+/*
  * bfp_gemm_group_partials -- the exact integer group dot products
  *   P[G][i][j] = sum_{k in G} qa'[i][k] * qb'[j][k]
  * (parts M and A of section III-B), qa' and qb' being the magnitudes at m_a and

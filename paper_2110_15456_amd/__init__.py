@@ -20,8 +20,8 @@ import torch
 
 from ._lib import BFPError, check, load
 
-__all__ = ["BFPTensor", "BFPError", "quantize", "dequantize", "gemm", "gemm_group_partials", "chunks",
-           "quantized_sizes", "ROUNDING"]
+__all__ = ["BFPTensor", "BFPError", "quantize", "dequantize", "gemm", "gemm_bfp", "gemm_group_partials",
+           "quantize_adaptive", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING"]
 
 ROUNDING = {"nearest": 0, "stochastic": 1, "truncate": 2}
 
@@ -209,6 +209,30 @@ def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = N
                           A.len, A.g, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0), _stream(A.device)),
           "bfp_gemm")
     return C
+
+
+def gemm_bfp(A: BFPTensor, B: BFPTensor, c_m: int, m_a: int | None = None, m_b: int | None = None,
+             rounding: str = "nearest", seed: int = 0, status: torch.Tensor | None = None,
+             out: BFPTensor | None = None) -> BFPTensor:
+    """C = A . B^T converted to BFP in the GEMM's epilogue: a [A.rows, B.rows]
+    BFP tensor with groups of 16 along each row of C at c_m bits, equal to
+    quantize(gemm(A, B), g=16, m=c_m, rounding, seed)."""
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    m_a, m_b = _gemm_args(A, B, m_a, m_b)
+    t = out if out is not None else BFPTensor.empty(A.rows, B.rows, 16, c_m, A.device)
+    if (t.rows, t.len, t.g, t.m) != (A.rows, B.rows, 16, c_m):
+        raise ValueError("out has the wrong shape or format")
+    st_ptr = None
+    if status is not None:
+        _need_cuda(status, "status")
+        st_ptr = ctypes.c_void_p(status.data_ptr())
+    check(load().bfp_gemm_bfp(ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
+                              ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows,
+                              B.rows, A.len, A.g, m_a, m_b, c_m, ROUNDING[rounding],
+                              ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(t.mant.data_ptr()),
+                              ctypes.c_void_p(t.exp.data_ptr()), st_ptr, _stream(A.device)), "bfp_gemm_bfp")
+    return t
 
 
 def gemm_group_partials(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = None) -> torch.Tensor:

@@ -116,6 +116,24 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
                                            static_cast<hipStream_t>(stream)));
 }
 
+int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+                 int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int c_m_bits, int round_mode,
+                 uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status_word, void* stream) {
+  int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
+  if (st != BFP_OK) return st;
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  st = check_tensor(M, N, 16, c_m_bits);
+  if (st != BFP_OK) return st;
+  if (M == 0 || N == 0) return BFP_OK;
+  if (!c_mant || !c_exp || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
+  if (!aligned(c_mant, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
+  if (g != 16) return BFP_E_UNSUPPORTED;
+  const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
+  return status_of(fastbfp::launch_gemm_mx_bfp(a_mant, a_exp, na, b_mant, b_exp, nb, M, N, K, 4 - m_a - m_b, c_m_bits,
+                                               round_mode, seed, c_mant, c_exp, status_word,
+                                               static_cast<hipStream_t>(stream)));
+}
+
 int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* b_mant, int b_m_bits, int64_t M,
                             int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream) {
   int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);

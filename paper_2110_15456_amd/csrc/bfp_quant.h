@@ -1,0 +1,120 @@
+// bfp_quant.h -- the FP32 -> BFP group converter (section III-A steps
+// (a)-(d); the converter of section V-C), shared by the quantize kernels and
+// the GEMM epilogue that converts its output.
+#pragma once
+#include "bfp_device.h"
+#include "launch.h"
+
+namespace fastbfp {
+
+// Signed chunk value as the float the FP6 converter takes: +-c * 0.5 (the
+// E2M3 code of c/2), with a zero magnitude as +0.0 so that it packs as code 0.
+// neg_half is -0.5 or +0.5 carrying the sign of the input value.
+__device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
+  return __builtin_fmaf((float)c, neg_half, 0.0f);  // 0 * -0.5 + 0 = +0
+}
+
+// Quantize one group whose FP32 bit patterns are in b[].  Writes the packed
+// chunk planes to w[plane][...] and the shared exponent to E_out; nonfinite is
+// set if any input was Inf/NaN.
+//
+// Alignment is done in floating point, exactly: with the shared exponent E,
+// one LSB is 2^(E-127-(m-1)), so a = |x| / LSB = ldexp(|x|, 127 + (m-1) - E)
+// is a power-of-two scaling of an FP32 value into [0, 2^m) and has no
+// rounding.  Truncating conversions to integer then implement the three
+// rounding rules exactly:
+//   truncate:   q = floor(a)
+//   nearest:    q = (floor(2a) + 1) >> 1           (half an LSB added, ties up)
+//   stochastic: q = (floor(256a) + U) >> 8         (U = the noise byte)
+// Subnormal inputs are read as zero (explicitly: the result does not depend
+// on the FP32 denormal mode of the including file).  Codes are produced by the gfx950
+// FP6 converter, which interleaves its two 16-value inputs: output value 2i is
+// a[i] / scale and 2i+1 is b[i] / scale.
+//
+// ADAPT (m = 4 only; section V-D and Eq. 2): plane 0 gets the 4-bit magnitude
+// q as one code, plane 1 (if NCH = 2) the 2-bit mantissa left when the low
+// chunk is discarded, q >> 2; s_lo and s_hi return the group's sums of q & 3
+// and q >> 2 (the magnitudes BFP(X,4) - BFP(X,2) and BFP(X,2) in units of
+// 2^(E-130) and 2^(E-128)).
+template <int G, int MODE, int NCH, bool ADAPT = false>
+__device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
+                                               uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
+                                               bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
+  s_lo = 0u;
+  s_hi = 0u;
+  // (a) shared exponent: the largest biased exponent field in the group.
+  uint32_t E = 0;
+#pragma unroll
+  for (int t = 0; t < G; ++t) E = max(E, (b[t] >> 23) & 0xFFu);
+  E_out = E;
+  nonfinite = (E == 255u);
+
+  uint32_t noise[G / 4];
+  if (MODE == kStochastic) {
+#pragma unroll
+    for (int blk = 0; blk < G / 16; ++blk) {
+      const uint4 r = philox4x32_10(make_uint4((uint32_t)gid, (uint32_t)(gid >> 32), (uint32_t)blk, 0u), key0, key1);
+      noise[4 * blk + 0] = r.x;
+      noise[4 * blk + 1] = r.y;
+      noise[4 * blk + 2] = r.z;
+      noise[4 * blk + 3] = r.w;
+    }
+  }
+
+  const uint32_t qmax = (1u << m) - 1u;
+  // (b) the exponent that aligns a value to the group's LSB (times 2 for
+  // nearest, 256 for stochastic rounding).
+  const int align = 127 + (int)m - 1 - (int)E + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
+  typedef float v16f __attribute__((ext_vector_type(16)));
+  v16f ev[NCH][G / 32 + (G % 32 != 0)], od[NCH][G / 32 + (G % 32 != 0)];
+#pragma unroll
+  for (int p = 0; p < NCH; ++p)
+#pragma unroll
+    for (int h = 0; h < G / 32 + (G % 32 != 0); ++h) {
+      ev[p][h] = v16f{};
+      od[p][h] = v16f{};
+    }
+#pragma unroll
+  for (int t = 0; t < G; ++t) {
+    const uint32_t abits = ((b[t] >> 23) & 0xFFu) ? (b[t] & 0x7FFFFFFFu) : 0u;  // subnormals read as zero
+    const float mag = __builtin_ldexpf(__uint_as_float(abits), align);
+    const uint32_t fl = (uint32_t)mag;  // truncating conversion: floor
+    uint32_t q;
+    if (MODE == kNearest) {
+      q = (fl + 1u) >> 1;
+    } else if (MODE == kTruncate) {
+      q = fl;
+    } else {
+      // (c) add the noise byte below the LSB, (d) truncate.
+      q = (fl + ((noise[t >> 2] >> (8 * (t & 3))) & 0xFFu)) >> 8;
+    }
+    q = min(q, qmax);  // a group maximum that rounds up to 2^m saturates
+    const float nh = __uint_as_float((b[t] & 0x80000000u) | 0x3F000000u);  // +-0.5
+    const int h = t / 32, k = (t % 32) / 2;
+    if (ADAPT) {
+      s_lo += q & 3u;
+      s_hi += q >> 2;
+      const float f4 = signed_half(q, nh), f2 = signed_half(q >> 2, nh);
+      if (t % 2 == 0) { ev[0][h][k] = f4; ev[NCH - 1][h][k] = NCH == 2 ? f2 : f4; }
+      else { od[0][h][k] = f4; od[NCH - 1][h][k] = NCH == 2 ? f2 : f4; }
+    } else if (NCH == 1) {
+      const float f = signed_half(q, nh);
+      if (t % 2 == 0) ev[0][h][k] = f; else od[0][h][k] = f;
+    } else {
+      const float fh = signed_half(q >> 4, nh), fl2 = signed_half(q & 15u, nh);
+      if (t % 2 == 0) { ev[0][h][k] = fh; ev[NCH - 1][h][k] = fl2; }
+      else { od[0][h][k] = fh; od[NCH - 1][h][k] = fl2; }
+    }
+  }
+  typedef uint32_t v6u __attribute__((ext_vector_type(6)));
+#pragma unroll
+  for (int p = 0; p < NCH; ++p)
+#pragma unroll
+    for (int h = 0; h < G / 32 + (G % 32 != 0); ++h) {
+      const v6u c = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev[p][h], od[p][h], 1.0f);
+#pragma unroll
+      for (int i = 0; i < 6 && 6 * h + i < G * 6 / 32; ++i) w[p][6 * h + i] = c[i];
+    }
+}
+
+}  // namespace fastbfp

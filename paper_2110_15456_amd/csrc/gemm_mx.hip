@@ -37,8 +37,7 @@
 // (2x2 waves) computes a 256x256 tile (128 along an operand with two chunk
 // planes); tiles are ordered so that neighbours share panels in L2 on the
 // same XCD.
-#include "bfp_device.h"
-#include "launch.h"
+#include "bfp_quant.h"
 
 namespace fastbfp {
 
@@ -180,12 +179,24 @@ __device__ __forceinline__ void prefetch_plane(uint8_t* lds_sink, rsrc_t rsrc, u
   }
 }
 
-template <class CF, bool EXP_FULL>
+// Where the epilogue puts C: FP32 rows (QNCH = 0), or BFP with groups of 16
+// along each row of C (the next GEMM's K) at c_m bits in QNCH chunk planes --
+// the converter of section V-C applied to the FP32 results in the epilogue.
+struct OutBFP {
+  uint8_t* mant0;
+  uint8_t* mant1;
+  uint8_t* exps;
+  uint32_t* status;
+  int m, mode;
+  uint32_t key0, key1;
+};
+
+template <class CF, bool EXP_FULL, int QNCH>
 __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
                                                  int64_t a_plane_stride, const uint8_t* __restrict__ b_mant,
                                                  const uint8_t* __restrict__ b_exp, int64_t b_plane_stride, int M,
                                                  int N, int ng, float scale, float* __restrict__ C, int64_t ldc,
-                                                 int tiles_m, int tiles_n) {
+                                                 int tiles_m, int tiles_n, OutBFP qo) {
   // Two stages as two LDS objects: the compiler then knows that the direct
   // loads into one stage do not alias the fragment reads of the other, and
   // does not wait for the next slab's loads before computing on this one.
@@ -428,33 +439,105 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   if (s < nslabs) step(stage0, stage1, s);
 
   // Epilogue: lane holds rows 4*lb + r, column lr of each 16x16 tile.
+  if constexpr (QNCH == 0) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = col0 + wc * CF::WN + j * 16 + lr;
+      for (int j = 0; j < TN; ++j) {
+        const int col = col0 + wc * CF::WN + j * 16 + lr;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = row0 + wr * CF::WM + i * 16 + lb * 4 + r;
-        if (row < M && col < N) C[(int64_t)row * ldc + col] = acc[i][j][r] * scale;
+        for (int r = 0; r < 4; ++r) {
+          const int row = row0 + wr * CF::WM + i * 16 + lb * 4 + r;
+          if (row < M && col < N) C[(int64_t)row * ldc + col] = acc[i][j][r] * scale;
+        }
       }
+  } else {
+    // Converted output.  A row group of C (16 consecutive columns) is spread
+    // over the 16 lanes of one lane block, so each wave stages one 16-row
+    // strip of its tile at a time in LDS (the stage memory, free now), and
+    // then every lane converts whole groups with the quantizer's converter:
+    // the same FP32 values and the same noise addressing (gid = the group's
+    // index in the output exponent array) as converting C separately.
+    constexpr int SROW = CF::WN + 4;  // strip row stride in floats (padding spreads the banks)
+    static_assert(4 * 16 * SROW * 4 <= CF::STAGE, "four strips fit in one stage");
+    // Every wave is done with the stages, and no direct load (the last
+    // steps' no-op loads included) can still write them.
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    float* strip = reinterpret_cast<float*>(stage0) + wave * (16 * SROW);
+    const int ngN = N / 16;
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) strip[(lb * 4 + r) * SROW + j * 16 + lr] = acc[i][j][r] * scale;
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's strip writes are done
+      __builtin_amdgcn_wave_barrier();
+      for (int gi = lane; gi < 16 * TN; gi += 64) {
+        const int rr = gi / TN, jj = gi % TN;
+        const int row = row0 + wr * CF::WM + i * 16 + rr;
+        const int gcol = (col0 + wc * CF::WN) / 16 + jj;
+        uint32_t b[16];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float4 v = *reinterpret_cast<const float4*>(&strip[rr * SROW + jj * 16 + 4 * k]);
+          b[4 * k] = __float_as_uint(v.x);
+          b[4 * k + 1] = __float_as_uint(v.y);
+          b[4 * k + 2] = __float_as_uint(v.z);
+          b[4 * k + 3] = __float_as_uint(v.w);
+        }
+        if (row < M && gcol < ngN) {
+          const int64_t gid = (int64_t)row * ngN + gcol;
+          uint32_t w[QNCH][16 * 6 / 32];
+          uint32_t E, s_lo, s_hi;
+          bool nonfinite;
+          if (qo.mode == kStochastic)
+            quantize_group<16, kStochastic, QNCH>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+                                                  s_lo, s_hi);
+          else if (qo.mode == kNearest)
+            quantize_group<16, kNearest, QNCH>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+                                               s_lo, s_hi);
+          else
+            quantize_group<16, kTruncate, QNCH>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+                                                s_lo, s_hi);
+          qo.exps[gid] = (uint8_t)E;
+#pragma unroll
+          for (int p = 0; p < QNCH; ++p)
+            *reinterpret_cast<uint3*>((p ? qo.mant1 : qo.mant0) + gid * 12) = make_uint3(w[p][0], w[p][1], w[p][2]);
+          bad |= nonfinite;
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // the strip's reads are done before the next strip overwrites it
+      __builtin_amdgcn_wave_barrier();
     }
+    if (qo.status && bad) atomicOr(qo.status, 1u);
+  }
 }
 
 template <class CF, bool EXP_FULL>
 static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
                               const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
-                              int64_t ldc, hipStream_t s) {
+                              int64_t ldc, const OutBFP* qo, hipStream_t s) {
   const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
-  hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL>), dim3((unsigned)(tiles_m * tiles_n)), dim3(mx::NT), 0, s, a_mant,
-                     a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, tiles_m, tiles_n);
+  const dim3 grid((unsigned)(tiles_m * tiles_n)), block(mx::NT);
+  if (!qo)
+    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
+                       ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
+  else if (qo->m > 4)
+    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 2>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
+                       ng, scale, C, ldc, tiles_m, tiles_n, *qo);
+  else
+    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 1>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
+                       ng, scale, C, ldc, tiles_m, tiles_n, *qo);
   return hipGetLastError();
 }
 
 template <int NA, int NB>
 static hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
                               const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
-                              int64_t ldc, hipStream_t s) {
+                              int64_t ldc, const OutBFP* qo, hipStream_t s) {
   // The tile shrinks along an operand with two chunk planes so that two LDS
   // stages fit in 160 KB.
   using CF = mx::Cfg<(NA == 1 && NB == 1) ? FASTBFP_MX11_BM : NA == 1 ? FASTBFP_MX_BM : FASTBFP_MX_BM / 2,
@@ -462,8 +545,24 @@ static hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64
   auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
   // direct exponent loads need full slabs and 4-byte aligned exponent rows
   const bool ef = ng % mx::KG == 0 && al(a_exp, 4) && al(b_exp, 4);
-  if (ef) return launch_mx_v<CF, true>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
-  return launch_mx_v<CF, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
+  if (ef) return launch_mx_v<CF, true>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  return launch_mx_v<CF, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+}
+
+static hipError_t launch_gemm_any(const uint8_t* a_mant, const uint8_t* a_exp, int na, const uint8_t* b_mant,
+                                  const uint8_t* b_exp, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+                                  float* C, int64_t ldc, const OutBFP* qo, hipStream_t s) {
+  if (M == 0 || N == 0) return hipSuccess;
+  const int ng = (int)(K / 16);
+  const int64_t a_ps = M * ng * 12, b_ps = N * ng * 12;
+  const float scale = ldexpf(1.0f, scale_log2);
+  if (na == 1 && nb == 1)
+    return launch_mx_t<1, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  if (na == 1 && nb == 2)
+    return launch_mx_t<1, 2>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  if (na == 2 && nb == 1)
+    return launch_mx_t<2, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  return launch_mx_t<2, 2>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
 }
 
 hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_planes, int na, const uint8_t* b_mant,
@@ -472,14 +571,15 @@ hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_pla
   (void)a_planes;
   (void)b_planes;
   (void)g;
-  if (M == 0 || N == 0) return hipSuccess;
-  const int ng = (int)(K / 16);
-  const int64_t a_ps = M * ng * 12, b_ps = N * ng * 12;
-  const float scale = ldexpf(1.0f, scale_log2);
-  if (na == 1 && nb == 1) return launch_mx_t<1, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
-  if (na == 1 && nb == 2) return launch_mx_t<1, 2>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
-  if (na == 2 && nb == 1) return launch_mx_t<2, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
-  return launch_mx_t<2, 2>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, s);
+  return launch_gemm_any(a_mant, a_exp, na, b_mant, b_exp, nb, M, N, K, scale_log2, C, ldc, nullptr, s);
+}
+
+hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int na, const uint8_t* b_mant,
+                              const uint8_t* b_exp, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+                              int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status,
+                              hipStream_t s) {
+  OutBFP qo{c_mant, c_mant + M * (N / 16) * 12, c_exp, status, c_m, mode, (uint32_t)seed, (uint32_t)(seed >> 32)};
+  return launch_gemm_any(a_mant, a_exp, na, b_mant, b_exp, nb, M, N, K, scale_log2, nullptr, N, &qo, s);
 }
 
 }  // namespace fastbfp

@@ -30,6 +30,12 @@ hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t r
 hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_planes, int na, const uint8_t* b_mant,
                           const uint8_t* b_exp, int b_planes, int nb, int64_t M, int64_t N, int64_t K, int g,
                           int scale_log2, float* C, int64_t ldc, hipStream_t s);
+// bfp_gemm with the output converted in the epilogue: groups of 16 along each
+// row of C at c_m bits (rounding mode and Philox seed as for quantize).
+hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int na, const uint8_t* b_mant,
+                              const uint8_t* b_exp, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+                              int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status,
+                              hipStream_t s);
 hipError_t launch_group_partials(const uint8_t* a_mant, int a_planes, int na, const uint8_t* b_mant, int b_planes,
                                  int nb, int64_t M, int64_t N, int64_t K, int g, int32_t* P, hipStream_t s);
 

@@ -194,3 +194,24 @@ def test_adaptive_sums_len(lib):
     assert lib.bfp_adaptive_sums_len(4, 32, 1, 16) == 4          # 8 groups: one workgroup of 256 groups
     assert lib.bfp_adaptive_sums_len(8192, 8192, 1, 16) == 2 + 2 * (8192 * 512 // 256)
     assert lib.bfp_adaptive_sums_len(512, 100, 0, 16) == 2 + 2 * (2 * 1)  # 2 column blocks x 1 group-row block
+
+
+def gb(lib, a=FAKE, ae=FAKE, am=4, b=FAKE, be=FAKE, bm=4, M=8, N=16, K=64, g=16, ma=4, mb=4, cm=4, mode=0,
+       cmant=FAKE, cexp=FAKE, st=None):
+    return lib.bfp_gemm_bfp(a, ae, am, b, be, bm, M, N, K, g, ma, mb, cm, mode, 0, cmant, cexp, st, None)
+
+
+def test_gemm_bfp_validation(lib):
+    assert gb(lib, a=None) == E_ARG
+    assert gb(lib, cmant=None) == E_ARG
+    assert gb(lib, cexp=None) == E_ARG
+    assert gb(lib, ae=None) == E_ARG
+    assert gb(lib, mode=3) == E_ARG
+    assert gb(lib, N=24) == E_SHAPE            # C's rows are grouped by 16
+    assert gb(lib, K=40) == E_SHAPE
+    assert gb(lib, cm=0) == E_PREC and gb(lib, cm=9) == E_PREC
+    assert gb(lib, am=8, ma=5) == E_PREC
+    assert gb(lib, g=32, K=64) == E_UNSUP
+    assert gb(lib, cmant=ctypes.c_void_p(0x100002)) == E_ARG
+    assert gb(lib, st=ctypes.c_void_p(0x100001)) == E_ARG
+    assert gb(lib, M=0) == OK and gb(lib, N=0) == OK

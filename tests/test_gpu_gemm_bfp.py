@@ -1,0 +1,122 @@
+"""GPU parity of bfp_gemm_bfp, the GEMM whose epilogue converts C to BFP
+(groups of 16 along each row of C; the converter of section V-C at the array
+output, section V-A).
+
+Two checks: (1) the fused output is bit-exact with converting the FP32 C of
+bfp_gemm separately (same values, same noise addressing); (2) against the
+oracle: its double-precision GEMM, rounded to FP32, then its quantizer.  The
+GPU's FP32 accumulation may differ from the oracle's C by up to 1e-6 * sum|T|
+(the GEMM tolerance), so an element's (E, q) is required to match exactly
+wherever the oracle gives the same (E, q) for C - tol, C and C + tol, and to
+be one of those three results elsewhere."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import bfp_codec
+import paper_2110_15456_amd as fb
+from paper_2110_15456_amd import synth
+from gpu_util import announce, THREADS
+
+pytestmark = pytest.mark.gpu
+MODES = ("nearest", "stochastic", "truncate")
+
+
+def operands(shape_a, shape_b, m_a, m_b, seed):
+    a = synth.draw("half_normal", shape_a, seed)
+    b = synth.draw("weights", shape_b, seed + 1)
+    A = fb.quantize(torch.from_numpy(a).cuda(), g=16, m=m_a)
+    B = fb.quantize(torch.from_numpy(b).cuda(), g=16, m=m_b)
+    return a, b, A, B
+
+
+def decode(t):
+    q = bfp_codec.decode(t.mant.cpu().numpy(), t.rows, t.len, t.m)
+    return q, t.exp.cpu().numpy()
+
+
+@pytest.mark.parametrize("mm", [(4, 4), (2, 4), (6, 6), (4, 8), (8, 4)])
+@pytest.mark.parametrize("shape", [(300, 208, 512), (256, 256, 4096), (130, 48, 576), (17, 16, 16)])
+def test_fused_equals_separate_conversion(mm, shape):
+    m_a, m_b = mm
+    M, N, K = shape
+    _, _, A, B = operands((M, K), (N, K), m_a, m_b, 4000 + M + N + K)
+    C = fb.gemm(A, B)
+    for c_m in (1, 2, 4, 6, 8):
+        for mode in MODES:
+            announce("gemm_bfp %dx%dx%d (%d,%d) -> m=%d %s" % (M, N, K, m_a, m_b, c_m, mode))
+            st = torch.zeros(1, dtype=torch.int32, device="cuda")
+            T = fb.gemm_bfp(A, B, c_m, rounding=mode, seed=99, status=st)
+            R = fb.quantize(C, g=16, m=c_m, rounding=mode, seed=99)
+            torch.cuda.synchronize()
+            assert int(st.item()) == 0
+            assert torch.equal(T.exp, R.exp), "exponents differ"
+            assert torch.equal(T.mant, R.mant), "mantissas differ"
+
+
+@pytest.mark.parametrize("mm", [(4, 4), (6, 6), (2, 8)])
+@pytest.mark.parametrize("mode", MODES)
+def test_fused_against_oracle(mm, mode):
+    m_a, m_b = mm
+    M, N, K = 96, 160, 1024
+    a, b, A, B = operands((M, K), (N, K), m_a, m_b, 4100 + m_a * 10 + m_b)
+    qa, ea, _ = oracle.quantize(a, g=16, m=m_a)
+    qb, eb, _ = oracle.quantize(b, g=16, m=m_b)
+    Co, S = oracle.gemm(qa, ea, m_a, qb, eb, m_b, g=16, threads=THREADS)
+    tol = 1e-6 * S
+    for c_m in (2, 4, 8):
+        announce("gemm_bfp vs oracle (%d,%d) -> m=%d %s" % (m_a, m_b, c_m, mode))
+        T = fb.gemm_bfp(A, B, c_m, rounding=mode, seed=7)
+        q, E = decode(T)
+        var = []
+        for d in (-1.0, 0.0, 1.0):
+            x = (Co + d * tol).astype(np.float32)
+            qo, eo, _ = oracle.quantize(x, g=16, m=c_m, mode=mode, seed=7)
+            var.append((qo, np.repeat(eo, 16, axis=1)))
+        Ee = np.repeat(E, 16, axis=1)
+        stable = ((var[0][0] == var[1][0]) & (var[1][0] == var[2][0]) &
+                  (var[0][1] == var[1][1]) & (var[1][1] == var[2][1]))
+        assert stable.mean() > 0.95
+        assert np.array_equal(q[stable], var[1][0][stable]) and np.array_equal(Ee[stable], var[1][1][stable])
+        ok = np.zeros_like(stable)
+        for qo, eo in var:
+            ok |= (q == qo) & (Ee == eo)
+        assert ok.all(), "unstable elements outside the perturbed results: %d" % (~ok).sum()
+
+
+def test_fused_edges():
+    # all-zero product: every group has E = 0 and q = 0
+    announce("gemm_bfp zero operand")
+    z = torch.zeros((64, 256), dtype=torch.float32, device="cuda")
+    A = fb.quantize(z, g=16, m=4)
+    _, _, _, B = operands((64, 256), (48, 256), 4, 4, 4200)
+    T = fb.gemm_bfp(A, B, 4)
+    assert int(T.exp.max()) == 0 and int(T.mant.max()) == 0
+    # N not a multiple of 16 is a shape error
+    _, _, A2, B2 = operands((32, 64), (40, 64), 4, 4, 4201)
+    with pytest.raises(fb.BFPError):
+        fb.gemm_bfp(A2, B2, 4)
+
+
+def test_fused_full_size_sampled():
+    """The FFN up-projection shape (8192 x 16384 x 4096, (4,4) -> m=4, SR):
+    equal to the separate conversion on sampled row blocks."""
+    announce("gemm_bfp ffn_up sampled")
+    M, N, K = 8192, 16384, 4096
+    x = torch.from_numpy(synth.draw("normal", (M, K), 41)).cuda()
+    w = torch.from_numpy(synth.draw("weights", (N, K), 42)).cuda()
+    A, B = fb.quantize(x, g=16, m=4), fb.quantize(w, g=16, m=4)
+    del x, w
+    T = fb.gemm_bfp(A, B, 4, rounding="stochastic", seed=5)
+    C = fb.gemm(A, B)
+    R = fb.quantize(C, g=16, m=4, rounding="stochastic", seed=5)
+    torch.cuda.synchronize()
+    assert torch.equal(T.exp, R.exp)
+    nb = N // 16 * 12
+    tm, rm = T.mant.view(M, nb), R.mant.view(M, nb)
+    rows = torch.from_numpy(np.random.default_rng(1).choice(M, 256, replace=False)).cuda()
+    assert torch.equal(tm[rows], rm[rows])
+    assert torch.equal(T.mant, R.mant)
