@@ -39,10 +39,16 @@ def planes(m):
     return 1 if m <= 4 else 2
 
 
+def code_bits(m):
+    """Mantissa bits per value: 4-bit codes for a chunk of at most 2 bits, 6-bit
+    codes otherwise (plane 0 of m = 1, 2, 5, 6 is the 4-bit one)."""
+    return {1: 4, 2: 4, 3: 6, 4: 6, 5: 10, 6: 10, 7: 12, 8: 12}[m]
+
+
 def q_bytes(n_elems, m, g=G):
     """Algorithmic HBM bytes of one quantization: read FP32, write the chunk
-    planes (6 bits per value each) and one exponent byte per group."""
-    return n_elems * (4 + 0.75 * planes(m) + 1.0 / g)
+    planes and one exponent byte per group."""
+    return n_elems * (4 + code_bits(m) / 8.0 + 1.0 / g)
 
 
 def parse():
@@ -199,7 +205,7 @@ def quantize_sweep(torch, fb, synth, dev, args):
         z.record()
         torch.cuda.synchronize()
         ms = a.elapsed_time(z) / reps
-        gbs = n * (4 + 0.75 * 2 + 1.0 / G) / (ms * 1e-3) / 1e9
+        gbs = n * (4 + 0.75 + 0.5 + 1.0 / G) / (ms * 1e-3) / 1e9
         out["adaptive_m4m2_%s" % mode] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
                                           "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
         log(args, "adaptive m=4/2 %s: %.1f us, %.0f GB/s" % (mode, ms * 1e3, gbs))

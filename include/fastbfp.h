@@ -32,18 +32,28 @@
  *          One unit in the last place of the group is 2^(E - 127 - (m-1)).
  *   mant : chunk planes.  A magnitude q in [0, 2^m - 1] is split into 4-bit
  *          chunks, most significant first: one chunk (q itself) when m <= 4,
- *          two (hi = q >> 4, lo = q & 15) when 5 <= m <= 8.  Plane c holds
- *          chunk c of every value, with the value's sign, as the OCP FP6 E2M3
- *          code of (+-chunk / 2): every integer 0..15 halved is exact in E2M3.
- *          Codes are packed little-endian, 6 bits per value (value t of a
- *          group at bits 6t..6t+5), so a group takes 3g/4 bytes per plane:
- *            plane c, row r, group G at byte offset
- *            ((c * rows + r) * (len/g) + G) * (3g/4).
+ *          two (hi = q >> 4, which has m - 4 bits, and lo = q & 15) when
+ *          5 <= m <= 8.  Plane c holds chunk c of every value, with the
+ *          value's sign, as the code of (+-chunk / 2) in the narrowest OCP MX
+ *          element format that holds it exactly:
+ *            FP4 E2M1 (4 bits: the sign, then the chunk itself in the three
+ *              low bits) for a chunk of at most 2 bits, i.e. plane 0 when m
+ *              is 1, 2, 5 or 6;
+ *            FP6 E2M3 (6 bits) otherwise: every integer 0..15 halved is exact.
+ *          Codes are packed little-endian, w bits per value (value t of a
+ *          group at bits w*t .. w*t + w - 1; w = 4 or 6), so a group takes
+ *          B_c = g/2 (FP4) or 3g/4 (FP6) bytes in plane c:
+ *            plane 0, row r, group G at byte offset (r * (len/g) + G) * B_0,
+ *            plane 1 at rows * (len/g) * B_0 + (r * (len/g) + G) * B_1.
  *          A zero magnitude is stored as code 0 (no sign).
- *          This is the paper's chunk-plane storage (section V-D) with a chunk
- *          width of 4 bits, the width that gfx950's block-scaled MFMA consumes
- *          at its full FP6 rate; the lower chunk's scale is 2^4 below the upper
- *          chunk's, as the paper decrements the lower 2-bit chunk's exponent.
+ *          This is the paper's chunk-plane storage (section V-D) with 4-bit
+ *          chunks, the width gfx950's block-scaled MFMA consumes at its full
+ *          FP6/FP4 rate; a chunk of at most 2 bits is the paper's sign plus
+ *          2-bit chunk, kept in a 4-bit code (the paper packs it in 3 bits;
+ *          the matrix cores read 4).  The lower chunk's scale is 2^4 below the
+ *          upper chunk's, as the paper decrements the lower 2-bit chunk's
+ *          exponent.  Bits per value at g = 16, exponent included: 4.5
+ *          (m <= 2), 6.5 (m = 3, 4), 10.5 (m = 5, 6), 12.5 (m = 7, 8).
  */
 #ifndef FASTBFP_H
 #define FASTBFP_H
@@ -55,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FASTBFP_ABI_VERSION 2
+#define FASTBFP_ABI_VERSION 3
 
 typedef enum {
   BFP_ROUND_NEAREST = 0,    /* add half an LSB, then truncate (ties away from zero) */
@@ -193,8 +203,9 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
  * so that r(X) = sums[0] / sums[1] (Eq. 2).
  *   x, R, C, group_axis, g, round_mode, seed, status_word : as bfp_quantize.
  *   mant4, exp  : the m = 4 tensor (layout of bfp_quantize, m_bits = 4).
- *   mant2       : optional (may be NULL): the m = 2 tensor's mantissas, same
- *                 size as mant4; it shares exp.  Either tensor can be handed to
+ *   mant2       : optional (may be NULL): the m = 2 tensor's mantissas (layout
+ *                 of bfp_quantize, m_bits = 2: one plane of 4-bit codes, two
+ *                 thirds of mant4's size); it shares exp.  Either tensor can be handed to
  *                 bfp_gemm (m_bits 4 or 2) without converting again.
  *   sums        : device doubles, bfp_adaptive_sums_len(R, C, group_axis, g)
  *                 of them (8-byte aligned): sums[0] and sums[1] receive the two

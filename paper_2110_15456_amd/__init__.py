@@ -145,7 +145,10 @@ def quantize_adaptive(x: torch.Tensor, group_axis: int = -1, g: int = 16, roundi
     else:
         raise ValueError("group_axis must be the last axis, or 0 of a 2-D tensor")
     t4 = BFPTensor.empty(rows, length, g, 4, x.device)
-    t2 = BFPTensor(torch.empty_like(t4.mant), t4.exp, rows, length, g, 2) if with_m2 else None
+    t2 = None
+    if with_m2:  # its own (4-bit code) mantissa plane, sharing t4's exponents
+        t2 = BFPTensor(torch.empty(quantized_sizes(rows, length, g, 2)[0], dtype=torch.uint8, device=x.device), t4.exp,
+                       rows, length, g, 2)
     lib = load()
     n_sums = lib.bfp_adaptive_sums_len(R, C, axis_flag, g)
     if n_sums < 2:

@@ -33,7 +33,7 @@ SIGNATURES = {
     "bfp_adaptive_threshold": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, _I64, _I64, _I64, _I64]),
     "bfp_adaptive_mantissa": (_I, [ctypes.c_double, ctypes.c_double, ctypes.c_double]),
 }
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 _lock = threading.Lock()
 _lib = None

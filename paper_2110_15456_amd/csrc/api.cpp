@@ -70,7 +70,9 @@ int bfp_quantized_sizes(int64_t rows, int64_t len, int g, int m_bits, size_t* ma
   if (!mant_bytes || !exp_bytes) return BFP_E_ARG;
   const int st = check_tensor(rows, len, g, m_bits);
   if (st != BFP_OK) return st;
-  *mant_bytes = (size_t)bfp_chunks(m_bits) * (size_t)rows * (size_t)len * 3 / 4;
+  size_t per_group = 0;
+  for (int p = 0; p < bfp_chunks(m_bits); ++p) per_group += (size_t)fastbfp::plane_group_bytes(g, m_bits, p);
+  *mant_bytes = per_group * (size_t)rows * (size_t)(len / g);
   *exp_bytes = (size_t)rows * (size_t)(len / g);
   return BFP_OK;
 }
@@ -111,9 +113,8 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
   if (!C || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
   if (g != 16) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
-  return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, bfp_chunks(a_m_bits), na, b_mant, b_exp,
-                                           bfp_chunks(b_m_bits), nb, M, N, K, g, 4 - m_a - m_b, C, ldc,
-                                           static_cast<hipStream_t>(stream)));
+  return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K,
+                                           4 - m_a - m_b, C, ldc, static_cast<hipStream_t>(stream)));
 }
 
 int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
@@ -129,8 +130,8 @@ int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, cons
   if (!aligned(c_mant, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
   if (g != 16) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
-  return status_of(fastbfp::launch_gemm_mx_bfp(a_mant, a_exp, na, b_mant, b_exp, nb, M, N, K, 4 - m_a - m_b, c_m_bits,
-                                               round_mode, seed, c_mant, c_exp, status_word,
+  return status_of(fastbfp::launch_gemm_mx_bfp(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K,
+                                               4 - m_a - m_b, c_m_bits, round_mode, seed, c_mant, c_exp, status_word,
                                                static_cast<hipStream_t>(stream)));
 }
 
@@ -142,8 +143,8 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
   if (!P) return BFP_E_ARG;
   if ((M + 31) / 32 > 65535 || K / g > 65535) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
-  return status_of(fastbfp::launch_group_partials(a_mant, bfp_chunks(a_m_bits), na, b_mant, bfp_chunks(b_m_bits), nb,
-                                                  M, N, K, g, P, static_cast<hipStream_t>(stream)));
+  return status_of(fastbfp::launch_group_partials(a_mant, a_m_bits, na, b_mant, b_m_bits, nb, M, N, K, g, P,
+                                                  static_cast<hipStream_t>(stream)));
 }
 
 int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode, uint64_t seed,

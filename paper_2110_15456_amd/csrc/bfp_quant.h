@@ -27,19 +27,24 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
 //   nearest:    q = (floor(2a) + 1) >> 1           (half an LSB added, ties up)
 //   stochastic: q = (floor(256a) + U) >> 8         (U = the noise byte)
 // Subnormal inputs are read as zero (explicitly: the result does not depend
-// on the FP32 denormal mode of the including file).  Codes are produced by the gfx950
-// FP6 converter, which interleaves its two 16-value inputs: output value 2i is
-// a[i] / scale and 2i+1 is b[i] / scale.
+// on the FP32 denormal mode of the including file).
+//
+// Plane formats: F0 / F1 true makes plane 0 / 1 an FP4 E2M1 plane (chunks of
+// at most 2 bits: the code is the sign bit above the chunk itself, 4 bits per
+// value, G/8 words); otherwise an FP6 E2M3 plane (3G/16 words), whose codes
+// come from the gfx950 FP6 converter.  That converter interleaves its two
+// 16-value inputs: output value 2i is a[i] / scale and 2i+1 is b[i] / scale.
 //
 // ADAPT (m = 4 only; section V-D and Eq. 2): plane 0 gets the 4-bit magnitude
 // q as one code, plane 1 (if NCH = 2) the 2-bit mantissa left when the low
 // chunk is discarded, q >> 2; s_lo and s_hi return the group's sums of q & 3
 // and q >> 2 (the magnitudes BFP(X,4) - BFP(X,2) and BFP(X,2) in units of
 // 2^(E-130) and 2^(E-128)).
-template <int G, int MODE, int NCH, bool ADAPT = false>
+template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1>
 __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
                                                uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
                                                bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
+  constexpr bool FP4[2] = {F0, F1};
   s_lo = 0u;
   s_hi = 0u;
   // (a) shared exponent: the largest biased exponent field in the group.
@@ -66,14 +71,18 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
   // nearest, 256 for stochastic rounding).
   const int align = 127 + (int)m - 1 - (int)E + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
   typedef float v16f __attribute__((ext_vector_type(16)));
-  v16f ev[NCH][G / 32 + (G % 32 != 0)], od[NCH][G / 32 + (G % 32 != 0)];
+  constexpr int NH = G / 32 + (G % 32 != 0);
+  v16f ev[NCH][NH], od[NCH][NH];
 #pragma unroll
-  for (int p = 0; p < NCH; ++p)
+  for (int p = 0; p < NCH; ++p) {
 #pragma unroll
-    for (int h = 0; h < G / 32 + (G % 32 != 0); ++h) {
+    for (int h = 0; h < NH; ++h) {
       ev[p][h] = v16f{};
       od[p][h] = v16f{};
     }
+#pragma unroll
+    for (int i = 0; i < G * 6 / 32; ++i) w[p][i] = 0u;
+  }
 #pragma unroll
   for (int t = 0; t < G; ++t) {
     const uint32_t abits = ((b[t] >> 23) & 0xFFu) ? (b[t] & 0x7FFFFFFFu) : 0u;  // subnormals read as zero
@@ -89,32 +98,61 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
       q = (fl + ((noise[t >> 2] >> (8 * (t & 3))) & 0xFFu)) >> 8;
     }
     q = min(q, qmax);  // a group maximum that rounds up to 2^m saturates
-    const float nh = __uint_as_float((b[t] & 0x80000000u) | 0x3F000000u);  // +-0.5
-    const int h = t / 32, k = (t % 32) / 2;
     if (ADAPT) {
       s_lo += q & 3u;
       s_hi += q >> 2;
-      const float f4 = signed_half(q, nh), f2 = signed_half(q >> 2, nh);
-      if (t % 2 == 0) { ev[0][h][k] = f4; ev[NCH - 1][h][k] = NCH == 2 ? f2 : f4; }
-      else { od[0][h][k] = f4; od[NCH - 1][h][k] = NCH == 2 ? f2 : f4; }
+    }
+    // the chunk of each plane
+    uint32_t c[2];
+    if (ADAPT) {
+      c[0] = q;
+      c[1] = q >> 2;
     } else if (NCH == 1) {
-      const float f = signed_half(q, nh);
-      if (t % 2 == 0) ev[0][h][k] = f; else od[0][h][k] = f;
+      c[0] = q;
+      c[1] = 0u;
     } else {
-      const float fh = signed_half(q >> 4, nh), fl2 = signed_half(q & 15u, nh);
-      if (t % 2 == 0) { ev[0][h][k] = fh; ev[NCH - 1][h][k] = fl2; }
-      else { od[0][h][k] = fh; od[NCH - 1][h][k] = fl2; }
+      c[0] = q >> 4;
+      c[1] = q & 15u;
+    }
+    const float nh = __uint_as_float((b[t] & 0x80000000u) | 0x3F000000u);  // +-0.5
+    const uint32_t sgn = (b[t] >> 28) & 8u;                                  // the FP4 sign bit
+    const int h = t / 32, k = (t % 32) / 2;
+#pragma unroll
+    for (int p = 0; p < NCH; ++p) {
+      if (FP4[p]) {
+        w[p][t >> 3] |= (c[p] ? (sgn | c[p]) : 0u) << (4 * (t & 7));
+      } else {
+        const float f = signed_half(c[p], nh);
+        if (t % 2 == 0) ev[p][h][k] = f; else od[p][h][k] = f;
+      }
     }
   }
   typedef uint32_t v6u __attribute__((ext_vector_type(6)));
 #pragma unroll
-  for (int p = 0; p < NCH; ++p)
+  for (int p = 0; p < NCH; ++p) {
+    if (FP4[p]) continue;
 #pragma unroll
-    for (int h = 0; h < G / 32 + (G % 32 != 0); ++h) {
-      const v6u c = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev[p][h], od[p][h], 1.0f);
+    for (int h = 0; h < NH; ++h) {
+      const v6u cv = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev[p][h], od[p][h], 1.0f);
 #pragma unroll
-      for (int i = 0; i < 6 && 6 * h + i < G * 6 / 32; ++i) w[p][6 * h + i] = c[i];
+      for (int i = 0; i < 6 && 6 * h + i < G * 6 / 32; ++i) w[p][6 * h + i] = cv[i];
     }
+  }
+}
+
+// Stores plane p's codes of group gid (from quantize_group) at
+// mant_p + gid * bytes-per-group: 8 or 12 bytes per 16 values.
+template <int G, bool FP4>
+__device__ __forceinline__ void store_plane(uint8_t* __restrict__ mant, int64_t gid, const uint32_t* w) {
+  if (FP4) {
+    uint2* dst = reinterpret_cast<uint2*>(mant + gid * (G / 2));
+#pragma unroll
+    for (int i = 0; i < G / 16; ++i) dst[i] = make_uint2(w[2 * i], w[2 * i + 1]);
+  } else {
+    uint3* dst = reinterpret_cast<uint3*>(mant + gid * (G * 3 / 4));
+#pragma unroll
+    for (int i = 0; i < G / 16; ++i) dst[i] = make_uint3(w[3 * i], w[3 * i + 1], w[3 * i + 2]);
+  }
 }
 
 }  // namespace fastbfp

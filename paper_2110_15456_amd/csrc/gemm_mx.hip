@@ -1,585 +1,71 @@
-// gemm_mx.hip -- the variable-precision BFP GEMM on gfx950's block-scaled MFMA
-// (section III-B dot product; fMAC of section V-B).
-//
-// C[M][N] = A[M][K] * B[N][K]^T, both operands BFP with groups of 16 along K,
-// stored as FP6 E2M3 chunk planes (value +-chunk/2, 12 bytes per group) and
-// one exponent byte per group.
-//
-// What the fMAC does per group pair -- g integer products, an adder tree, one
-// exponent addition, conversion to FP and an FP32 accumulation -- is what one
-// v_mfma_scale_f32_16x16x128_f8f6f4 does per 32-value block: the FP6 products
-// of 4-bit chunks are exact, the block sum is scaled by 2^(sa-127) * 2^(sb-127)
-// with the shared exponents as the E8M0 block scales, and the result is added
-// to an FP32 accumulator.  The hardware block is 32 values and a BFP group is
-// 16, so each lane's block carries one group followed by 16 zeros on the A
-// side (whatever follows on the B side meets those zeros; FP6 has no NaN or
-// Inf encodings).  One instruction thus covers 4 groups of K, one per lane
-// block.
-//
-// Variable precision (section V-B): an m-bit magnitude is one 4-bit chunk when
-// m <= 4 and two when m > 4; each chunk-plane pair (ca, cb) is one pass of
-// MFMAs over the group with the chunk's scale raised by 4 per chunk of
-// significance (the paper lowers the exponent of the lower chunk instead; both
-// give the same weights).  Passes per group pair = chunks(m_a) * chunks(m_b).
-// The one remaining constant factor, 2^(4 - m_a - m_b) (the E2M3 halving of
-// both operands and the (m-1) in the LSB), is applied exactly in the epilogue.
-//
-// Staging: every group of a K slab (8 groups) occupies a 16-byte LDS slot
-// filled by a direct buffer->LDS 12-byte load, which leaves the slot's last
-// dword untouched; those dwords are zeroed once, so a slot read is exactly the
-// first four dwords of the zero-padded A operand (the last two are zero
-// registers).  The slot order within a row is XOR-swizzled by the row so that
-// the 16-byte fragment reads of 16 rows hit all 64 banks, while each load
-// instruction still reads whole 96-byte runs of 8 rows.  Slabs are double
-// buffered in two LDS objects: the loads of slab s+1 are issued right after
-// the barrier that publishes slab s and have all of slab s's MFMAs to land,
-// and slab s+2 is touched in L2 at the same time.  A 256-thread workgroup
-// (2x2 waves) computes a 256x256 tile (128 along an operand with two chunk
-// planes); tiles are ordered so that neighbours share panels in L2 on the
-// same XCD.
-#include "bfp_quant.h"
+// gemm_mx.hip -- dispatch of the BFP GEMM (kernel in gemm_mx.h) over the
+// operand formats: chunk planes read per operand (1 or 2) and whether the
+// first plane holds FP4 codes.  Each plane-count pair is instantiated in its
+// own file (gemm_mx_{11,12,21,22}.hip) so that they compile in parallel.
+#include "gemm_mx.h"
 
 namespace fastbfp {
 
-namespace mx {
-#ifndef FASTBFP_MX_BM
-#define FASTBFP_MX_BM 256
-#endif
-#ifndef FASTBFP_MX_BN
-#define FASTBFP_MX_BN 256
-#endif
-#ifndef FASTBFP_MX_PIPE11
-#define FASTBFP_MX_PIPE11 1
-#endif
-#ifndef FASTBFP_MX11_BM
-#define FASTBFP_MX11_BM FASTBFP_MX_BM
-#endif
-#ifndef FASTBFP_MX11_BN
-#define FASTBFP_MX11_BN FASTBFP_MX_BN
-#endif
-constexpr int WGM = 2, WGN = 2;  // wave grid along M and N
-constexpr int NT = 64 * WGM * WGN;
-constexpr int KG = 8;            // groups per K slab (two MFMA K-steps)
-template <int BM_, int BN_, int NA_, int NB_>
-struct Cfg {
-  static constexpr int BM = BM_, BN = BN_, NA = NA_, NB = NB_;
-  static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
-  static constexpr int TM = WM / 16, TN = WN / 16;    // 16x16 MFMA tiles per wave
-  static constexpr int PLANE_A = BM * KG * 16, PLANE_B = BN * KG * 16;  // slot bytes per plane
-  static constexpr int OFF_B = NA * PLANE_A;
-  static constexpr int OFF_EA = OFF_B + NB * PLANE_B;
-  static constexpr int OFF_EB = OFF_EA + BM * KG;
-  static constexpr int SPARE = OFF_EB + BN * KG;  // 8 bytes written by threads without an exponent row
-  static constexpr int STAGE = SPARE + 16;
-  static constexpr int EXP_ROWS_PER_T = (BM + BN + NT - 1) / NT;
-  // Explicitly software-pipelined fragment reads (one chunk per operand);
-  // otherwise the compiler schedules them.
-  static constexpr bool PIPE = FASTBFP_MX_PIPE11 && NA == 1 && NB == 1;
-  static_assert(TM * 16 * WGM == BM && TN * 16 * WGN == BN, "wave tiles cover the tile");
-  static_assert((BM + BN) % 64 == 0 && (BM * KG) % (64 * 4) == 0 && (BN * KG) % (64 * 4) == 0,
-                "loads split evenly over the waves; whole waves skip exponent rows past BM + BN");
-  static_assert(2 * STAGE <= 160 * 1024, "two stages fit in LDS");
-};
-// Slot of group g (0..7) of row r within a plane: rows of 8 slots, the group
-// index XOR-ed with (r >> 1) & 7.
-__device__ __forceinline__ int slot_of(int r, int g) { return r * KG + (g ^ ((r >> 1) & 7)); }
-}  // namespace mx
-
-// Workgroup id -> (tile_m, tile_n).  Dispatch places consecutive workgroup ids
-// on consecutive XCDs; the remap gives each XCD a contiguous run of logical
-// tiles, and logical tiles are walked in column-major groups of GROUP_M tile
-// rows so that concurrently running workgroups share A and B panels in L2.
-__device__ __forceinline__ void tile_of(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
-  constexpr int NXCD = 8, GROUP_M = 8;
-  int lid = bid;
-  if (nblocks % NXCD == 0) lid = (bid % NXCD) * (nblocks / NXCD) + bid / NXCD;
-  const int per_group = GROUP_M * tiles_n;
-  const int grp = lid / per_group;
-  const int first_m = grp * GROUP_M;
-  const int rows_in_group = min(tiles_m - first_m, GROUP_M);
-  const int in = lid % per_group;
-  tm = first_m + in % rows_in_group;
-  tn = in / rows_in_group;
-}
-
-// Exponents of one slab for one row (8 bytes), zero past the last group and
-// for rows past the end.
-__device__ __forceinline__ uint2 load_exps(const uint8_t* __restrict__ exps, int row, int row_end, int ng, int slab) {
-  const bool rok = row < row_end;
-  const int64_t base = (int64_t)(rok ? row : 0) * ng + slab * mx::KG;
-  const int gvalid = min(mx::KG, ng - slab * mx::KG);
-  uint32_t w[2] = {0u, 0u};
-#pragma unroll
-  for (int j = 0; j < mx::KG; ++j) {
-    const uint32_t b = exps[base + min(j, gvalid - 1)];
-    w[j >> 2] |= ((rok && j < gvalid) ? b : 0u) << (8 * (j & 3));
-  }
-  return make_uint2(w[0], w[1]);
-}
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-
-// Buffer resource over [p, p + bytes): loads at offsets past the end read
-// zero instead of faulting.  (Third dword: the gfx9 raw-buffer format.)
-__device__ __forceinline__ rsrc_t make_rsrc(const uint8_t* p, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p), (short)0, (int)bytes, 0x00020000);
-}
-
-// Direct buffer->LDS loads of one slab of one operand plane: ROWS rows x 8
-// groups, i.e. ROWS * 8 / 64 load instructions of 64 slots, spread over the
-// four waves.  The resource starts at the tile's first row and ends at its
-// last valid one, so rows past the end read zero.  Instruction blk covers
-// rows 8 blk .. 8 blk + 7; a wave's instructions all have the parity of its
-// index, so the lane's part of the offset (row within the 8, swizzled group)
-// is one register, lane_off.  RAGGED: groups past K get an offset past the
-// resource and read zero.
-template <int ROWS, bool RAGGED>
-__device__ __forceinline__ void load_plane(uint8_t* lds_plane, rsrc_t rsrc, uint32_t lane_off, uint32_t row_bytes,
-                                           int slab, bool g_ok, int wave) {
-  constexpr int INSTR = ROWS * mx::KG / 64;
-#pragma unroll
-  for (int u = 0; u < INSTR / 4; ++u) {
-    const int blk = wave + 4 * u;
-    uint32_t off = lane_off + (uint32_t)blk * 8u * row_bytes + (uint32_t)slab * (mx::KG * 12);
-    if (RAGGED && !g_ok) off = 0x80000000u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_plane + blk * 64 * 16), 12, off, 0, 0, 0);
-  }
-}
-
-// Direct buffer->LDS loads of one full slab of exponents (8 bytes per row, as
-// two dwords) for ROWS rows: row r lands at lds_exps + 8 r.  lane_off is
-// (lane / 2) * ng + (lane % 2) * 4.
-template <int ROWS>
-__device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, uint32_t lane_off, int ng, int slab,
-                                              int wave) {
-  constexpr int INSTR = ROWS * 2 / 64;
-  static_assert(INSTR % 4 == 0, "exponent loads split evenly over the waves");
-#pragma unroll
-  for (int u = 0; u < INSTR / 4; ++u) {
-    const int blk = wave + 4 * u;
-    const uint32_t off = lane_off + (uint32_t)blk * 32u * (uint32_t)ng + (uint32_t)slab * mx::KG;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_exps + blk * 256), 4, off, 0, 0, 0);
-  }
-}
-
-// L2 prefetch of one slab of one operand plane, two slabs ahead of use: each
-// row's 96-byte run is touched at its first and last dword (the one or two
-// 128-byte lines it spans) by a direct load into a sink that is never read.
-// ROWS rows take 2 * ROWS / 256 instructions per wave.
-template <int ROWS>
-__device__ __forceinline__ void prefetch_plane(uint8_t* lds_sink, rsrc_t rsrc, uint32_t row_bytes, int slab, int tid) {
-  static_assert((2 * ROWS) % mx::NT == 0, "touches split evenly over the threads");
-#pragma unroll
-  for (int u = 0; u < 2 * ROWS / mx::NT; ++u) {
-    const int t = tid + u * mx::NT;
-    const uint32_t off = (uint32_t)(t >> 1) * row_bytes + (uint32_t)slab * (mx::KG * 12) + (uint32_t)(t & 1) * 92u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)lds_sink, 4, off, 0, 0, 0);
-  }
-}
-
-// Where the epilogue puts C: FP32 rows (QNCH = 0), or BFP with groups of 16
-// along each row of C (the next GEMM's K) at c_m bits in QNCH chunk planes --
-// the converter of section V-C applied to the FP32 results in the epilogue.
-struct OutBFP {
-  uint8_t* mant0;
-  uint8_t* mant1;
-  uint8_t* exps;
-  uint32_t* status;
-  int m, mode;
-  uint32_t key0, key1;
-};
-
-template <class CF, bool EXP_FULL, int QNCH>
-__global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
-                                                 int64_t a_plane_stride, const uint8_t* __restrict__ b_mant,
-                                                 const uint8_t* __restrict__ b_exp, int64_t b_plane_stride, int M,
-                                                 int N, int ng, float scale, float* __restrict__ C, int64_t ldc,
-                                                 int tiles_m, int tiles_n, OutBFP qo) {
-  // Two stages as two LDS objects: the compiler then knows that the direct
-  // loads into one stage do not alias the fragment reads of the other, and
-  // does not wait for the next slab's loads before computing on this one.
-  __shared__ __attribute__((aligned(16))) uint8_t stage0[CF::STAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t stage1[CF::STAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t pf_sink[4 * 256];  // prefetch destination, never read
-  constexpr int TM = CF::TM, TN = CF::TN, NA = CF::NA, NB = CF::NB;
-  const int tid = threadIdx.x;
-  int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-  const int row0 = tm * CF::BM, col0 = tn * CF::BN;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index in an SGPR
-  const int wr = wave / mx::WGN, wc = wave % mx::WGN;
-  const int lr = lane & 15, lb = lane >> 4;
-
-  // Zero both stages once: the slot dwords that the 12-byte loads never write
-  // are the zero padding of the A operand.
-  for (int i = tid; i < CF::STAGE / 16; i += mx::NT) {
-    reinterpret_cast<u32x4*>(stage0)[i] = u32x4{0u, 0u, 0u, 0u};
-    reinterpret_cast<u32x4*>(stage1)[i] = u32x4{0u, 0u, 0u, 0u};
-  }
-  __syncthreads();
-
-  v4f acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  const int nslabs = (ng + mx::KG - 1) / mx::KG;
-  auto exp_row = [&](int k, const uint8_t*& src, int& grow, int& gend, int& lds) {
-    const int r = tid + k * mx::NT;
-    const bool is_a = r < CF::BM;
-    const int rr = is_a ? r : r - CF::BM;
-    src = is_a ? a_exp : b_exp;
-    grow = (is_a ? row0 : col0) + rr;
-    gend = is_a ? M : N;
-    lds = (is_a ? CF::OFF_EA : CF::OFF_EB) + rr * mx::KG;
-  };
-  // Per-tile resources and the lane parts of the load offsets.
-  const uint32_t row_bytes = (uint32_t)ng * 12u;
-  const int a_rows = min(CF::BM, M - row0), b_rows = min(CF::BN, N - col0);
-  rsrc_t ra[NA], rb[NB];
-#pragma unroll
-  for (int p = 0; p < NA; ++p)
-    ra[p] = make_rsrc(a_mant + p * a_plane_stride + (int64_t)row0 * row_bytes, (uint32_t)a_rows * row_bytes);
-#pragma unroll
-  for (int p = 0; p < NB; ++p)
-    rb[p] = make_rsrc(b_mant + p * b_plane_stride + (int64_t)col0 * row_bytes, (uint32_t)b_rows * row_bytes);
-  const int g_lane = (lane & 7) ^ ((4 * (wave & 1) + (lane >> 4)) & 7);  // swizzled group of this lane's slot
-  const uint32_t m_lane_off = (uint32_t)(lane >> 3) * row_bytes + (uint32_t)g_lane * 12u;
-  const rsrc_t rea = make_rsrc(a_exp + (int64_t)row0 * ng, (uint32_t)(a_rows * ng));
-  const rsrc_t reb = make_rsrc(b_exp + (int64_t)col0 * ng, (uint32_t)(b_rows * ng));
-  const uint32_t e_lane_off = (uint32_t)(lane >> 1) * (uint32_t)ng + (uint32_t)(lane & 1) * 4u;
-
-  // Exponents: with full slabs, direct loads like the mantissas.  Otherwise
-  // through registers (zeros are needed past K): this thread handles rows
-  // tid + k*NT of the BM + BN exponent rows, A's first, loaded with the slab's
-  // mantissas and written to LDS after the MFMAs.
-  //
-  // Branch-free: with live false (no next slab) the direct loads go through
-  // zero-length resources and the register loads reread slab `slab`, so that
-  // a whole step is one basic block and the MFMAs cannot be moved past the
-  // next step's barrier.
-  const rsrc_t rnull = make_rsrc(a_exp, 0u);
-  auto issue = [&](uint8_t* stage, int slab, bool live, bool pf_live, uint2 (&e)[CF::EXP_ROWS_PER_T]) {
-    if constexpr (!EXP_FULL) {
-#pragma unroll
-      for (int k = 0; k < CF::EXP_ROWS_PER_T; ++k) {
-        e[k] = make_uint2(0u, 0u);
-        if (tid + k * mx::NT >= CF::BM + CF::BN) break;
-        const uint8_t* src;
-        int grow, gend, lds;
-        exp_row(k, src, grow, gend, lds);
-        e[k] = load_exps(src, grow, gend, ng, slab);
-      }
-    }
-    const bool g_ok = slab * mx::KG + g_lane < ng;
-#pragma unroll
-    for (int p = 0; p < NA; ++p)
-      load_plane<CF::BM, !EXP_FULL>(stage + p * CF::PLANE_A, live ? ra[p] : rnull, m_lane_off, row_bytes, slab, g_ok,
-                                    wave);
-#pragma unroll
-    for (int p = 0; p < NB; ++p)
-      load_plane<CF::BN, !EXP_FULL>(stage + CF::OFF_B + p * CF::PLANE_B, live ? rb[p] : rnull, m_lane_off, row_bytes,
-                                    slab, g_ok, wave);
-    if constexpr (EXP_FULL) {
-      load_exps_lds<CF::BM>(stage + CF::OFF_EA, live ? rea : rnull, e_lane_off, ng, slab, wave);
-      load_exps_lds<CF::BN>(stage + CF::OFF_EB, live ? reb : rnull, e_lane_off, ng, slab, wave);
-    }
-    // Last: the NPF prefetches of slab + 1, which the next step does not wait for.
-#pragma unroll
-    for (int p = 0; p < NA; ++p)
-      prefetch_plane<CF::BM>(pf_sink + wave * 256, pf_live ? ra[p] : rnull, row_bytes, slab + 1, tid);
-#pragma unroll
-    for (int p = 0; p < NB; ++p)
-      prefetch_plane<CF::BN>(pf_sink + wave * 256, pf_live ? rb[p] : rnull, row_bytes, slab + 1, tid);
-  };
-  constexpr int NPF = NA * 2 * CF::BM / mx::NT + NB * 2 * CF::BN / mx::NT;
-  static_assert(NPF < 16, "prefetches fit the vmcnt field of s_waitcnt");
-  // Branch-free, so that it stays behind the MFMAs in one basic block: rows
-  // past BM + BN write to a spare 8 bytes after the exponents.
-  auto put_exps = [&](uint8_t* stage, const uint2 (&e)[CF::EXP_ROWS_PER_T]) {
-    if constexpr (!EXP_FULL) {
-#pragma unroll
-      for (int k = 0; k < CF::EXP_ROWS_PER_T; ++k) {
-        const uint8_t* src;
-        int grow, gend, lds;
-        exp_row(k, src, grow, gend, lds);
-        if (tid + k * mx::NT >= CF::BM + CF::BN) lds = CF::SPARE;
-        *reinterpret_cast<uint2*>(stage + lds) = e[k];
-      }
-    }
-  };
-
-  uint2 e_regs[CF::EXP_ROWS_PER_T];
-  if (nslabs > 0) {
-    issue(stage0, 0, true, nslabs > 1, e_regs);
-    put_exps(stage0, e_regs);
-  }
-
-  // One slab: publish slab s (its direct loads and exponent writes, from
-  // every wave), start the loads of slab s + 1 into the other stage (which
-  // held slab s - 1, finished by every wave), compute slab s, then write the
-  // next slab's exponents.
-  auto step = [&](const uint8_t* cur, uint8_t* nxt, int s) {
-    // Every wave's direct loads into cur must have landed before any wave
-    // passes the barrier (the compiler only orders them against this wave's
-    // own LDS reads): wait for them explicitly.  Loads complete in order, so
-    // vmcnt = NPF leaves only the last step's prefetches in flight
-    // (s_waitcnt immediate: vmcnt in bits 3:0, expcnt and lgkmcnt zero).
-    __builtin_amdgcn_s_waitcnt(NPF);
-    // No fence (a release fence would also wait for the prefetches, which
-    // write LDS): the empty asm statements keep the compiler from moving
-    // memory accesses across the barrier, the s_waitcnt above orders the
-    // hardware.
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    const bool more = s + 1 < nslabs;
-    issue(nxt, more ? s + 1 : s, more, s + 2 < nslabs, e_regs);
-    __builtin_amdgcn_sched_barrier(0);
-    // Fragment addresses.  Row rl = wr*WM + 16*i + lr has swizzle
-    // ((rl >> 1) & 7) = ((lr >> 1) & 7) (WM and 16*i are multiples of 16), so
-    // for a K-step the slot column is a lane constant and fragment i / j sits
-    // at an immediate offset of 16 rows * 128 bytes.  A lane's block scale is
-    // the exponent byte of its row and K block: one byte read.
-    const int swz = (lr >> 1) & 7;
-    // (Every address is one offset from the stage base, which keeps the
-    // accesses attributable to the stage object.)
-    const int a_row = (wr * CF::WM + lr) * (mx::KG * 16);
-    const int b_row = CF::OFF_B + (wc * CF::WN + lr) * (mx::KG * 16);
-    const int ea_lane = CF::OFF_EA + (wr * CF::WM + lr) * mx::KG + lb;
-    const int eb_lane = CF::OFF_EB + (wc * CF::WN + lr) * mx::KG + lb;
-    auto col16 = [&](int ks) { return ((4 * ks + lb) ^ swz) * 16; };
-    if constexpr (CF::PIPE) {
-      // Software pipeline.  A block is the TN MFMAs of one A fragment (chunk
-      // ca, row tile i) against the B fragments of chunk cb; a phase (ks, cb)
-      // is NA * TM blocks.  Each block reads the next block's A fragment and a
-      // share of the next phase's B fragments, and a scheduling barrier closes
-      // it, so that about two blocks' fragments are live at a time.
-      constexpr int BPP = NA * TM;            // blocks per phase
-      constexpr int NPH = 2 * NB;             // phases per slab
-      v8i bf[2][TN], af[2];
-      int be[2][TN], ae[2];
-      auto read_b = [&](int ph, int j) {
-        const int ks = ph / NB, cb = ph % NB;
-        const u32x4 y = *reinterpret_cast<const u32x4*>(cur + (b_row + cb * CF::PLANE_B + j * 16 * (mx::KG * 16) + col16(ks)));
-        // lanes 4..7 of the B operand face A's zeros (or are unused): any value
-        bf[ph & 1][j] = __builtin_shufflevector(reinterpret_cast<const v4i&>(y), reinterpret_cast<const v4i&>(y), 0, 1,
-                                                2, 3, -1, -1, -1, -1);
-        // +4 per chunk of significance (E <= 250)
-        be[ph & 1][j] = (int)cur[eb_lane + j * 16 * mx::KG + 4 * ks] + 4 * (NB - 1 - cb);
-      };
-      auto read_a = [&](int blk) {
-        const int ph = blk / BPP, ks = ph / NB, ca = (blk % BPP) / TM, i = blk % TM;
-        const u32x4 x = *reinterpret_cast<const u32x4*>(cur + (a_row + ca * CF::PLANE_A + i * 16 * (mx::KG * 16) + col16(ks)));
-        af[blk & 1] = v8i{(int)x[0], (int)x[1], (int)x[2], (int)x[3], 0, 0, 0, 0};
-        ae[blk & 1] = (int)cur[ea_lane + i * 16 * mx::KG + 4 * ks] + 4 * (NA - 1 - ca);
-      };
-#pragma unroll
-      for (int j = 0; j < TN; ++j) read_b(0, j);
-      read_a(0);
-#pragma unroll
-      for (int blk = 0; blk < NPH * BPP; ++blk) {
-        const int ph = blk / BPP, bi = blk % BPP, i = blk % TM;
-        if (blk + 1 < NPH * BPP) read_a(blk + 1);
-        if (ph + 1 < NPH) {
-#pragma unroll
-          for (int j = bi * TN / BPP; j < (bi + 1) * TN / BPP; ++j) read_b(ph + 1, j);
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af[blk & 1], bf[ph & 1][j], acc[i][j], 2, 2, 0,
-                                                                       ae[blk & 1], 0, be[ph & 1][j]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    } else {
-      // Compiler-scheduled: per K-step and B chunk, the B fragments, then each
-      // A fragment against them.
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-        for (int cb = 0; cb < NB; ++cb) {
-          v8i bv[TN];
-          int eb[TN];
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const u32x4 y =
-                *reinterpret_cast<const u32x4*>(cur + (b_row + cb * CF::PLANE_B + j * 16 * (mx::KG * 16) + col16(ks)));
-            bv[j] = __builtin_shufflevector(reinterpret_cast<const v4i&>(y), reinterpret_cast<const v4i&>(y), 0, 1, 2,
-                                            3, -1, -1, -1, -1);
-            eb[j] = (int)cur[eb_lane + j * 16 * mx::KG + 4 * ks] + 4 * (NB - 1 - cb);
-          }
-#pragma unroll
-          for (int ca = 0; ca < NA; ++ca) {
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-              const u32x4 x =
-                  *reinterpret_cast<const u32x4*>(cur + (a_row + ca * CF::PLANE_A + i * 16 * (mx::KG * 16) + col16(ks)));
-              const v8i av = {(int)x[0], (int)x[1], (int)x[2], (int)x[3], 0, 0, 0, 0};
-              const int ea = (int)cur[ea_lane + i * 16 * mx::KG + 4 * ks] + 4 * (NA - 1 - ca);
-#pragma unroll
-              for (int j = 0; j < TN; ++j)
-                acc[i][j] =
-                    __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(av, bv[j], acc[i][j], 2, 2, 0, ea, 0, eb[j]);
-            }
-          }
-        }
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    put_exps(nxt, e_regs);  // stale but harmless after the last slab
-  };
-  int s = 0;
-  for (; s + 2 <= nslabs; s += 2) {
-    step(stage0, stage1, s);
-    step(stage1, stage0, s + 1);
-  }
-  if (s < nslabs) step(stage0, stage1, s);
-
-  // Epilogue: lane holds rows 4*lb + r, column lr of each 16x16 tile.
-  if constexpr (QNCH == 0) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = col0 + wc * CF::WN + j * 16 + lr;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = row0 + wr * CF::WM + i * 16 + lb * 4 + r;
-          if (row < M && col < N) C[(int64_t)row * ldc + col] = acc[i][j][r] * scale;
-        }
-      }
-  } else {
-    // Converted output.  A row group of C (16 consecutive columns) is spread
-    // over the 16 lanes of one lane block, so each wave stages one 16-row
-    // strip of its tile at a time in LDS (the stage memory, free now), and
-    // then every lane converts whole groups with the quantizer's converter:
-    // the same FP32 values and the same noise addressing (gid = the group's
-    // index in the output exponent array) as converting C separately.
-    constexpr int SROW = CF::WN + 4;  // strip row stride in floats (padding spreads the banks)
-    static_assert(4 * 16 * SROW * 4 <= CF::STAGE, "four strips fit in one stage");
-    // Every wave is done with the stages, and no direct load (the last
-    // steps' no-op loads included) can still write them.
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    float* strip = reinterpret_cast<float*>(stage0) + wave * (16 * SROW);
-    const int ngN = N / 16;
-    bool bad = false;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) strip[(lb * 4 + r) * SROW + j * 16 + lr] = acc[i][j][r] * scale;
-      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's strip writes are done
-      __builtin_amdgcn_wave_barrier();
-      for (int gi = lane; gi < 16 * TN; gi += 64) {
-        const int rr = gi / TN, jj = gi % TN;
-        const int row = row0 + wr * CF::WM + i * 16 + rr;
-        const int gcol = (col0 + wc * CF::WN) / 16 + jj;
-        uint32_t b[16];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const float4 v = *reinterpret_cast<const float4*>(&strip[rr * SROW + jj * 16 + 4 * k]);
-          b[4 * k] = __float_as_uint(v.x);
-          b[4 * k + 1] = __float_as_uint(v.y);
-          b[4 * k + 2] = __float_as_uint(v.z);
-          b[4 * k + 3] = __float_as_uint(v.w);
-        }
-        if (row < M && gcol < ngN) {
-          const int64_t gid = (int64_t)row * ngN + gcol;
-          uint32_t w[QNCH][16 * 6 / 32];
-          uint32_t E, s_lo, s_hi;
-          bool nonfinite;
-          if (qo.mode == kStochastic)
-            quantize_group<16, kStochastic, QNCH>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
-                                                  s_lo, s_hi);
-          else if (qo.mode == kNearest)
-            quantize_group<16, kNearest, QNCH>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
-                                               s_lo, s_hi);
-          else
-            quantize_group<16, kTruncate, QNCH>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
-                                                s_lo, s_hi);
-          qo.exps[gid] = (uint8_t)E;
-#pragma unroll
-          for (int p = 0; p < QNCH; ++p)
-            *reinterpret_cast<uint3*>((p ? qo.mant1 : qo.mant0) + gid * 12) = make_uint3(w[p][0], w[p][1], w[p][2]);
-          bad |= nonfinite;
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(0xC07F);  // the strip's reads are done before the next strip overwrites it
-      __builtin_amdgcn_wave_barrier();
-    }
-    if (qo.status && bad) atomicOr(qo.status, 1u);
-  }
-}
-
-template <class CF, bool EXP_FULL>
-static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
-                              const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
-                              int64_t ldc, const OutBFP* qo, hipStream_t s) {
-  const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
-  const dim3 grid((unsigned)(tiles_m * tiles_n)), block(mx::NT);
-  if (!qo)
-    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
-                       ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
-  else if (qo->m > 4)
-    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 2>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
-                       ng, scale, C, ldc, tiles_m, tiles_n, *qo);
-  else
-    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 1>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
-                       ng, scale, C, ldc, tiles_m, tiles_n, *qo);
-  return hipGetLastError();
-}
+FASTBFP_MX_DECLARE(1, 1, 0, 0)
+FASTBFP_MX_DECLARE(1, 1, 0, 1)
+FASTBFP_MX_DECLARE(1, 1, 1, 0)
+FASTBFP_MX_DECLARE(1, 1, 1, 1)
+FASTBFP_MX_DECLARE(1, 2, 0, 0)
+FASTBFP_MX_DECLARE(1, 2, 0, 1)
+FASTBFP_MX_DECLARE(1, 2, 1, 0)
+FASTBFP_MX_DECLARE(1, 2, 1, 1)
+FASTBFP_MX_DECLARE(2, 1, 0, 0)
+FASTBFP_MX_DECLARE(2, 1, 0, 1)
+FASTBFP_MX_DECLARE(2, 1, 1, 0)
+FASTBFP_MX_DECLARE(2, 1, 1, 1)
+FASTBFP_MX_DECLARE(2, 2, 0, 0)
+FASTBFP_MX_DECLARE(2, 2, 0, 1)
+FASTBFP_MX_DECLARE(2, 2, 1, 0)
+FASTBFP_MX_DECLARE(2, 2, 1, 1)
 
 template <int NA, int NB>
-static hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
-                              const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
-                              int64_t ldc, const OutBFP* qo, hipStream_t s) {
-  // The tile shrinks along an operand with two chunk planes so that two LDS
-  // stages fit in 160 KB.
-  using CF = mx::Cfg<(NA == 1 && NB == 1) ? FASTBFP_MX11_BM : NA == 1 ? FASTBFP_MX_BM : FASTBFP_MX_BM / 2,
-                     (NA == 1 && NB == 1) ? FASTBFP_MX11_BN : NB == 1 ? FASTBFP_MX_BN : FASTBFP_MX_BN / 2, NA, NB>;
-  auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
-  // direct exponent loads need full slabs and 4-byte aligned exponent rows
-  const bool ef = ng % mx::KG == 0 && al(a_exp, 4) && al(b_exp, 4);
-  if (ef) return launch_mx_v<CF, true>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
-  return launch_mx_v<CF, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+static hipError_t launch_fmt(int fa, int fb, const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps,
+                             const uint8_t* b_mant, const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng,
+                             float scale, float* C, int64_t ldc, const OutBFP* qo, hipStream_t s) {
+  if (!fa && !fb) return launch_mx_t<NA, NB, 0, 0>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  if (!fa) return launch_mx_t<NA, NB, 0, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  if (!fb) return launch_mx_t<NA, NB, 1, 0>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+  return launch_mx_t<NA, NB, 1, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
 }
 
-static hipError_t launch_gemm_any(const uint8_t* a_mant, const uint8_t* a_exp, int na, const uint8_t* b_mant,
-                                  const uint8_t* b_exp, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
-                                  float* C, int64_t ldc, const OutBFP* qo, hipStream_t s) {
+// a_m / b_m: the stored operands' widths (they fix the plane formats and the
+// plane stride); na / nb: planes read.
+static hipError_t launch_gemm_any(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
+                                  const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K,
+                                  int scale_log2, float* C, int64_t ldc, const OutBFP* qo, hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
   const int ng = (int)(K / 16);
-  const int64_t a_ps = M * ng * 12, b_ps = N * ng * 12;
+  const int64_t a_ps = M * ng * plane_group_bytes(16, a_m, 0), b_ps = N * ng * plane_group_bytes(16, b_m, 0);
+  const int fa = plane0_fp4(a_m), fb = plane0_fp4(b_m);
   const float scale = ldexpf(1.0f, scale_log2);
+  const int m = (int)M, n = (int)N;
   if (na == 1 && nb == 1)
-    return launch_mx_t<1, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+    return launch_fmt<1, 1>(fa, fb, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, m, n, ng, scale, C, ldc, qo, s);
   if (na == 1 && nb == 2)
-    return launch_mx_t<1, 2>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+    return launch_fmt<1, 2>(fa, fb, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, m, n, ng, scale, C, ldc, qo, s);
   if (na == 2 && nb == 1)
-    return launch_mx_t<2, 1>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
-  return launch_mx_t<2, 2>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
+    return launch_fmt<2, 1>(fa, fb, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, m, n, ng, scale, C, ldc, qo, s);
+  return launch_fmt<2, 2>(fa, fb, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, m, n, ng, scale, C, ldc, qo, s);
 }
 
-hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_planes, int na, const uint8_t* b_mant,
-                          const uint8_t* b_exp, int b_planes, int nb, int64_t M, int64_t N, int64_t K, int g,
-                          int scale_log2, float* C, int64_t ldc, hipStream_t s) {
-  (void)a_planes;
-  (void)b_planes;
-  (void)g;
-  return launch_gemm_any(a_mant, a_exp, na, b_mant, b_exp, nb, M, N, K, scale_log2, C, ldc, nullptr, s);
+hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
+                          const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+                          float* C, int64_t ldc, hipStream_t s) {
+  return launch_gemm_any(a_mant, a_exp, a_m, na, b_mant, b_exp, b_m, nb, M, N, K, scale_log2, C, ldc, nullptr, s);
 }
 
-hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int na, const uint8_t* b_mant,
-                              const uint8_t* b_exp, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
+                              const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
                               int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status,
                               hipStream_t s) {
-  OutBFP qo{c_mant, c_mant + M * (N / 16) * 12, c_exp, status, c_m, mode, (uint32_t)seed, (uint32_t)(seed >> 32)};
-  return launch_gemm_any(a_mant, a_exp, na, b_mant, b_exp, nb, M, N, K, scale_log2, nullptr, N, &qo, s);
+  const OutBFP qo{c_mant,     c_mant + M * (N / 16) * plane_group_bytes(16, c_m, 0), c_exp, status, c_m, mode,
+                  plane0_fp4(c_m), (uint32_t)seed, (uint32_t)(seed >> 32)};
+  return launch_gemm_any(a_mant, a_exp, a_m, na, b_mant, b_exp, b_m, nb, M, N, K, scale_log2, nullptr, N, &qo, s);
 }
 
 }  // namespace fastbfp

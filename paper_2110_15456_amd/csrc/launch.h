@@ -10,6 +10,15 @@ namespace fastbfp {
 // Rounding modes, numerically equal to bfp_round_t.
 enum { kNearest = 0, kStochastic = 1, kTruncate = 2 };
 
+// Chunk-plane formats of an m-bit tensor (the layout of include/fastbfp.h):
+// plane 0 holds FP4 E2M1 codes when its chunk has at most 2 bits (m = 1, 2, 5,
+// 6) and FP6 E2M3 codes otherwise; plane 1 (m >= 5) always holds FP6 codes.
+__host__ __device__ constexpr bool plane0_fp4(int m) { return m <= 2 || m == 5 || m == 6; }
+// Bytes per group of g values in plane p.
+__host__ __device__ constexpr int plane_group_bytes(int g, int m, int p) {
+  return (p == 0 && plane0_fp4(m)) ? g / 2 : 3 * g / 4;
+}
+
 hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
 hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
@@ -25,18 +34,19 @@ hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int gr
                                     uint32_t* status, hipStream_t s);
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
                              float* y, hipStream_t s);
-// na / nb: chunk planes used (1 or 2); a_off / b_off: the stored operand's plane
-// count, which sets the plane stride.  scale_log2 = 4 - m_a - m_b.
-hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_planes, int na, const uint8_t* b_mant,
-                          const uint8_t* b_exp, int b_planes, int nb, int64_t M, int64_t N, int64_t K, int g,
-                          int scale_log2, float* C, int64_t ldc, hipStream_t s);
+// a_m / b_m: the stored operands' widths (they fix the plane formats and
+// plane stride); na / nb: chunk planes read (1 or 2).  scale_log2 =
+// 4 - m_a - m_b.
+hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
+                          const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+                          float* C, int64_t ldc, hipStream_t s);
 // bfp_gemm with the output converted in the epilogue: groups of 16 along each
 // row of C at c_m bits (rounding mode and Philox seed as for quantize).
-hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int na, const uint8_t* b_mant,
-                              const uint8_t* b_exp, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
+                              const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
                               int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status,
                               hipStream_t s);
-hipError_t launch_group_partials(const uint8_t* a_mant, int a_planes, int na, const uint8_t* b_mant, int b_planes,
-                                 int nb, int64_t M, int64_t N, int64_t K, int g, int32_t* P, hipStream_t s);
+hipError_t launch_group_partials(const uint8_t* a_mant, int a_m, int na, const uint8_t* b_mant, int b_m, int nb,
+                                 int64_t M, int64_t N, int64_t K, int g, int32_t* P, hipStream_t s);
 
 }  // namespace fastbfp

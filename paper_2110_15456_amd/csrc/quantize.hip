@@ -5,8 +5,9 @@
 // the shared exponent with an in-register max (the comparator tree), aligns
 // each significand with one clamped shift (the barrel shifter), adds the
 // rounding term (half an LSB, nothing, or an 8-bit Philox noise byte), keeps
-// the carry, saturates, and writes the magnitudes as packed FP6 E2M3 chunk
-// codes (3G/4 bytes per chunk plane) plus one exponent byte.  Owning a whole
+// the carry, saturates, and writes the magnitudes as packed chunk codes
+// (FP4 E2M1 for chunks of at most 2 bits, G/2 bytes per plane; FP6 E2M3
+// otherwise, 3G/4 bytes) plus one exponent byte.  Owning a whole
 // group per lane makes one Philox call serve 16 values, which keeps stochastic
 // rounding within the HBM-bound budget.
 #include "bfp_quant.h"
@@ -15,15 +16,11 @@ namespace fastbfp {
 
 // Plane p of the group goes to mant_p (plane 1 of a two-chunk tensor, or the
 // separate 2-bit tensor of the adaptive path).
-template <int G, int NCH>
+template <int G, int NCH, bool F0, bool F1>
 __device__ __forceinline__ void store_group(uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1, int64_t gid,
                                             const uint32_t (&w)[NCH][G * 6 / 32]) {
-#pragma unroll
-  for (int p = 0; p < NCH; ++p) {
-    uint3* dst = reinterpret_cast<uint3*>((p ? mant1 : mant0) + gid * (G * 3 / 4));
-#pragma unroll
-    for (int i = 0; i < G / 16; ++i) dst[i] = make_uint3(w[p][3 * i], w[p][3 * i + 1], w[p][3 * i + 2]);
-  }
+  store_plane<G, F0>(mant0, gid, w[0]);
+  if (NCH == 2) store_plane<G, F1>(mant1, gid, w[NCH - 1]);
 }
 
 // Writes the block's Eq. 2 partial sums to part[2 * blockIdx.x + {0, 1}]:
@@ -82,7 +79,7 @@ __global__ __launch_bounds__(256) void k_improvement_finalize(double* sums, int6
 // all 64 banks on the read-back.  (Reading 64 contiguous bytes per lane
 // straight from global memory instead leaves each load instruction touching
 // 64 scattered 16-byte pieces, which costs about a third of HBM bandwidth.)
-template <int G, int MODE, int NCH, bool ADAPT>
+template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1>
 __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__ x, int64_t ngroups, uint32_t m,
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
                                                        uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
@@ -123,10 +120,10 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   uint32_t w[NCH][G * 6 / 32];
   uint32_t E, s_lo, s_hi;
   bool nonfinite;
-  quantize_group<G, MODE, NCH, ADAPT>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
+  quantize_group<G, MODE, NCH, ADAPT, F0, F1>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
   if (valid) {
     exps[gid] = (uint8_t)E;
-    store_group<G, NCH>(mant0, mant1, gid, w);
+    store_group<G, NCH, F0, F1>(mant0, mant1, gid, w);
     if (status && nonfinite) atomicOr(status, 1u);
   }
   if (ADAPT)
@@ -141,14 +138,15 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
 // consecutive group rows (NGT per wave).  The packed codes and exponents of
 // the 64 x JB groups are gathered in LDS and then written row by row, so that
 // every store instruction writes contiguous bytes of one output row.
-template <int G, int MODE, int NCH, int NGT, bool ADAPT>
+template <int G, int MODE, int NCH, int NGT, bool ADAPT, bool F0, bool F1>
 __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__ x, int64_t R, int64_t C,
                                                        int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
                                                        uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1,
                                                        uint8_t* __restrict__ exps, uint32_t* status, double* sums) {
   constexpr int JB = 4 * NGT;             // group rows per block
-  constexpr int WPG = G * 6 / 32;         // code dwords per group per plane
-  constexpr int ROWW = JB * WPG;          // code dwords per output row per plane in this block
+  constexpr int WPG = G * 6 / 32;         // code dwords per group of an FP6 plane (an FP4 plane: G / 8)
+  constexpr int WP[2] = {F0 ? G / 8 : WPG, F1 ? G / 8 : WPG};  // code dwords per group of each plane
+  constexpr int ROWW = JB * WPG;          // LDS row stride, code dwords per output row
   __shared__ uint32_t sc[NCH][64][ROWW];
   __shared__ uint8_t se[64][JB];
   const int64_t bx = blockIdx.x % nbx, by = blockIdx.x / nbx;
@@ -171,7 +169,8 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       uint32_t w[NCH][WPG];
       uint32_t E, s_lo, s_hi;
       bool nonfinite;
-      quantize_group<G, MODE, NCH, ADAPT>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo, s_hi);
+      quantize_group<G, MODE, NCH, ADAPT, F0, F1>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo,
+                                                  s_hi);
       if (ADAPT) {
         num += ldexp((double)s_lo, (int)E - 130);
         den += ldexp((double)s_hi, (int)E - 128);
@@ -179,7 +178,7 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
 #pragma unroll
       for (int p = 0; p < NCH; ++p)
 #pragma unroll
-        for (int k = 0; k < WPG; ++k) sc[p][lane][jl * WPG + k] = w[p][k];
+        for (int k = 0; k < WP[p]; ++k) sc[p][lane][jl * WP[p] + k] = w[p][k];
       se[lane][jl] = (uint8_t)E;
       any_bad |= nonfinite;
     }
@@ -188,12 +187,15 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
   __syncthreads();
   // Write-out: output row c0 + r gets jn groups starting at group jb.
   const int ncols = (int)min((int64_t)64, C - c0);
-  for (int d = threadIdx.x; d < ncols * ROWW; d += 256) {
-    const int r = d / ROWW, k = d % ROWW;
-    if (k < jn * WPG) {
-      const int64_t o = ((c0 + r) * gpr + jb) * WPG + k;
 #pragma unroll
-      for (int p = 0; p < NCH; ++p) reinterpret_cast<uint32_t*>(p ? mant1 : mant0)[o] = sc[p][r][k];
+  for (int p = 0; p < NCH; ++p) {
+    const int rw = JB * WP[p];  // code dwords of a full output row of this block in plane p
+    for (int d = threadIdx.x; d < ncols * rw; d += 256) {
+      const int r = d / rw, k = d % rw;
+      if (k < jn * WP[p]) {
+        const int64_t o = ((c0 + r) * gpr + jb) * WP[p] + k;
+        reinterpret_cast<uint32_t*>(p ? mant1 : mant0)[o] = sc[p][r][k];
+      }
     }
   }
   for (int d = threadIdx.x; d < ncols * JB; d += 256) {
@@ -203,25 +205,30 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
   if (status && any_bad) atomicOr(status, 1u);
 }
 
-// BFP -> FP32: y = +-q * 2^(E-127-(m-1)).  One lane per group.
-template <int G, int NCH>
+// BFP -> FP32: y = +-q * 2^(E-127-(m-1)).  One lane per group.  F0: plane 0
+// holds FP4 codes.
+template <int G, int NCH, bool F0>
 __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ mant, const uint8_t* __restrict__ exps,
                                                     int64_t ngroups, int m, float* __restrict__ y) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= ngroups) return;
+  constexpr int B0 = F0 ? G / 2 : G * 3 / 4;  // bytes per group in plane 0
   uint32_t w[NCH][G * 6 / 32];
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
-    const uint3* src = reinterpret_cast<const uint3*>(mant + p * ngroups * (G * 3 / 4) + gid * (G * 3 / 4));
+    const int gb = (p == 0 && F0) ? G / 2 : G * 3 / 4;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(mant + p * ngroups * B0 + gid * gb);
 #pragma unroll
-    for (int i = 0; i < G / 16; ++i) {
-      const uint3 v = src[i];
-      w[p][3 * i] = v.x;
-      w[p][3 * i + 1] = v.y;
-      w[p][3 * i + 2] = v.z;
-    }
+    for (int i = 0; i < G * 6 / 32; ++i) w[p][i] = i < gb / 4 ? src[i] : 0u;
   }
   const int e = (int)exps[gid] - 127 - (m - 1);
+  auto chunk = [&](int p, int t) {
+    if (p == 0 && F0) {
+      const uint32_t nib = (w[0][t >> 3] >> (4 * (t & 7))) & 0xFu;
+      return (nib & 8u) ? -(int)(nib & 7u) : (int)(nib & 7u);
+    }
+    return e2m3_half_decode(fp6_field(w[p], t));
+  };
   float4* dst = reinterpret_cast<float4*>(y + gid * G);
 #pragma unroll
   for (int i = 0; i < G / 4; ++i) {
@@ -229,79 +236,88 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int t = 4 * i + k;
-      int q = e2m3_half_decode(fp6_field(w[0], t));
-      if (NCH == 2) {
-        const int lo = e2m3_half_decode(fp6_field(w[NCH - 1], t));
-        q = q * 16 + lo;  // both chunks carry the value's sign
-      }
+      int q = chunk(0, t);
+      if (NCH == 2) q = q * 16 + chunk(NCH - 1, t);  // both chunks carry the value's sign
       v[k] = ldexpf((float)q, e);
     }
     dst[i] = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
-template <int G, int MODE, int NCH, bool ADAPT = false>
+template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
 static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
                                 uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
   const int64_t blocks = (ngroups + 255) / 256;
-  hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
+  hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, F0, F1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
                      (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
   return hipGetLastError();
 }
 
-template <int G, int MODE, int NCH, bool ADAPT = false>
+template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
 static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant0,
                                 uint8_t* mant1, uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
   constexpr int NGT = 8;
   const int64_t gpr = R / G;
   const int64_t nbx = (C + 63) / 64, nby = (gpr + 4 * NGT - 1) / (4 * NGT);
-  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
+  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, F0, F1>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
                      C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
   return hipGetLastError();
 }
 
-#define FASTBFP_DISPATCH_QUANT(FN, ...)                                  \
-  do {                                                                   \
-    const bool two = m > 4;                                              \
-    if (g == 16) {                                                       \
-      if (mode == kNearest) return two ? FN<16, kNearest, 2>(__VA_ARGS__) : FN<16, kNearest, 1>(__VA_ARGS__); \
-      if (mode == kStochastic) return two ? FN<16, kStochastic, 2>(__VA_ARGS__) : FN<16, kStochastic, 1>(__VA_ARGS__); \
-      return two ? FN<16, kTruncate, 2>(__VA_ARGS__) : FN<16, kTruncate, 1>(__VA_ARGS__); \
-    } else {                                                             \
-      if (mode == kNearest) return two ? FN<32, kNearest, 2>(__VA_ARGS__) : FN<32, kNearest, 1>(__VA_ARGS__); \
-      if (mode == kStochastic) return two ? FN<32, kStochastic, 2>(__VA_ARGS__) : FN<32, kStochastic, 1>(__VA_ARGS__); \
-      return two ? FN<32, kTruncate, 2>(__VA_ARGS__) : FN<32, kTruncate, 1>(__VA_ARGS__); \
-    }                                                                    \
+// Specialisation for (g, rounding mode, m): planes and plane-0 format.
+#define FASTBFP_QUANT_M(FN, G, MODE, ...)                                         \
+  do {                                                                            \
+    if (m <= 2) return FN<G, MODE, 1, true>(__VA_ARGS__);                         \
+    if (m <= 4) return FN<G, MODE, 1, false>(__VA_ARGS__);                        \
+    if (m <= 6) return FN<G, MODE, 2, true>(__VA_ARGS__);                         \
+    return FN<G, MODE, 2, false>(__VA_ARGS__);                                    \
+  } while (0)
+#define FASTBFP_DISPATCH_QUANT(FN, ...)                                           \
+  do {                                                                            \
+    if (g == 16) {                                                                \
+      if (mode == kNearest) FASTBFP_QUANT_M(FN, 16, kNearest, __VA_ARGS__);       \
+      if (mode == kStochastic) FASTBFP_QUANT_M(FN, 16, kStochastic, __VA_ARGS__); \
+      FASTBFP_QUANT_M(FN, 16, kTruncate, __VA_ARGS__);                            \
+    } else {                                                                      \
+      if (mode == kNearest) FASTBFP_QUANT_M(FN, 32, kNearest, __VA_ARGS__);       \
+      if (mode == kStochastic) FASTBFP_QUANT_M(FN, 32, kStochastic, __VA_ARGS__); \
+      FASTBFP_QUANT_M(FN, 32, kTruncate, __VA_ARGS__);                            \
+    }                                                                             \
   } while (0)
 
 hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s) {
   const int64_t ngroups = rows * (len / g);
   if (ngroups == 0) return hipSuccess;
-  uint8_t* mant1 = mant + ngroups * (g * 3 / 4);  // plane 1 when m > 4
+  uint8_t* mant1 = mant + ngroups * plane_group_bytes(g, m, 0);  // plane 1 when m > 4
   FASTBFP_DISPATCH_QUANT(launch_rows_t, x, ngroups, m, seed, mant, mant1, exps, status, nullptr, s);
 }
 
 hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s) {
   if (R == 0 || C == 0) return hipSuccess;
-  uint8_t* mant1 = mant + C * (R / g) * (g * 3 / 4);  // plane 1 when m > 4
+  uint8_t* mant1 = mant + C * (R / g) * plane_group_bytes(g, m, 0);  // plane 1 when m > 4
   FASTBFP_DISPATCH_QUANT(launch_cols_t, x, R, C, m, seed, mant, mant1, exps, status, nullptr, s);
 }
 
-#define FASTBFP_DISPATCH_ADAPT(FN, ...)                                                                    \
-  do {                                                                                                    \
-    if (g == 16) {                                                                                        \
-      if (mode == kNearest) return two ? FN<16, kNearest, 2, true>(__VA_ARGS__) : FN<16, kNearest, 1, true>(__VA_ARGS__); \
-      if (mode == kStochastic)                                                                            \
-        return two ? FN<16, kStochastic, 2, true>(__VA_ARGS__) : FN<16, kStochastic, 1, true>(__VA_ARGS__); \
-      return two ? FN<16, kTruncate, 2, true>(__VA_ARGS__) : FN<16, kTruncate, 1, true>(__VA_ARGS__);   \
-    } else {                                                                                              \
-      if (mode == kNearest) return two ? FN<32, kNearest, 2, true>(__VA_ARGS__) : FN<32, kNearest, 1, true>(__VA_ARGS__); \
-      if (mode == kStochastic)                                                                            \
-        return two ? FN<32, kStochastic, 2, true>(__VA_ARGS__) : FN<32, kStochastic, 1, true>(__VA_ARGS__); \
-      return two ? FN<32, kTruncate, 2, true>(__VA_ARGS__) : FN<32, kTruncate, 1, true>(__VA_ARGS__);   \
-    }                                                                                                     \
+// The adaptive specialisations: plane 0 the m = 4 codes (FP6), plane 1 (if
+// two) the 2-bit tensor (FP4).
+#define FASTBFP_ADAPT_M(FN, G, MODE, ...)                                         \
+  do {                                                                            \
+    if (two) return FN<G, MODE, 2, false, true, true>(__VA_ARGS__);               \
+    return FN<G, MODE, 1, false, true, true>(__VA_ARGS__);                        \
+  } while (0)
+#define FASTBFP_DISPATCH_ADAPT(FN, ...)                                           \
+  do {                                                                            \
+    if (g == 16) {                                                                \
+      if (mode == kNearest) FASTBFP_ADAPT_M(FN, 16, kNearest, __VA_ARGS__);       \
+      if (mode == kStochastic) FASTBFP_ADAPT_M(FN, 16, kStochastic, __VA_ARGS__); \
+      FASTBFP_ADAPT_M(FN, 16, kTruncate, __VA_ARGS__);                            \
+    } else {                                                                      \
+      if (mode == kNearest) FASTBFP_ADAPT_M(FN, 32, kNearest, __VA_ARGS__);       \
+      if (mode == kStochastic) FASTBFP_ADAPT_M(FN, 32, kStochastic, __VA_ARGS__); \
+      FASTBFP_ADAPT_M(FN, 32, kTruncate, __VA_ARGS__);                            \
+    }                                                                             \
   } while (0)
 
 int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g) {
@@ -335,20 +351,29 @@ hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int gr
   return hipGetLastError();
 }
 
+template <int G, int NCH, bool F0>
+static hipError_t launch_deq_t(const uint8_t* mant, const uint8_t* exps, int64_t ngroups, int m, float* y,
+                               hipStream_t s) {
+  const unsigned blocks = (unsigned)((ngroups + 255) / 256);
+  hipLaunchKernelGGL((k_dequantize<G, NCH, F0>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
+  return hipGetLastError();
+}
+
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
                              float* y, hipStream_t s) {
   const int64_t ngroups = rows * (len / g);
   if (ngroups == 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((ngroups + 255) / 256);
-  const bool two = m > 4;
+  const bool two = m > 4, f4 = plane0_fp4(m);
   if (g == 16) {
-    if (two) hipLaunchKernelGGL((k_dequantize<16, 2>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
-    else hipLaunchKernelGGL((k_dequantize<16, 1>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
-  } else {
-    if (two) hipLaunchKernelGGL((k_dequantize<32, 2>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
-    else hipLaunchKernelGGL((k_dequantize<32, 1>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
+    if (two) return f4 ? launch_deq_t<16, 2, true>(mant, exps, ngroups, m, y, s)
+                       : launch_deq_t<16, 2, false>(mant, exps, ngroups, m, y, s);
+    return f4 ? launch_deq_t<16, 1, true>(mant, exps, ngroups, m, y, s)
+              : launch_deq_t<16, 1, false>(mant, exps, ngroups, m, y, s);
   }
-  return hipGetLastError();
+  if (two) return f4 ? launch_deq_t<32, 2, true>(mant, exps, ngroups, m, y, s)
+                     : launch_deq_t<32, 2, false>(mant, exps, ngroups, m, y, s);
+  return f4 ? launch_deq_t<32, 1, true>(mant, exps, ngroups, m, y, s)
+            : launch_deq_t<32, 1, false>(mant, exps, ngroups, m, y, s);
 }
 
 }  // namespace fastbfp

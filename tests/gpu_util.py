@@ -40,12 +40,17 @@ def check_quantize(x: np.ndarray, axis: int, g: int, m: int, mode: str, seed: in
     mant = t.mant.cpu().numpy()
     r0, r1 = (0, t.rows) if rows is None else rows
     assert np.array_equal(E[r0:r1], E_o), "shared exponents differ"
-    nb = t.rows * t.len * 3 // 4
-    planes = mant.reshape(bfp_codec.n_planes(m), nb)
-    lo, hi = r0 * t.len * 3 // 4, r1 * t.len * 3 // 4
-    want = bfp_codec.encode(q_o, m).reshape(bfp_codec.n_planes(m), -1)
-    if not np.array_equal(planes[:, lo:hi], want):
-        got_q = bfp_codec.decode(planes[:, lo:hi].reshape(-1), r1 - r0, t.len, m)
+    # the compared rows of every plane (each plane is rows x len codes)
+    got, off = [], 0
+    for p in range(bfp_codec.n_planes(m)):
+        per_row = bfp_codec.plane_bytes(1, t.len, m, p)
+        got.append(mant[off + r0 * per_row: off + r1 * per_row])
+        off += bfp_codec.plane_bytes(t.rows, t.len, m, p)
+    assert off == mant.size
+    got = np.concatenate(got)
+    want = bfp_codec.encode(q_o, m)
+    if not np.array_equal(got, want):
+        got_q = bfp_codec.decode(got, r1 - r0, t.len, m)
         bad_idx = np.argwhere(got_q != q_o)
         raise AssertionError("mantissas differ at %d positions, first %s: gpu %s oracle %s"
                              % (len(bad_idx), bad_idx[:3].tolist(), got_q[tuple(bad_idx[0])] if len(bad_idx) else None,

@@ -64,6 +64,10 @@ def test_quantized_sizes(lib):
     assert (mb.value, eb.value) == (8192 * 8192 * 3 // 4, 8192 * 512)
     assert lib.bfp_quantized_sizes(3, 64, 32, 8, ctypes.byref(mb), ctypes.byref(eb)) == OK
     assert (mb.value, eb.value) == (2 * 3 * 64 * 3 // 4, 6)
+    # chunks of at most 2 bits take 4-bit codes: m = 1, 2 (one plane), 5, 6 (the upper plane)
+    for m, bits in ((1, 4), (2, 4), (3, 6), (4, 6), (5, 10), (6, 10), (7, 12), (8, 12)):
+        assert lib.bfp_quantized_sizes(5, 96, 16, m, ctypes.byref(mb), ctypes.byref(eb)) == OK
+        assert (mb.value, eb.value) == (5 * 96 * bits // 8, 5 * 6), m
     assert lib.bfp_quantized_sizes(3, 40, 16, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_SHAPE
     assert lib.bfp_quantized_sizes(3, 64, 8, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_UNSUP
     assert lib.bfp_quantized_sizes(3, 64, 16, 9, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC

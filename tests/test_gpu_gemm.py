@@ -70,7 +70,12 @@ def test_config1_256():
 
 
 SHAPES = [(300, 200, 592), (257, 129, 576), (129, 257, 144), (1, 1, 16), (5, 300, 4096), (64, 64, 2048)]
-PAIRS = [(2, 2), (2, 4), (4, 4), (4, 6), (6, 8), (8, 8), (3, 7), (1, 5)]
+# Every kernel variant: (planes, plane-0 format) of A x B, where m = 1, 2 is one
+# FP4 plane, 3, 4 one FP6 plane, 5, 6 an FP4 + FP6 pair and 7, 8 two FP6 planes.
+PAIRS = [(2, 2), (2, 4), (4, 2), (4, 4),          # one plane each
+         (1, 5), (2, 8), (4, 6), (3, 7),          # one x two
+         (5, 2), (6, 3), (8, 1), (7, 4),          # two x one
+         (6, 6), (6, 8), (8, 6), (8, 8)]          # two x two
 
 
 @pytest.mark.parametrize("shape", SHAPES)
