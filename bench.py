@@ -2,10 +2,12 @@
 """Benchmark of the BFP hot path on one MI355X.
 
 A step is one BFP training step of one FFN layer (M = 8192 tokens, 4096 ->
-16384, groups of 16): six quantizations -- X and W for the forward GEMM (W
-regrouped along its rows, i.e. transposed on quantize), dY (stochastic
-rounding) and W for dX = dY . W^T, X and dY regrouped along the token axis for
-dW = X^T . dY -- and the three GEMMs.  The mantissa width follows the schedule
+16384, groups of 16): X converted in both groupings from one read (along its
+features for the forward GEMM, along the tokens for dW), the forward GEMM
+Y = X . W, dY converted in both groupings with stochastic rounding, the
+backward GEMMs dX = dY . W^T and dW = X^T . dY, and the weight update
+W <- W - lr * dW with W converted in both groupings for the next step (the
+forward and dX operands).  The mantissa width follows the schedule
 2 -> 4 -> 6 bits over consecutive steps.  Inputs are resident in HBM before
 timing (three dY tensors rotate with the schedule).
 
@@ -51,6 +53,12 @@ def q_bytes(n_elems, m, g=G):
     return n_elems * (4 + code_bits(m) / 8.0 + 1.0 / g)
 
 
+def dual_bytes(n_elems, m, g=G):
+    """Algorithmic HBM bytes of a two-grouping conversion: read FP32 once,
+    write both BFP tensors."""
+    return n_elems * (4 + 2 * (code_bits(m) / 8.0 + 1.0 / g))
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -93,6 +101,9 @@ class Step:
         self.Y = torch.empty((M_TOK, D_FF), dtype=torch.float32, device=dev)
         self.dX = torch.empty((M_TOK, D_IN), dtype=torch.float32, device=dev)
         self.dW = torch.empty((D_IN, D_FF), dtype=torch.float32, device=dev)
+        # the first step's BFP weights (later steps get them from the update)
+        b = self.q[SCHEDULE[0]]
+        fb.quantize_dual(self.W, g=G, m=SCHEDULE[0], out_rows=b["wk"], out_cols=b["wb"])
 
     def run(self, s, ev=None):
         """Enqueue step s.  ev: optional list collecting (name, start, end) events."""
@@ -112,18 +123,18 @@ class Step:
             z.record()
             ev.append((name, m, a, z))
 
-        rec("quantize_rows", lambda: fb.quantize(self.X, g=G, m=m, out=b["xa"]))
-        rec("quantize_cols", lambda: fb.quantize(self.W, group_axis=0, g=G, m=m, out=b["wb"]))
+        nb = self.q[SCHEDULE[(s + 1) % 3]]
+        rec("quantize_dual", lambda: fb.quantize_dual(self.X, g=G, m=m, out_rows=b["xa"], out_cols=b["xt"]))
         rec("gemm", lambda: fb.gemm(b["xa"], b["wb"], out=self.Y))
-        rec("quantize_rows", lambda: fb.quantize(dy, g=G, m=m, rounding="stochastic", seed=seed, out=b["dya"]))
-        rec("quantize_rows", lambda: fb.quantize(self.W, g=G, m=m, out=b["wk"]))
+        rec("quantize_dual", lambda: fb.quantize_dual(dy, g=G, m=m, rounding="stochastic", seed_rows=seed,
+                                                      seed_cols=seed + 1, out_rows=b["dya"], out_cols=b["dyt"]))
         rec("gemm", lambda: fb.gemm(b["dya"], b["wk"], out=self.dX))
-        rec("quantize_cols", lambda: fb.quantize(self.X, group_axis=0, g=G, m=m, out=b["xt"]))
-        rec("quantize_cols", lambda: fb.quantize(dy, group_axis=0, g=G, m=m, rounding="stochastic", seed=seed + 1,
-                                                 out=b["dyt"]))
         rec("gemm", lambda: fb.gemm(b["xt"], b["dyt"], out=self.dW))
+        rec("weight_update", lambda: fb.weight_update(self.W, self.dW, -LR, g=G, m=SCHEDULE[(s + 1) % 3], w_out=self.W,
+                                                      out_rows=nb["wk"], out_cols=nb["wb"]))
 
 
+LR = 1e-3  # SGD step on the raw weight gradient
 STEP_OPS = 3 * 2.0 * M_TOK * D_FF * D_IN
 GEMM_OPS = 2.0 * M_TOK * D_FF * D_IN  # every one of the three GEMMs has M*N*K = 8192*16384*4096
 
@@ -270,7 +281,7 @@ def measured_traffic(key):
 
 def cpu_baseline(args):
     """The oracle, untuned, on the host cores (at most the 16-thread CPU share
-    of one GPU): every quantization of one m=4 step in full, plus the first
+    of one GPU): every conversion and the weight update of one m=4 step in full, plus the first
     SAMPLE_ROWS output rows of each GEMM; the GEMM time is scaled to all rows
     and the step rate reported in the bench's unit."""
     import numpy as np
@@ -282,12 +293,10 @@ def cpu_baseline(args):
     dY = synth.draw("grads", (M_TOK, D_FF), 53)
     m = 4
     t0 = time.time()
-    xa = oracle.quantize(X, axis=-1, g=G, m=m, threads=threads)
-    wb = oracle.quantize(W, axis=0, g=G, m=m, threads=threads)
-    dya = oracle.quantize(dY, axis=-1, g=G, m=m, mode="stochastic", seed=1000, threads=threads)
-    wk = oracle.quantize(W, axis=-1, g=G, m=m, threads=threads)
-    xt = oracle.quantize(X, axis=0, g=G, m=m, threads=threads)
-    dyt = oracle.quantize(dY, axis=0, g=G, m=m, mode="stochastic", seed=1001, threads=threads)
+    wk, wb, _ = oracle.quantize_dual(W, g=G, m=m, threads=threads)
+    xa, xt, _ = oracle.quantize_dual(X, g=G, m=m, threads=threads)
+    dya, dyt, _ = oracle.quantize_dual(dY, g=G, m=m, mode="stochastic", seed_rows=1000, seed_cols=1001,
+                                       threads=threads)
     tq = time.time() - t0
     SAMPLE_ROWS = 384
     rows = np.arange(SAMPLE_ROWS)
@@ -296,13 +305,20 @@ def cpu_baseline(args):
     oracle.gemm(dya[0], dya[1], m, wk[0], wk[1], m, g=G, rows=rows, threads=threads)
     oracle.gemm(xt[0], xt[1], m, dyt[0], dyt[1], m, g=G, rows=rows, threads=threads)
     tg = time.time() - t1
+    # the weight update (on a stand-in gradient of the right shape) and its
+    # two-grouping conversion for the next step
+    t2 = time.time()
+    W2 = oracle.weight_update(W, dY[:D_IN, :D_FF], -LR)
+    oracle.quantize_dual(W2, g=G, m=m, threads=threads)
+    tq += time.time() - t2
     # rows sampled: SAMPLE_ROWS of 8192 (fwd, dX) and of 4096 (dW); the three
     # GEMMs have the same N*K per output row, so each took about tg / 3
     full_gemm_s = tg / 3 * (M_TOK + M_TOK + D_IN) / SAMPLE_ROWS
     step_s = tq + full_gemm_s
     return {"value": round(STEP_OPS / step_s / 1e12, 6), "unit": "TOPS", "cores": threads, "kind": "oracle",
-            "sample": ("one m=4 FFN step: all six quantizations in full (%.1f s) and the first %d output rows of "
-                       "each GEMM (%.1f s), GEMM time scaled by rows to the full step (est. %.0f s per step)"
+            "sample": ("one m=4 FFN step: the conversions of X and dY and the weight update with its conversion in "
+                       "full (%.1f s) and the first %d output rows of each GEMM (%.1f s), GEMM time scaled by rows "
+                       "to the full step (est. %.0f s per step)"
                        % (tq, SAMPLE_ROWS, tg, step_s)),
             "cpu_seconds": round(tq + tg, 1)}
 
@@ -342,13 +358,20 @@ def main():
 
     # per-kernel table from the events recorded inside the timed region
     table = {}
-    sizes = [M_TOK * D_IN, D_IN * D_FF, 0, M_TOK * D_FF, D_IN * D_FF, 0, M_TOK * D_IN, M_TOK * D_FF, 0]
+    # algorithmic HBM bytes of the conversions: read the FP32 input(s), write
+    # two BFP tensors (and, for the update, the FP32 weights)
+    sizes = [M_TOK * D_IN, 0, M_TOK * D_FF, 0, 0, D_IN * D_FF]
     for i, (name, m, a, z) in enumerate(events):
-        k = i % 9
+        k = i % 6
         r = table.setdefault("%s_m%d" % (name, m), {"launches": 0, "ms": 0.0, "work": 0.0})
         r["launches"] += 1
         r["ms"] += a.elapsed_time(z)
-        r["work"] += GEMM_OPS if name == "gemm" else q_bytes(sizes[k], m)
+        if name == "gemm":
+            r["work"] += GEMM_OPS
+        elif name == "quantize_dual":
+            r["work"] += dual_bytes(sizes[k], m)
+        else:  # the update converts at the next step's width
+            r["work"] += dual_bytes(sizes[k], SCHEDULE[(SCHEDULE.index(m) + 1) % 3]) + 8.0 * sizes[k]
     kernels = {}
     for key, r in table.items():
         avg = r["ms"] / r["launches"]
@@ -379,8 +402,9 @@ def main():
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "fp6", "data": "synthetic",
-        "config": {"workload": "BFP FFN training step: tokens 8192, 4096->16384, g=16, fwd+dX+dW GEMMs with six "
-                               "quantizations (two regrouped along tokens, SR on dY), mantissa schedule 2->4->6",
+        "config": {"workload": "BFP FFN training step: tokens 8192, 4096->16384, g=16, fwd+dX+dW GEMMs, X and dY "
+                               "converted in both groupings from one read (SR on dY), SGD weight update with both "
+                               "groupings of W for the next step, mantissa schedule 2->4->6",
                    "M": M_TOK, "d_in": D_IN, "d_ff": D_FF, "g": G, "schedule": list(SCHEDULE)},
         "roofline": roof, "kernels": kernels,
     }

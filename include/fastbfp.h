@@ -194,6 +194,44 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
                             int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream);
 
 /*
+ * bfp_quantize_dual -- both groupings of one FP32 matrix from a single read:
+ * the row grouping (group_axis 1: rows = R, len = C) into mant_r/exp_r with
+ * seed_r, and the column grouping (group_axis 0: rows = C, len = R) into
+ * mant_c/exp_c with seed_c, each byte for byte what bfp_quantize writes for
+ * that axis and seed.  A training step needs both of some tensors: the
+ * activations and the output gradient enter one GEMM along their feature axis
+ * and the weight-gradient GEMM along the token axis (section II-B), which the
+ * paper serves by entering the systolic array from another side (section V-A).
+ *   x           : FP32 [R][C], row-major, contiguous, 16-byte aligned.
+ *   R, C        : multiples of 16 (BFP_E_SHAPE otherwise), C < 2^22.
+ *   g           : 16 (BFP_E_UNSUPPORTED otherwise).
+ *   m_bits, round_mode, status_word : as bfp_quantize (one width and rounding
+ *                 rule for both outputs).
+ *   outputs     : sized by bfp_quantized_sizes(R, C, 16, m_bits) (either).
+ */
+int bfp_quantize_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, uint64_t seed_r,
+                      uint64_t seed_c, uint8_t* mant_r, uint8_t* exp_r, uint8_t* mant_c, uint8_t* exp_c,
+                      uint32_t* status_word, void* stream);
+
+/*
+ * bfp_weight_update -- the end of a training step (sections V-A and the
+ * training workflow): the weight gradient is added to the weights and the
+ * updated weights are converted to BFP for the next step, in one pass:
+ *   w_out[r][c] = w[r][c] + alpha * dw[r][c]
+ * in FP32 with the product and the sum each rounded to nearest (no fused
+ * multiply-add; alpha = 1 is the paper's plain sum, alpha = -learning rate an
+ * SGD step on a raw gradient), then both groupings of w_out as
+ * bfp_quantize_dual.  Subnormal inputs, products and sums are read as, and
+ * flushed to, zero of the same sign.  w_out may be w (in place); dw must not
+ * overlap w_out.
+ *   w, dw, w_out : FP32 [R][C], row-major, contiguous, 16-byte aligned.
+ *   The rest     : as bfp_quantize_dual.
+ */
+int bfp_weight_update(const float* w, const float* dw, float alpha, float* w_out, int64_t R, int64_t C, int g,
+                      int m_bits, int round_mode, uint64_t seed_r, uint64_t seed_c, uint8_t* mant_r, uint8_t* exp_r,
+                      uint8_t* mant_c, uint8_t* exp_c, uint32_t* status_word, void* stream);
+
+/*
  * bfp_quantize_adaptive -- the converter and improvement block of the adaptive
  * scheme (Algorithm 1, Eq. 2, section V-C; section V-D for the chunk discard),
  * in one pass over x: BFP(X, 4) is written as by bfp_quantize with m_bits = 4;

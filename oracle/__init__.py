@@ -245,3 +245,32 @@ def select_mantissa(num: float, den: float, eps: float) -> int:
     """Algorithm 1's per-tensor choice (2 or 4 bits)."""
     return int(_load().oracle_select_mantissa(num, den, eps))
 
+
+
+def quantize_dual(x, g: int = 16, m: int = 4, mode="nearest", seed_rows: int = 0, seed_cols: int = 0,
+                  threads: int = 1):
+    """Both groupings of one matrix, by definition two conversions (section
+    III-A): along its rows with seed_rows and down its columns with seed_cols.
+    Returns ((q_r, E_r), (q_c, E_c), nonfinite groups)."""
+    qr, er, br = quantize(x, axis=-1, g=g, m=m, mode=mode, seed=seed_rows, threads=threads)
+    qc, ec, bc = quantize(x, axis=0, g=g, m=m, mode=mode, seed=seed_cols, threads=threads)
+    return (qr, er), (qc, ec), br + bc
+
+
+def _flush(x: np.ndarray) -> np.ndarray:
+    """Subnormal FP32 values to zero of the same sign."""
+    x = np.asarray(x, dtype=np.float32)
+    return np.where(np.abs(x) < np.finfo(np.float32).tiny, np.copysign(np.float32(0.0), x), x).astype(np.float32)
+
+
+def weight_update(w, dw, alpha: float) -> np.ndarray:
+    """The updated weights of the training workflow's last step (the weight
+    gradient added to the weights, section V-A): w + alpha * dw in FP32, the
+    product and the sum each rounded to nearest-even (numpy's float32
+    arithmetic; no fused multiply-add).  Subnormal inputs, product and sum
+    are read as / flushed to zero of the same sign, as the converter reads
+    subnormal inputs."""
+    w = _flush(w)
+    dw = _flush(dw)
+    prod = _flush(np.float32(_flush(np.float32(alpha))) * dw)
+    return _flush(w + prod)

@@ -20,8 +20,8 @@ import torch
 
 from ._lib import BFPError, check, load
 
-__all__ = ["BFPTensor", "BFPError", "quantize", "dequantize", "gemm", "gemm_bfp", "gemm_group_partials",
-           "quantize_adaptive", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING"]
+__all__ = ["BFPTensor", "BFPError", "quantize", "quantize_dual", "weight_update", "dequantize", "gemm", "gemm_bfp",
+           "gemm_group_partials", "quantize_adaptive", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING"]
 
 ROUNDING = {"nearest": 0, "stochastic": 1, "truncate": 2}
 
@@ -119,6 +119,74 @@ def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rou
                            ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(t.mant.data_ptr()),
                            ctypes.c_void_p(t.exp.data_ptr()), st_ptr, _stream(x.device)), "bfp_quantize")
     return t
+
+
+def _status_ptr(status):
+    if status is None:
+        return None
+    _need_cuda(status, "status")
+    return ctypes.c_void_p(status.data_ptr())
+
+
+def _dual_outputs(R, C, g, m, device, out_rows, out_cols):
+    tr = out_rows if out_rows is not None else BFPTensor.empty(R, C, g, m, device)
+    tc = out_cols if out_cols is not None else BFPTensor.empty(C, R, g, m, device)
+    if (tr.rows, tr.len, tr.g, tr.m) != (R, C, g, m) or (tc.rows, tc.len, tc.g, tc.m) != (C, R, g, m):
+        raise ValueError("out_rows / out_cols have the wrong shape or format")
+    return tr, tc
+
+
+def quantize_dual(x: torch.Tensor, g: int = 16, m: int = 4, rounding: str = "nearest", seed_rows: int = 0,
+                  seed_cols: int = 0, status: torch.Tensor | None = None, out_rows: BFPTensor | None = None,
+                  out_cols: BFPTensor | None = None):
+    """Both groupings of a 2-D [R, C] FP32 tensor from one read: ``(tr, tc)``
+    with tr = quantize(x, -1, seed=seed_rows) ([R, C], groups along rows) and
+    tc = quantize(x, 0, seed=seed_cols) ([C, R], groups down the columns)."""
+    _need_cuda(x, "x", torch.float32)
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D")
+    R, C = x.shape
+    tr, tc = _dual_outputs(R, C, g, m, x.device, out_rows, out_cols)
+    check(load().bfp_quantize_dual(ctypes.c_void_p(x.data_ptr()), R, C, g, m, ROUNDING[rounding],
+                                   ctypes.c_uint64(seed_rows & 0xFFFFFFFFFFFFFFFF),
+                                   ctypes.c_uint64(seed_cols & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(tr.mant.data_ptr()),
+                                   ctypes.c_void_p(tr.exp.data_ptr()), ctypes.c_void_p(tc.mant.data_ptr()),
+                                   ctypes.c_void_p(tc.exp.data_ptr()), _status_ptr(status), _stream(x.device)),
+          "bfp_quantize_dual")
+    return tr, tc
+
+
+def weight_update(w: torch.Tensor, dw: torch.Tensor, alpha: float, g: int = 16, m: int = 4,
+                  rounding: str = "nearest", seed_rows: int = 0, seed_cols: int = 0, w_out: torch.Tensor | None = None,
+                  status: torch.Tensor | None = None, out_rows: BFPTensor | None = None,
+                  out_cols: BFPTensor | None = None):
+    """w_out = w + alpha * dw (FP32, product and sum each rounded; w_out = w
+    updates in place when passed as w) and both groupings of the result, as
+    quantize_dual.  Returns ``(w_out, tr, tc)``."""
+    _need_cuda(w, "w", torch.float32)
+    _need_cuda(dw, "dw", torch.float32)
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    if w.dim() != 2 or dw.shape != w.shape:
+        raise ValueError("w must be 2-D and dw of the same shape")
+    R, C = w.shape
+    if w_out is None:
+        w_out = torch.empty_like(w)
+    else:
+        _need_cuda(w_out, "w_out", torch.float32)
+        if w_out.shape != w.shape:
+            raise ValueError("w_out has the wrong shape")
+    tr, tc = _dual_outputs(R, C, g, m, w.device, out_rows, out_cols)
+    check(load().bfp_weight_update(ctypes.c_void_p(w.data_ptr()), ctypes.c_void_p(dw.data_ptr()), ctypes.c_float(alpha),
+                                   ctypes.c_void_p(w_out.data_ptr()), R, C, g, m, ROUNDING[rounding],
+                                   ctypes.c_uint64(seed_rows & 0xFFFFFFFFFFFFFFFF),
+                                   ctypes.c_uint64(seed_cols & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(tr.mant.data_ptr()),
+                                   ctypes.c_void_p(tr.exp.data_ptr()), ctypes.c_void_p(tc.mant.data_ptr()),
+                                   ctypes.c_void_p(tc.exp.data_ptr()), _status_ptr(status), _stream(w.device)),
+          "bfp_weight_update")
+    return w_out, tr, tc
 
 
 def quantize_adaptive(x: torch.Tensor, group_axis: int = -1, g: int = 16, rounding: str = "nearest",

@@ -28,6 +28,9 @@ SIGNATURES = {
     "bfp_gemm": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _I64, _P]),
     "bfp_gemm_group_partials": (_I, [_P, _I, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _P]),
     "bfp_gemm_bfp": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _I, _I, _U64, _P, _P, _P, _P]),
+    "bfp_quantize_dual": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P, _P]),
+    "bfp_weight_update": (_I, [_P, _P, ctypes.c_float, _P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P,
+                               _P]),
     "bfp_quantize_adaptive": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _P, _P, _P, _P, _P, _P]),
     "bfp_adaptive_sums_len": (_I64, [_I64, _I64, _I, _I]),
     "bfp_adaptive_threshold": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, _I64, _I64, _I64, _I64]),

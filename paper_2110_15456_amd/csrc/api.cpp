@@ -45,6 +45,20 @@ int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, i
   return BFP_OK;
 }
 
+int check_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, const uint8_t* mr,
+               const uint8_t* er, const uint8_t* mc, const uint8_t* ec, const uint32_t* status_word) {
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  int st = check_tensor(R, C, g, m_bits);
+  if (st != BFP_OK) return st;
+  if (g != 16) return BFP_E_UNSUPPORTED;
+  if (R % 16 != 0) return BFP_E_SHAPE;
+  if (C >= (int64_t(1) << 22)) return BFP_E_UNSUPPORTED;
+  if (R == 0 || C == 0) return BFP_OK;
+  if (!x || !mr || !er || !mc || !ec) return BFP_E_ARG;
+  if (!aligned(x, 16) || !aligned(mr, 4) || !aligned(mc, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
+  return BFP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -145,6 +159,29 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
   return status_of(fastbfp::launch_group_partials(a_mant, a_m_bits, na, b_mant, b_m_bits, nb, M, N, K, g, P,
                                                   static_cast<hipStream_t>(stream)));
+}
+
+int bfp_quantize_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, uint64_t seed_r,
+                      uint64_t seed_c, uint8_t* mant_r, uint8_t* exp_r, uint8_t* mant_c, uint8_t* exp_c,
+                      uint32_t* status_word, void* stream) {
+  const int st = check_dual(x, R, C, g, m_bits, round_mode, mant_r, exp_r, mant_c, exp_c, status_word);
+  if (st != BFP_OK || R == 0 || C == 0) return st;
+  return status_of(fastbfp::launch_quantize_dual(x, R, C, m_bits, round_mode, seed_r, seed_c, mant_r, exp_r, mant_c,
+                                                 exp_c, status_word, static_cast<hipStream_t>(stream)));
+}
+
+int bfp_weight_update(const float* w, const float* dw, float alpha, float* w_out, int64_t R, int64_t C, int g,
+                      int m_bits, int round_mode, uint64_t seed_r, uint64_t seed_c, uint8_t* mant_r, uint8_t* exp_r,
+                      uint8_t* mant_c, uint8_t* exp_c, uint32_t* status_word, void* stream) {
+  const int st = check_dual(w, R, C, g, m_bits, round_mode, mant_r, exp_r, mant_c, exp_c, status_word);
+  if (st != BFP_OK || R == 0 || C == 0) return st;
+  if (!dw || !w_out || !aligned(dw, 16) || !aligned(w_out, 16)) return BFP_E_ARG;
+  const size_t bytes = (size_t)R * (size_t)C * 4;
+  const uintptr_t d0 = reinterpret_cast<uintptr_t>(dw), o0 = reinterpret_cast<uintptr_t>(w_out);
+  if (d0 < o0 + bytes && o0 < d0 + bytes) return BFP_E_ARG;  // dw overlaps w_out
+  return status_of(fastbfp::launch_weight_update(w, dw, alpha, w_out, R, C, m_bits, round_mode, seed_r, seed_c, mant_r,
+                                                 exp_r, mant_c, exp_c, status_word,
+                                                 static_cast<hipStream_t>(stream)));
 }
 
 int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode, uint64_t seed,

@@ -32,6 +32,16 @@ int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g);
 hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
                                     uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
                                     uint32_t* status, hipStream_t s);
+// Both groupings (g = 16) of x[R][C] from one read: mr/er along rows (seed_r),
+// mc/ec along columns (seed_c), in the layout of quantize.
+hipError_t launch_quantize_dual(const float* x, int64_t R, int64_t C, int m, int mode, uint64_t seed_r,
+                                uint64_t seed_c, uint8_t* mr, uint8_t* er, uint8_t* mc, uint8_t* ec,
+                                uint32_t* status, hipStream_t s);
+// w_out = w + alpha * dw (two FP32 roundings), then both groupings of w_out as
+// launch_quantize_dual.  w_out may be w.
+hipError_t launch_weight_update(const float* w, const float* dw, float alpha, float* w_out, int64_t R, int64_t C,
+                                int m, int mode, uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er,
+                                uint8_t* mc, uint8_t* ec, uint32_t* status, hipStream_t s);
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
                              float* y, hipStream_t s);
 // a_m / b_m: the stored operands' widths (they fix the plane formats and

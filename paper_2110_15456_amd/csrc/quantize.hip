@@ -351,6 +351,158 @@ hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int gr
   return hipGetLastError();
 }
 
+// Both groupings of a matrix from one read (and, with UPD, the weight update
+// in front of them).  x[R][C] is converted with groups of 16 along its rows
+// (output "r": rows = R, len = C, gid = r * C/16 + j) and along its columns
+// (output "c": rows = C, len = R, gid = c * R/16 + i), each byte for byte what
+// the single-axis kernels write with that output's seed.  UPD: the matrix is
+// x' = x + alpha * dx, computed as the two FP32 roundings of the product and
+// the sum (no fused multiply-add), written to x_out and converted.
+//
+// A block owns a 128 x 128 tile, staged in LDS once: row r's 16-byte granule
+// g sits at granule g ^ (r & 15), so that 16 lanes reading one granule of 16
+// consecutive rows (a row group each), and 64 lanes reading one float of 64
+// consecutive columns (a column group each), both hit distinct banks.  Each
+// thread then converts 4 row groups and 4 column groups.  Tile rows past R
+// read zero (the buffer resource ends at the last row); columns past C read
+// whatever follows in memory, and only whole groups past C are affected, which
+// are never stored.
+template <int MODE, int NCH, bool F0, bool UPD>
+__global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const float* dx, float alpha, float* x_out,
+                                                       int64_t R, int64_t C,
+                                                       int tiles_c, uint32_t m, uint32_t kr0, uint32_t kr1,
+                                                       uint32_t kc0, uint32_t kc1, uint8_t* __restrict__ mr0,
+                                                       uint8_t* __restrict__ mr1, uint8_t* __restrict__ er,
+                                                       uint8_t* __restrict__ mc0, uint8_t* __restrict__ mc1,
+                                                       uint8_t* __restrict__ ec, uint32_t* status) {
+  constexpr int T = 128;
+  __shared__ __attribute__((aligned(16))) float tile[T * T];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t r0 = (int64_t)(blockIdx.x / tiles_c) * T, c0 = (int64_t)(blockIdx.x % tiles_c) * T;
+  const int rows = (int)min((int64_t)T, R - r0);
+  typedef __attribute__((address_space(3))) void lds_void;
+  // Tile rows [r0, r0 + rows) of x (and dx); offsets are within 128 rows of C floats.
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(x + r0 * C), (short)0, (int)(rows * C * 4), 0x00020000);
+  // Granule slot q = 64 * (16 * wave + n) + lane: row q / 32, slot q % 32,
+  // which holds the row's granule (q % 32) ^ (row & 15).
+#pragma unroll
+  for (int n = 0; n < 16; ++n) {
+    const int q = 64 * (16 * wave + n) + lane, row = q >> 5, g = (q & 31) ^ (row & 15);
+    const uint32_t off = (uint32_t)(row * C + c0 + 4 * g) * 4u;
+    if constexpr (UPD) {
+      const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(dx + r0 * C), (short)0, (int)(rows * C * 4), 0x00020000);
+      const v4i a = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
+      const v4i d = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rd, off, 0, 0));
+      float4 v;
+      {
+        // Two roundings, never a fused multiply-add.
+#pragma clang fp contract(off)
+        v.x = __int_as_float(a[0]) + alpha * __int_as_float(d[0]);
+        v.y = __int_as_float(a[1]) + alpha * __int_as_float(d[1]);
+        v.z = __int_as_float(a[2]) + alpha * __int_as_float(d[2]);
+        v.w = __int_as_float(a[3]) + alpha * __int_as_float(d[3]);
+      }
+      *reinterpret_cast<float4*>(&tile[4 * q]) = v;
+      if (row < rows && c0 + 4 * g < C) *reinterpret_cast<float4*>(x_out + (r0 + row) * C + c0 + 4 * g) = v;
+    } else {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)&tile[4 * 64 * (16 * wave + n)], 16, off, 0, 0, 0);
+    }
+  }
+  if constexpr (!UPD) __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
+  __syncthreads();
+
+  bool bad = false;
+  uint32_t b[16], w[NCH][3], E, s_lo, s_hi;
+  bool nonfinite;
+  // Row groups: item it of wave w covers 16 rows x 4 groups.
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int idx = 4 * it + wave;
+    const int row = 16 * (idx >> 1) + (lane & 15), cg = 4 * (idx & 1) + (lane >> 4);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(&tile[row * T + 4 * ((4 * cg + u) ^ (row & 15))]);
+      b[4 * u] = v[0];
+      b[4 * u + 1] = v[1];
+      b[4 * u + 2] = v[2];
+      b[4 * u + 3] = v[3];
+    }
+    if (r0 + row < R && c0 + 16 * cg < C) {
+      const int64_t gid = (r0 + row) * (C / 16) + c0 / 16 + cg;
+      quantize_group<16, MODE, NCH, false, F0, false>(b, m, (uint64_t)gid, kr0, kr1, w, E, nonfinite, s_lo, s_hi);
+      er[gid] = (uint8_t)E;
+      store_group<16, NCH, F0, false>(mr0, mr1, gid, w);
+      bad |= nonfinite;
+    }
+  }
+  // Column groups: item it of wave w covers 64 columns x 1 group.
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int idx = 4 * it + wave;
+    const int rg = idx >> 1, col = 64 * (idx & 1) + lane;
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      b[u] = __float_as_uint(tile[(16 * rg + u) * T + 4 * ((col >> 2) ^ u) + (col & 3)]);
+    if (c0 + col < C && r0 + 16 * rg < R) {
+      const int64_t gid = (c0 + col) * (R / 16) + r0 / 16 + rg;
+      quantize_group<16, MODE, NCH, false, F0, false>(b, m, (uint64_t)gid, kc0, kc1, w, E, nonfinite, s_lo, s_hi);
+      ec[gid] = (uint8_t)E;
+      store_group<16, NCH, F0, false>(mc0, mc1, gid, w);
+      bad |= nonfinite;
+    }
+  }
+  if (status && bad) atomicOr(status, 1u);
+}
+
+template <int MODE, int NCH, bool F0, bool UPD>
+static hipError_t launch_dual_t(const float* x, const float* dx, float alpha, float* x_out, int64_t R, int64_t C, int m,
+                                uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er, uint8_t* mc, uint8_t* ec,
+                                uint32_t* status, hipStream_t s) {
+  const int64_t tiles_r = (R + 127) / 128, tiles_c = (C + 127) / 128;
+  const int64_t ng = R * (C / 16);  // groups per output (either grouping)
+  const int64_t b0 = plane_group_bytes(16, m, 0);
+  hipLaunchKernelGGL((k_quantize_dual<MODE, NCH, F0, UPD>), dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0, s, x,
+                     dx, alpha, x_out, R, C, (int)tiles_c, (uint32_t)m, (uint32_t)seed_r, (uint32_t)(seed_r >> 32),
+                     (uint32_t)seed_c, (uint32_t)(seed_c >> 32), mr, mr + ng * b0, er, mc, mc + ng * b0, ec, status);
+  return hipGetLastError();
+}
+
+template <bool UPD>
+static hipError_t launch_dual_any(const float* x, const float* dx, float alpha, float* x_out, int64_t R, int64_t C,
+                                  int m, int mode, uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er,
+                                  uint8_t* mc, uint8_t* ec, uint32_t* status, hipStream_t s) {
+  if (R == 0 || C == 0) return hipSuccess;
+#define FASTBFP_DUAL(MODE)                                                                                         \
+  do {                                                                                                             \
+    if (m <= 2) return launch_dual_t<MODE, 1, true, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, \
+                                                         ec, status, s);                                           \
+    if (m <= 4) return launch_dual_t<MODE, 1, false, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, \
+                                                          ec, status, s);                                          \
+    if (m <= 6) return launch_dual_t<MODE, 2, true, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, \
+                                                         ec, status, s);                                           \
+    return launch_dual_t<MODE, 2, false, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, ec, status, \
+                                              s);                                                                  \
+  } while (0)
+  if (mode == kNearest) FASTBFP_DUAL(kNearest);
+  if (mode == kStochastic) FASTBFP_DUAL(kStochastic);
+  FASTBFP_DUAL(kTruncate);
+#undef FASTBFP_DUAL
+}
+
+hipError_t launch_quantize_dual(const float* x, int64_t R, int64_t C, int m, int mode, uint64_t seed_r,
+                                uint64_t seed_c, uint8_t* mr, uint8_t* er, uint8_t* mc, uint8_t* ec,
+                                uint32_t* status, hipStream_t s) {
+  return launch_dual_any<false>(x, nullptr, 0.0f, nullptr, R, C, m, mode, seed_r, seed_c, mr, er, mc, ec, status, s);
+}
+
+hipError_t launch_weight_update(const float* w, const float* dw, float alpha, float* w_out, int64_t R, int64_t C,
+                                int m, int mode, uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er,
+                                uint8_t* mc, uint8_t* ec, uint32_t* status, hipStream_t s) {
+  return launch_dual_any<true>(w, dw, alpha, w_out, R, C, m, mode, seed_r, seed_c, mr, er, mc, ec, status, s);
+}
+
 template <int G, int NCH, bool F0>
 static hipError_t launch_deq_t(const uint8_t* mant, const uint8_t* exps, int64_t ngroups, int m, float* y,
                                hipStream_t s) {

@@ -219,3 +219,24 @@ def test_gemm_bfp_validation(lib):
     assert gb(lib, cmant=ctypes.c_void_p(0x100002)) == E_ARG
     assert gb(lib, st=ctypes.c_void_p(0x100001)) == E_ARG
     assert gb(lib, M=0) == OK and gb(lib, N=0) == OK
+
+
+def test_dual_and_update_validation(lib):
+    d = lib.bfp_quantize_dual
+    assert d(FAKE, 32, 64, 16, 4, 3, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_ARG      # bad rounding mode
+    assert d(FAKE, 24, 64, 16, 4, 0, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_SHAPE    # R % 16
+    assert d(FAKE, 32, 40, 16, 4, 0, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_SHAPE    # C % 16
+    assert d(FAKE, 32, 64, 32, 4, 0, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_UNSUP    # g = 32
+    assert d(FAKE, 32, 64, 16, 9, 0, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_PREC
+    assert d(None, 32, 64, 16, 4, 0, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_ARG
+    assert d(FAKE, 32, 64, 16, 4, 0, 0, 0, FAKE, None, FAKE, FAKE, None, None) == E_ARG
+    assert d(ctypes.c_void_p(0x100004), 32, 64, 16, 4, 0, 0, 0, FAKE, FAKE, FAKE, FAKE, None, None) == E_ARG
+    assert d(None, 0, 64, 16, 4, 0, 0, 0, None, None, None, None, None, None) == OK
+    u = lib.bfp_weight_update
+    args = lambda w=FAKE, dw=ctypes.c_void_p(0x200000), wo=FAKE, R=32: (w, dw, 1.0, wo, R, 64, 16, 4, 0, 0, 0, FAKE,
+                                                                         FAKE, FAKE, FAKE, None, None)
+    assert u(*args(dw=None)) == E_ARG
+    assert u(*args(wo=None)) == E_ARG
+    assert u(*args(dw=FAKE)) == E_ARG        # dw overlaps w_out
+    assert u(*args(R=24)) == E_SHAPE
+    assert u(*args(w=None, R=0)) == OK

@@ -405,3 +405,42 @@ def test_threshold_eq1_and_selection():
     assert oracle.select_mantissa(1.0, 4.0, 0.2500001) == 2
     assert oracle.select_mantissa(0.0, 0.0, 0.0) == 4    # r = 0, eps = 0: not below
     assert oracle.select_mantissa(0.0, 0.0, 0.1) == 2
+
+
+def test_weight_update_rounding_pins():
+    """W' = fl32(w + fl32(alpha * dw)): exact cases, a tie, and a case that a
+    fused multiply-add would get wrong."""
+    f = np.float32
+    # exact: small integers, and alpha = -1/2 on dw = w halves w
+    assert oracle.weight_update(f([3.0]), f([-5.0]), 1.0)[0] == f(-2.0)
+    assert oracle.weight_update(f([6.0]), f([6.0]), -0.5)[0] == f(3.0)
+    # 1 + 2^-24 is a tie between 1 and 1 + 2^-23: nearest-even gives 1
+    assert oracle.weight_update(f([1.0]), f([2.0 ** -24]), 1.0)[0] == f(1.0)
+    # 1 + 1.5 * 2^-24 rounds up to 1 + 2^-23
+    assert oracle.weight_update(f([1.0]), f([1.5 * 2.0 ** -24]), 1.0)[0] == f(1.0 + 2.0 ** -23)
+    # (1 + 2^-23)^2 = 1 + 2^-22 + 2^-46 rounds to 1 + 2^-22 before the sum, so
+    # adding -(1 + 2^-22) gives exactly 0 (a fused multiply-add gives 2^-46)
+    a = 1.0 + 2.0 ** -23
+    assert oracle.weight_update(f([-(1.0 + 2.0 ** -22)]), f([a]), a)[0] == f(0.0)
+    # subnormals are read as, and flushed to, zero of the same sign (and
+    # -0 + -0 = -0, -0 + +0 = +0): a negative subnormal gradient, a negative
+    # subnormal product, a subnormal weight
+    tiny = float(np.finfo(np.float32).tiny)
+    r = oracle.weight_update(f([-0.0, -0.0, 0.25 * tiny, -0.0]), f([-0.5 * tiny, -1e-30, 1.0, 0.5 * tiny]), 1e-9)
+    assert r[0] == 0.0 and np.signbit(r[0])
+    assert r[1] == 0.0 and np.signbit(r[1])
+    assert r[2] == np.float32(1e-9)
+    assert r[3] == 0.0 and not np.signbit(r[3])
+
+
+def test_quantize_dual_is_the_two_conversions():
+    """Each output of the dual conversion is the single-axis conversion of the
+    same matrix (transposed for the column grouping)."""
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((48, 32)).astype(np.float32)
+    (qr, er), (qc, ec), bad = oracle.quantize_dual(x, m=3, mode="stochastic", seed_rows=5, seed_cols=9)
+    assert bad == 0
+    q1, e1, _ = oracle.quantize(x, m=3, mode="stochastic", seed=5)
+    q2, e2, _ = oracle.quantize(np.ascontiguousarray(x.T), m=3, mode="stochastic", seed=9)
+    assert np.array_equal(qr, q1) and np.array_equal(er, e1)
+    assert np.array_equal(qc, q2) and np.array_equal(ec, e2)
