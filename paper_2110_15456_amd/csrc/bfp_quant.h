@@ -26,8 +26,8 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
 //   truncate:   q = floor(a)
 //   nearest:    q = (floor(2a) + 1) >> 1           (half an LSB added, ties up)
 //   stochastic: q = (floor(256a) + U) >> 8         (U = the noise byte)
-// Subnormal inputs are read as zero (explicitly: the result does not depend
-// on the FP32 denormal mode of the including file).
+// Subnormal inputs are read as zero: explicitly, or (FTZ true, only for
+// files built with FP32 denormals flushed) by the ldexp's own input flush.
 //
 // Plane formats: F0 / F1 true makes plane 0 / 1 an FP4 E2M1 plane (chunks of
 // at most 2 bits: the code is the sign bit above the chunk itself, 4 bits per
@@ -40,7 +40,7 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
 // chunk is discarded, q >> 2; s_lo and s_hi return the group's sums of q & 3
 // and q >> 2 (the magnitudes BFP(X,4) - BFP(X,2) and BFP(X,2) in units of
 // 2^(E-130) and 2^(E-128)).
-template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1>
+template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ = false>
 __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
                                                uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
                                                bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
@@ -85,7 +85,9 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
   }
 #pragma unroll
   for (int t = 0; t < G; ++t) {
-    const uint32_t abits = ((b[t] >> 23) & 0xFFu) ? (b[t] & 0x7FFFFFFFu) : 0u;  // subnormals read as zero
+    // subnormals read as zero: by the FP32 flush mode of the including file
+    // (FTZ), or explicitly
+    const uint32_t abits = (FTZ || ((b[t] >> 23) & 0xFFu)) ? (b[t] & 0x7FFFFFFFu) : 0u;
     const float mag = __builtin_ldexpf(__uint_as_float(abits), align);
     const uint32_t fl = (uint32_t)mag;  // truncating conversion: floor
     uint32_t q;

@@ -120,7 +120,7 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   uint32_t w[NCH][G * 6 / 32];
   uint32_t E, s_lo, s_hi;
   bool nonfinite;
-  quantize_group<G, MODE, NCH, ADAPT, F0, F1>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
+  quantize_group<G, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
   if (valid) {
     exps[gid] = (uint8_t)E;
     store_group<G, NCH, F0, F1>(mant0, mant1, gid, w);
@@ -169,7 +169,7 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       uint32_t w[NCH][WPG];
       uint32_t E, s_lo, s_hi;
       bool nonfinite;
-      quantize_group<G, MODE, NCH, ADAPT, F0, F1>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo,
+      quantize_group<G, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo,
                                                   s_hi);
       if (ADAPT) {
         num += ldexp((double)s_lo, (int)E - 130);
@@ -359,36 +359,48 @@ hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int gr
 // x' = x + alpha * dx, computed as the two FP32 roundings of the product and
 // the sum (no fused multiply-add), written to x_out and converted.
 //
-// A block owns a 128 x 128 tile, staged in LDS once: row r's 16-byte granule
-// g sits at granule g ^ (r & 15), so that 16 lanes reading one granule of 16
-// consecutive rows (a row group each), and 64 lanes reading one float of 64
-// consecutive columns (a column group each), both hit distinct banks.  Each
-// thread then converts 4 row groups and 4 column groups.  Tile rows past R
-// read zero (the buffer resource ends at the last row); columns past C read
-// whatever follows in memory, and only whole groups past C are affected, which
-// are never stored.
+// A block owns a 64 x 64 tile, staged in LDS once (16 KB, so that several
+// blocks per CU overlap one another's loads and conversions): row r's 16-byte
+// granule g sits at granule g ^ s(r), s(r) = (r & 15) ^ 4 ((r >> 4) & 3), so
+// that 16 lanes reading one granule of 16 consecutive rows (a row group
+// each), and 64 lanes reading one float of 16 columns x 4 group rows (a
+// column group each), both hit distinct banks.  Each thread then converts one
+// row group and one column group; the lanes of a wave store 16 output rows x
+// 4 consecutive groups in either grouping, i.e. contiguous 4-group runs.  Tile
+// rows past R read zero (the buffer resource ends at the last row); columns
+// past C read whatever follows in memory, and only whole groups past C are
+// affected, which are never stored.
 template <int MODE, int NCH, bool F0, bool UPD>
 __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const float* dx, float alpha, float* x_out,
-                                                       int64_t R, int64_t C,
-                                                       int tiles_c, uint32_t m, uint32_t kr0, uint32_t kr1,
-                                                       uint32_t kc0, uint32_t kc1, uint8_t* __restrict__ mr0,
-                                                       uint8_t* __restrict__ mr1, uint8_t* __restrict__ er,
-                                                       uint8_t* __restrict__ mc0, uint8_t* __restrict__ mc1,
-                                                       uint8_t* __restrict__ ec, uint32_t* status) {
-  constexpr int T = 128;
+                                                       int64_t R, int64_t C, int tiles_c, uint32_t m, uint32_t kr0,
+                                                       uint32_t kr1, uint32_t kc0, uint32_t kc1,
+                                                       uint8_t* __restrict__ mr0, uint8_t* __restrict__ mr1,
+                                                       uint8_t* __restrict__ er, uint8_t* __restrict__ mc0,
+                                                       uint8_t* __restrict__ mc1, uint8_t* __restrict__ ec,
+                                                       uint32_t* status) {
+  constexpr int T = 64;
   __shared__ __attribute__((aligned(16))) float tile[T * T];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int64_t r0 = (int64_t)(blockIdx.x / tiles_c) * T, c0 = (int64_t)(blockIdx.x % tiles_c) * T;
+  // Tile order: each XCD (workgroups are dealt to the 8 XCDs in turn) takes a
+  // contiguous run of tiles, walked in bands of 8 tile rows, down each band's
+  // column first: an output row of either grouping then receives 8
+  // neighbouring tiles' groups (384 bytes) at about the same time.
+  int lid = blockIdx.x;
+  if (gridDim.x % 8 == 0) lid = (blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8;
+  const int tiles_r = (int)((R + T - 1) / T), band = lid / (8 * tiles_c), in = lid % (8 * tiles_c);
+  const int band_rows = min(8, tiles_r - 8 * band);
+  const int64_t r0 = (int64_t)(8 * band + in % band_rows) * T, c0 = (int64_t)(in / band_rows) * T;
   const int rows = (int)min((int64_t)T, R - r0);
   typedef __attribute__((address_space(3))) void lds_void;
-  // Tile rows [r0, r0 + rows) of x (and dx); offsets are within 128 rows of C floats.
+  // Tile rows [r0, r0 + rows) of x (and dx); offsets are within 64 rows of C floats.
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(x + r0 * C), (short)0, (int)(rows * C * 4), 0x00020000);
-  // Granule slot q = 64 * (16 * wave + n) + lane: row q / 32, slot q % 32,
-  // which holds the row's granule (q % 32) ^ (row & 15).
+  // Granule slot q = 64 * (4 * wave + n) + lane: row q / 16, slot q % 16,
+  // which holds the row's granule (q % 16) ^ s(row).
+  auto swz = [](int row) { return (row & 15) ^ (((row >> 4) & 3) << 2); };
 #pragma unroll
-  for (int n = 0; n < 16; ++n) {
-    const int q = 64 * (16 * wave + n) + lane, row = q >> 5, g = (q & 31) ^ (row & 15);
+  for (int n = 0; n < 4; ++n) {
+    const int q = 64 * (4 * wave + n) + lane, row = q >> 4, g = (q & 15) ^ swz(row);
     const uint32_t off = (uint32_t)(row * C + c0 + 4 * g) * 4u;
     if constexpr (UPD) {
       const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
@@ -407,7 +419,7 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
       *reinterpret_cast<float4*>(&tile[4 * q]) = v;
       if (row < rows && c0 + 4 * g < C) *reinterpret_cast<float4*>(x_out + (r0 + row) * C + c0 + 4 * g) = v;
     } else {
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)&tile[4 * 64 * (16 * wave + n)], 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)&tile[4 * 64 * (4 * wave + n)], 16, off, 0, 0, 0);
     }
   }
   if constexpr (!UPD) __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
@@ -416,14 +428,12 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
   bool bad = false;
   uint32_t b[16], w[NCH][3], E, s_lo, s_hi;
   bool nonfinite;
-  // Row groups: item it of wave w covers 16 rows x 4 groups.
-#pragma unroll
-  for (int it = 0; it < 4; ++it) {
-    const int idx = 4 * it + wave;
-    const int row = 16 * (idx >> 1) + (lane & 15), cg = 4 * (idx & 1) + (lane >> 4);
+  {
+    // Row group: wave w covers rows 16 w .. 16 w + 15, lane block lb group lb.
+    const int row = 16 * wave + (lane & 15), cg = lane >> 4;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(&tile[row * T + 4 * ((4 * cg + u) ^ (row & 15))]);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(&tile[row * T + 4 * ((4 * cg + u) ^ swz(row))]);
       b[4 * u] = v[0];
       b[4 * u + 1] = v[1];
       b[4 * u + 2] = v[2];
@@ -431,23 +441,24 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
     }
     if (r0 + row < R && c0 + 16 * cg < C) {
       const int64_t gid = (r0 + row) * (C / 16) + c0 / 16 + cg;
-      quantize_group<16, MODE, NCH, false, F0, false>(b, m, (uint64_t)gid, kr0, kr1, w, E, nonfinite, s_lo, s_hi);
+      quantize_group<16, MODE, NCH, false, F0, false, true>(b, m, (uint64_t)gid, kr0, kr1, w, E, nonfinite, s_lo,
+                                                            s_hi);
       er[gid] = (uint8_t)E;
       store_group<16, NCH, F0, false>(mr0, mr1, gid, w);
       bad |= nonfinite;
     }
   }
-  // Column groups: item it of wave w covers 64 columns x 1 group.
-#pragma unroll
-  for (int it = 0; it < 4; ++it) {
-    const int idx = 4 * it + wave;
-    const int rg = idx >> 1, col = 64 * (idx & 1) + lane;
+  {
+    // Column group: wave w covers columns 16 w .. 16 w + 15, lane block lb
+    // group row lb.
+    const int rg = lane >> 4, col = 16 * wave + (lane & 15);
 #pragma unroll
     for (int u = 0; u < 16; ++u)
-      b[u] = __float_as_uint(tile[(16 * rg + u) * T + 4 * ((col >> 2) ^ u) + (col & 3)]);
+      b[u] = __float_as_uint(tile[(16 * rg + u) * T + 4 * ((col >> 2) ^ swz(16 * rg + u)) + (col & 3)]);
     if (c0 + col < C && r0 + 16 * rg < R) {
       const int64_t gid = (c0 + col) * (R / 16) + r0 / 16 + rg;
-      quantize_group<16, MODE, NCH, false, F0, false>(b, m, (uint64_t)gid, kc0, kc1, w, E, nonfinite, s_lo, s_hi);
+      quantize_group<16, MODE, NCH, false, F0, false, true>(b, m, (uint64_t)gid, kc0, kc1, w, E, nonfinite, s_lo,
+                                                            s_hi);
       ec[gid] = (uint8_t)E;
       store_group<16, NCH, F0, false>(mc0, mc1, gid, w);
       bad |= nonfinite;
@@ -460,7 +471,7 @@ template <int MODE, int NCH, bool F0, bool UPD>
 static hipError_t launch_dual_t(const float* x, const float* dx, float alpha, float* x_out, int64_t R, int64_t C, int m,
                                 uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er, uint8_t* mc, uint8_t* ec,
                                 uint32_t* status, hipStream_t s) {
-  const int64_t tiles_r = (R + 127) / 128, tiles_c = (C + 127) / 128;
+  const int64_t tiles_r = (R + 63) / 64, tiles_c = (C + 63) / 64;
   const int64_t ng = R * (C / 16);  // groups per output (either grouping)
   const int64_t b0 = plane_group_bytes(16, m, 0);
   hipLaunchKernelGGL((k_quantize_dual<MODE, NCH, F0, UPD>), dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0, s, x,

@@ -116,3 +116,15 @@ def test_dual_edges():
         fb.quantize_dual(torch.zeros((24, 64), dtype=torch.float32, device="cuda"))  # R not a multiple of 16
     with pytest.raises(fb.BFPError):
         fb.quantize_dual(torch.zeros((32, 64), dtype=torch.float32, device="cuda"), g=32)
+
+
+def test_dual_special_values():
+    """Zeros of both signs, subnormals, powers of two, ties and extremes."""
+    x = synth.special_values(64 * 256, seed=9).reshape(64, 256)
+    xt = torch.from_numpy(x).cuda()
+    for m in (2, 4, 8):
+        for mode in MODES:
+            announce("dual special values m=%d %s" % (m, mode))
+            tr, tc = fb.quantize_dual(xt, m=m, rounding=mode, seed_rows=1, seed_cols=2)
+            torch.cuda.synchronize()
+            check_against_oracle(x, tr, tc, m, mode, 1, 2)
