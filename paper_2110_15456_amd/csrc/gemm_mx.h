@@ -659,8 +659,10 @@ hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps
                        const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C, int64_t ldc,
                        const OutBFP* qo, hipStream_t s) {
   // The tile shrinks along an operand with two chunk planes so that two LDS
-  // stages fit in 160 KB.
-  using CF = mx::Cfg<(NA == 1 && NB == 1) ? FASTBFP_MX11_BM : NA == 1 ? FASTBFP_MX_BM : FASTBFP_MX_BM / 2,
+  // stages fit in 160 KB; with FP4 upper planes on both sides (192 bytes per
+  // slab row instead of 256) A keeps 256 rows.
+  constexpr bool WIDE22 = NA == 2 && NB == 2 && FA && FB;
+  using CF = mx::Cfg<(NA == 1 && NB == 1) ? FASTBFP_MX11_BM : (NA == 1 || WIDE22) ? FASTBFP_MX_BM : FASTBFP_MX_BM / 2,
                      (NA == 1 && NB == 1) ? FASTBFP_MX11_BN : NB == 1 ? FASTBFP_MX_BN : FASTBFP_MX_BN / 2, NA, NB, FA,
                      FB>;
   auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
