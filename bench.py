@@ -172,7 +172,30 @@ def gemm_sweep(torch, fb, synth, dev, args):
                 "mfma_issued_tflops": round(issued, 1), "frac_fp6_peak_issued": round(issued / PEAK_FP6_TFLOPS, 4)}
             log(args, "gemm %s (%d,%d): %.3f ms, %.0f eff TOPS" % (name, pa, pb, ms, tops))
         del C
-    del X, Wt
+    # groups of 32 (the sensitivity study's other group size): one whole group
+    # per MFMA block, no zero padding
+    M, N, K = shapes["ffn_up"]
+    xa, wb = X[:M, :K].contiguous(), Wt[:N, :K].contiguous()
+    C = torch.empty((M, N), dtype=torch.float32, device=dev)
+    for pa, pb in [(2, 2), (4, 4), (6, 6), (8, 8)]:
+        A, B = fb.quantize(xa, g=32, m=pa), fb.quantize(wb, g=32, m=pb)
+        fb.gemm(A, B, out=C)
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(5):
+            fb.gemm(A, B, out=C)
+        z.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(z) / 5
+        tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+        issued = tops * planes(pa) * planes(pb)  # chunk passes, no padding
+        out["ffn_up_g32(%d,%d)" % (pa, pb)] = {
+            "M": M, "N": N, "K": K, "g": 32, "ms": round(ms, 4), "eff_tops": round(tops, 1),
+            "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4), "mfma_issued_tflops": round(issued, 1),
+            "frac_fp6_peak_issued": round(issued / PEAK_FP6_TFLOPS, 4)}
+        log(args, "gemm ffn_up g=32 (%d,%d): %.3f ms, %.0f eff TOPS" % (pa, pb, ms, tops))
+    del X, Wt, C
     return out
 
 

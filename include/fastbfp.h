@@ -153,6 +153,8 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
  *   Passes: the kernel issues chunks(m_a) * chunks(m_b) block-scaled MFMA
  *   passes per group pair (1 for m_a, m_b <= 4), the counterpart of the
  *   paper's (m_a/2)(m_b/2) fMAC rounds.
+ *   g            : 16 or 32 (both operands).  A group of 32 fills a whole
+ *                  MFMA block; a group of 16 leaves half of it zero.
  *   C            : FP32 with row stride ldc >= N (elements).
  * Preconditions for the stated accuracy: every group exponent E is at most 250,
  * and every scaled group sum, partial sum and |C| stays in the FP32 normal range.
@@ -171,7 +173,8 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
  * axis 1, g = 16, c_m_bits, round_mode, seed) of the FP32 C that bfp_gemm
  * computes: the same values, the same noise addressing (gid = the index into
  * c_exp), without writing or re-reading FP32 C.
- *   Operands and precisions : as bfp_gemm (g = 16).
+ *   Operands and precisions : as bfp_gemm (g = 16 or 32 for the operands;
+ *                 the output is grouped by 16).
  *   c_m_bits    : 1..8.  round_mode, seed, status_word : as bfp_quantize.
  *   c_mant, c_exp : outputs sized by bfp_quantized_sizes(M, N, 16, c_m_bits).
  * N must be a multiple of 16 (BFP_E_SHAPE otherwise).

@@ -19,8 +19,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfastbfp.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
-SOURCES = ["quantize.hip", "gemm_mx.hip", "gemm_mx_11.hip", "gemm_mx_12.hip", "gemm_mx_21.hip", "gemm_mx_22.hip",
-           "gemm_i8.hip", "api.cpp"]
+SOURCES = ["quantize.hip", "gemm_mx.hip", "gemm_i8.hip", "api.cpp"] + [
+    "gemm_mx_%s%s.hip" % (p, g) for g in ("", "_g32") for p in ("11", "12", "21", "22")]
 # Per-source extra flags: the quantizer aligns values with ldexp and relies on
 # FP32 denormal flushing to read subnormal inputs as zero.
 SOURCE_FLAGS = {"quantize.hip": ["-fgpu-flush-denormals-to-zero"]}

@@ -125,9 +125,8 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
   if (ldc < N) return BFP_E_SHAPE;
   if (M == 0 || N == 0) return BFP_OK;
   if (!C || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
-  if (g != 16) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
-  return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K,
+  return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K, g,
                                            4 - m_a - m_b, C, ldc, static_cast<hipStream_t>(stream)));
 }
 
@@ -142,9 +141,8 @@ int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, cons
   if (M == 0 || N == 0) return BFP_OK;
   if (!c_mant || !c_exp || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
   if (!aligned(c_mant, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
-  if (g != 16) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
-  return status_of(fastbfp::launch_gemm_mx_bfp(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K,
+  return status_of(fastbfp::launch_gemm_mx_bfp(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K, g,
                                                4 - m_a - m_b, c_m_bits, round_mode, seed, c_mant, c_exp, status_word,
                                                static_cast<hipStream_t>(stream)));
 }

@@ -68,9 +68,17 @@ constexpr int NT = 64 * WGM * WGN;
 constexpr int KG = 8;            // groups per K slab (two MFMA K-steps)
 // NA / NB: chunk planes of A / B read; FA / FB: 1 if plane 0 of A / B holds
 // FP4 codes (plane 1 always holds FP6 codes).
-template <int BM_, int BN_, int NA_, int NB_, int FA_, int FB_>
+// G: the operands' group size, 16 or 32.  A slab is 8 groups of 16 (KG) or
+// 4 of 32: the mantissa planes of a g = 32 tensor are laid out exactly like
+// those of a g = 16 tensor with twice the groups (each group is its two
+// 16-value halves), so the staging works in 16-value halves either way; EK
+// exponent bytes per row and slab.
+template <int BM_, int BN_, int NA_, int NB_, int FA_, int FB_, int G_ = 16>
 struct Cfg {
-  static constexpr int BM = BM_, BN = BN_, NA = NA_, NB = NB_, FA = FA_, FB = FB_;
+  static constexpr int BM = BM_, BN = BN_, NA = NA_, NB = NB_, FA = FA_, FB = FB_, G = G_;
+  static constexpr int EK = KG * 16 / G;      // exponents per row and slab
+  static constexpr int KSTEPS = G == 16 ? 2 : 1;  // MFMA K-steps per slab
+  static_assert(G == 16 || G == 32, "group size 16 or 32");
   static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
   static constexpr int TM = WM / 16, TN = WN / 16;    // 16x16 MFMA tiles per wave
   // LDS bytes per row of a slab: 8 slots of one group (FP6) or 4 slots of a
@@ -80,13 +88,13 @@ struct Cfg {
   static constexpr int OFF_B = OFF_A1 + (NA == 2 ? BM * 128 : 0);
   static constexpr int OFF_B1 = OFF_B + BN * RB0;                // B's plane 1
   static constexpr int OFF_EA = OFF_B1 + (NB == 2 ? BN * 128 : 0);
-  static constexpr int OFF_EB = OFF_EA + BM * KG;
-  static constexpr int SPARE = OFF_EB + BN * KG;  // 8 bytes written by threads without an exponent row
+  static constexpr int OFF_EB = OFF_EA + BM * EK;
+  static constexpr int SPARE = OFF_EB + BN * EK;  // EK bytes written by threads without an exponent row
   static constexpr int STAGE = SPARE + 16;
   static constexpr int EXP_ROWS_PER_T = (BM + BN + NT - 1) / NT;
   // Explicitly software-pipelined fragment reads (one chunk per operand);
   // otherwise the compiler schedules them.
-  static constexpr bool PIPE = FASTBFP_MX_PIPE11 && NA == 1 && NB == 1;
+  static constexpr bool PIPE = FASTBFP_MX_PIPE11 && NA == 1 && NB == 1 && G == 16;
   static_assert(TM * 16 * WGM == BM && TN * 16 * WGN == BN, "wave tiles cover the tile");
   static_assert((BM + BN) % 64 == 0 && BM % 64 == 0 && BN % 64 == 0,
                 "loads split evenly over the waves; whole waves skip exponent rows past BM + BN");
@@ -127,15 +135,16 @@ __device__ __forceinline__ void tile_of(int bid, int nblocks, int tiles_m, int t
   tn = in / rows_in_group;
 }
 
-// Exponents of one slab for one row (8 bytes), zero past the last group and
-// for rows past the end.
+// Exponents of one slab for one row (EK bytes of ng_e per row), zero past
+// the last group and for rows past the end.
+template <int EK>
 __device__ __forceinline__ uint2 load_exps(const uint8_t* __restrict__ exps, int row, int row_end, int ng, int slab) {
   const bool rok = row < row_end;
-  const int64_t base = (int64_t)(rok ? row : 0) * ng + slab * mx::KG;
-  const int gvalid = min(mx::KG, ng - slab * mx::KG);
+  const int64_t base = (int64_t)(rok ? row : 0) * ng + slab * EK;
+  const int gvalid = min(EK, ng - slab * EK);
   uint32_t w[2] = {0u, 0u};
 #pragma unroll
-  for (int j = 0; j < mx::KG; ++j) {
+  for (int j = 0; j < EK; ++j) {
     const uint32_t b = exps[base + min(j, gvalid - 1)];
     w[j >> 2] |= ((rok && j < gvalid) ? b : 0u) << (8 * (j & 3));
   }
@@ -192,19 +201,22 @@ __device__ __forceinline__ void load_plane4(uint8_t* lds_plane, rsrc_t rsrc, uin
   }
 }
 
-// Direct buffer->LDS loads of one full slab of exponents (8 bytes per row, as
-// two dwords) for ROWS rows: row r lands at lds_exps + 8 r.  lane_off is
-// (lane / 2) * ng + (lane % 2) * 4.
-template <int ROWS>
-__device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, uint32_t lane_off, int ng, int slab,
-                                              int wave) {
-  constexpr int INSTR = ROWS * 2 / 64;
-  static_assert(INSTR % 4 == 0, "exponent loads split evenly over the waves");
+// Direct buffer->LDS loads of one full slab of exponents (EK bytes per row,
+// as DPR = EK / 4 dwords) for ROWS rows: row r lands at lds_exps + EK r.
+// lane_off is (lane / DPR) * ng + (lane % DPR) * 4.  Instructions past the
+// last (when they do not split evenly over the four waves) go through the
+// zero-length resource rnull into the sink.
+template <int ROWS, int EK>
+__device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, rsrc_t rnull, uint8_t* sink,
+                                              uint32_t lane_off, int ng, int slab, int wave) {
+  constexpr int DPR = EK / 4, INSTR = ROWS * DPR / 64;
 #pragma unroll
-  for (int u = 0; u < INSTR / 4; ++u) {
+  for (int u = 0; u < (INSTR + 3) / 4; ++u) {
     const int blk = wave + 4 * u;
-    const uint32_t off = lane_off + (uint32_t)blk * 32u * (uint32_t)ng + (uint32_t)slab * mx::KG;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_exps + blk * 256), 4, off, 0, 0, 0);
+    const bool ok = INSTR % 4 == 0 || blk < INSTR;
+    const uint32_t off = lane_off + (uint32_t)blk * (64u / DPR) * (uint32_t)ng + (uint32_t)slab * EK;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ok ? rsrc : rnull, (lds_void*)(ok ? lds_exps + blk * 256 : sink), 4, off,
+                                             0, 0, 0);
   }
 }
 
@@ -312,7 +324,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     src = is_a ? a_exp : b_exp;
     grow = (is_a ? row0 : col0) + rr;
     gend = is_a ? M : N;
-    lds = (is_a ? CF::OFF_EA : CF::OFF_EB) + rr * mx::KG;
+    lds = (is_a ? CF::OFF_EA : CF::OFF_EB) + rr * CF::EK;
   };
   // Per-tile resources and the lane parts of the load offsets.  Row bytes in
   // HBM: 12 per group in an FP6 plane, 8 in an FP4 plane.
@@ -338,9 +350,12 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // slot of row r holding pair slot ^ ((r >> 2) & 3).
   const int p_lane = (lane & 3) ^ ((lane >> 4) & 3);
   const uint32_t m4_lane_off = (uint32_t)(lane >> 2) * rb4 + (uint32_t)p_lane * 16u;
-  const rsrc_t rea = make_rsrc(a_exp + (int64_t)row0 * ng, (uint32_t)(a_rows * ng));
-  const rsrc_t reb = make_rsrc(b_exp + (int64_t)col0 * ng, (uint32_t)(b_rows * ng));
-  const uint32_t e_lane_off = (uint32_t)(lane >> 1) * (uint32_t)ng + (uint32_t)(lane & 1) * 4u;
+  // Exponents: ng_e per row (one per group of G).
+  const int ng_e = ng * 16 / CF::G;
+  const rsrc_t rea = make_rsrc(a_exp + (int64_t)row0 * ng_e, (uint32_t)(a_rows * ng_e));
+  const rsrc_t reb = make_rsrc(b_exp + (int64_t)col0 * ng_e, (uint32_t)(b_rows * ng_e));
+  constexpr int DPR = CF::EK / 4;
+  const uint32_t e_lane_off = (uint32_t)(lane / DPR) * (uint32_t)ng_e + (uint32_t)(lane % DPR) * 4u;
 
   // Exponents: with full slabs, direct loads like the mantissas.  Otherwise
   // through registers (zeros are needed past K): this thread handles rows
@@ -361,7 +376,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
         const uint8_t* src;
         int grow, gend, lds;
         exp_row(k, src, grow, gend, lds);
-        e[k] = load_exps(src, grow, gend, ng, slab);
+        e[k] = load_exps<CF::EK>(src, grow, gend, ng_e, slab);
       }
     }
     const bool g_ok = slab * mx::KG + g_lane < ng;
@@ -385,8 +400,10 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
                                       wave);
     }
     if constexpr (EXP_FULL) {
-      load_exps_lds<CF::BM>(stage + CF::OFF_EA, live ? rea : rnull, e_lane_off, ng, slab, wave);
-      load_exps_lds<CF::BN>(stage + CF::OFF_EB, live ? reb : rnull, e_lane_off, ng, slab, wave);
+      load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, pf_sink + wave * 256, e_lane_off,
+                                    ng_e, slab, wave);
+      load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, pf_sink + wave * 256, e_lane_off,
+                                    ng_e, slab, wave);
     }
     // Last: the NPF prefetches of slab + 1, which the next step does not wait for.
 #pragma unroll
@@ -416,7 +433,8 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
         int grow, gend, lds;
         exp_row(k, src, grow, gend, lds);
         if (tid + k * mx::NT >= CF::BM + CF::BN) lds = CF::SPARE;
-        *reinterpret_cast<uint2*>(stage + lds) = e[k];
+        if constexpr (CF::EK == 8) *reinterpret_cast<uint2*>(stage + lds) = e[k];
+        else *reinterpret_cast<uint32_t*>(stage + lds) = e[k].x;
       }
     }
   };
@@ -458,8 +476,10 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     // (Every address is one offset from the stage base, which keeps the
     // accesses attributable to the stage object.)
     const int a_r = wr * CF::WM + lr, b_r = wc * CF::WN + lr;
-    const int ea_lane = CF::OFF_EA + a_r * mx::KG + 2 * lb;
-    const int eb_lane = CF::OFF_EB + b_r * mx::KG + 2 * lb;
+    // the exponent of lane block lb's group in K-step ks: group 2 lb + ks
+    // (G = 16) or lb (G = 32, one K-step)
+    const int ea_lane = CF::OFF_EA + a_r * CF::EK + (CF::G == 16 ? 2 * lb : lb);
+    const int eb_lane = CF::OFF_EB + b_r * CF::EK + (CF::G == 16 ? 2 * lb : lb);
     // Byte offset of the 16-byte slot of row tile t, K-step ks, in a plane of
     // format fp4 starting at plane_off, for a lane of row r.
     auto slot_addr = [&](int plane_off, int fp4, int r, int t, int ks) {
@@ -467,24 +487,33 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
                  : plane_off + (r + 16 * t) * 128 + (((2 * lb + ks) ^ swz6) * 16);
     };
     auto rd = [&](int off) { return *reinterpret_cast<const u32x4*>(cur + off); };
+    // G = 32: the operand is the whole group, with no padding -- the FP4 slot
+    // as read, or the 12 bytes of each of the two FP6 half-group slots.
+    auto op32 = [&](int fp4, int plane_off, int r, int t) -> v8i {
+      const u32x4 x = rd(slot_addr(plane_off, fp4, r, t, 0));
+      if (fp4) return v8i{(int)x[0], (int)x[1], (int)x[2], (int)x[3], 0, 0, 0, 0};
+      const u32x4 y = rd(slot_addr(plane_off, 0, r, t, 1));
+      return v8i{(int)x[0], (int)x[1], (int)x[2], (int)y[0], (int)y[1], (int)y[2], 0, 0};
+    };
     if constexpr (CF::PIPE) {
       // Software pipeline.  A block is the TN MFMAs of one A fragment (row
       // tile i) against the B fragments of K-step ks; a phase is one K-step,
       // TM blocks.  Each block reads the next block's A fragment and a share
       // of the next phase's B fragments, and a scheduling barrier closes it,
       // so that about two blocks' fragments are live at a time.
-      constexpr int BPP = TM;  // blocks per phase
-      constexpr int NPH = 2;   // phases per slab
+      constexpr int BPP = TM;           // blocks per phase
+      constexpr int NPH = CF::KSTEPS;   // phases per slab
       v8i bf[2][TN], af[2];
       int be[2][TN], ae[2];
       auto read_b = [&](int ks, int j) {
-        bf[ks & 1][j] = op_b<FA, FB>(rd(slot_addr(CF::OFF_B, FB, b_r, j, ks)), ks);
-        be[ks & 1][j] = (int)cur[eb_lane + j * 16 * mx::KG + ks];
+        bf[ks & 1][j] = CF::G == 16 ? op_b<FA, FB>(rd(slot_addr(CF::OFF_B, FB, b_r, j, ks)), ks)
+                                    : op32(FB, CF::OFF_B, b_r, j);
+        be[ks & 1][j] = (int)cur[eb_lane + j * 16 * CF::EK + ks];
       };
       auto read_a = [&](int blk) {
         const int ks = blk / BPP, i = blk % BPP;
-        af[blk & 1] = op_a<FA, FB>(rd(slot_addr(0, FA, a_r, i, ks)), ks);
-        ae[blk & 1] = (int)cur[ea_lane + i * 16 * mx::KG + ks];
+        af[blk & 1] = CF::G == 16 ? op_a<FA, FB>(rd(slot_addr(0, FA, a_r, i, ks)), ks) : op32(FA, 0, a_r, i);
+        ae[blk & 1] = (int)cur[ea_lane + i * 16 * CF::EK + ks];
       };
 #pragma unroll
       for (int j = 0; j < TN; ++j) read_b(0, j);
@@ -492,11 +521,11 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
       // An FP4 slot serves both K-steps; the empty asm statements (here and
       // at the phase boundary) keep the compiler from merging the two phases'
       // reads of it, which would hold every raw fragment for the whole slab.
-      if constexpr (FA || FB) asm volatile("" ::: "memory");
+      if constexpr ((FA || FB) && NPH == 2) asm volatile("" ::: "memory");
 #pragma unroll
       for (int blk = 0; blk < NPH * BPP; ++blk) {
         const int ph = blk / BPP, bi = blk % BPP, i = blk % TM;
-        if constexpr (FA || FB)
+        if constexpr ((FA || FB) && NPH == 2)
           if (blk == BPP) asm volatile("" ::: "memory");
         if (blk + 1 < NPH * BPP) read_a(blk + 1);
         if (ph + 1 < NPH) {
@@ -510,6 +539,31 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
                                                                        ae[blk & 1], 0, be[ph & 1][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
+    } else if constexpr (CF::G == 32) {
+      // Compiler-scheduled, one K-step: per B chunk the B fragments, then each
+      // A fragment against them.
+      static_for<NB>([&](auto cbc) {
+        constexpr int cb = decltype(cbc)::value, fb = mx::b_fp4<CF>(cb);
+        v8i bv[TN];
+        int eb[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          bv[j] = op32(fb, mx::b_plane<CF>(cb), b_r, j);
+          eb[j] = (int)cur[eb_lane + j * 16 * CF::EK] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
+        }
+        static_for<NA>([&](auto cac) {
+          constexpr int ca = decltype(cac)::value, fa = mx::a_fp4<CF>(ca);
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const v8i av = op32(fa, mx::a_plane<CF>(ca), a_r, i);
+            const int ea = (int)cur[ea_lane + i * 16 * CF::EK] + 4 * (NA - 1 - ca);
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+                  av, bv[j], acc[i][j], mfma_fmt<fa>::value, mfma_fmt<fb>::value, 0, ea, 0, eb[j]);
+          }
+        });
+      });
     } else {
       // Compiler-scheduled: per K-step and B chunk, the B fragments, then each
       // A fragment against them.
@@ -522,14 +576,14 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
             y[j] = rd(slot_addr(mx::b_plane<CF>(cb), fb, b_r, j, ks));
-            eb[j] = (int)cur[eb_lane + j * 16 * mx::KG + ks] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
+            eb[j] = (int)cur[eb_lane + j * 16 * CF::EK + ks] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
           }
           static_for<NA>([&](auto cac) {
             constexpr int ca = decltype(cac)::value, fa = mx::a_fp4<CF>(ca);
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
               const v8i av = op_a<fa, fb>(rd(slot_addr(mx::a_plane<CF>(ca), fa, a_r, i, ks)), ks);
-              const int ea = (int)cur[ea_lane + i * 16 * mx::KG + ks] + 4 * (NA - 1 - ca);
+              const int ea = (int)cur[ea_lane + i * 16 * CF::EK + ks] + 4 * (NA - 1 - ca);
 #pragma unroll
               for (int j = 0; j < TN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
@@ -653,8 +707,9 @@ static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64
 }
 
 // One operand-format combination: NA / NB planes read, FA / FB plane 0 of A /
-// B in FP4.  a_ps / b_ps: byte offset of plane 1 (the stored plane 0's size).
-template <int NA, int NB, int FA, int FB>
+// B in FP4, G the group size.  a_ps / b_ps: byte offset of plane 1 (the stored
+// plane 0's size); ng: 16-value halves (K / 16) per row.
+template <int NA, int NB, int FA, int FB, int G>
 hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps, const uint8_t* b_mant,
                        const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C, int64_t ldc,
                        const OutBFP* qo, hipStream_t s) {
@@ -664,21 +719,22 @@ hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps
   constexpr bool WIDE22 = NA == 2 && NB == 2 && FA && FB;
   using CF = mx::Cfg<(NA == 1 && NB == 1) ? FASTBFP_MX11_BM : (NA == 1 || WIDE22) ? FASTBFP_MX_BM : FASTBFP_MX_BM / 2,
                      (NA == 1 && NB == 1) ? FASTBFP_MX11_BN : NB == 1 ? FASTBFP_MX_BN : FASTBFP_MX_BN / 2, NA, NB, FA,
-                     FB>;
+                     FB, G>;
   auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
   // direct exponent loads need full slabs and 4-byte aligned exponent rows
-  const bool ef = ng % mx::KG == 0 && al(a_exp, 4) && al(b_exp, 4);
+  const bool ef = ng % mx::KG == 0 && al(a_exp, 4) && al(b_exp, 4);  // (K a multiple of 128 either way)
   if (ef) return launch_mx_v<CF, true>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
   return launch_mx_v<CF, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
 }
 
-#define FASTBFP_MX_DECLARE(NA, NB, FA, FB)                                                                      \
-  extern template hipError_t launch_mx_t<NA, NB, FA, FB>(const uint8_t*, const uint8_t*, int64_t, const uint8_t*, \
-                                                         const uint8_t*, int64_t, int, int, int, float, float*,   \
-                                                         int64_t, const OutBFP*, hipStream_t);
-#define FASTBFP_MX_INSTANTIATE(NA, NB, FA, FB)                                                           \
-  template hipError_t launch_mx_t<NA, NB, FA, FB>(const uint8_t*, const uint8_t*, int64_t, const uint8_t*, \
-                                                  const uint8_t*, int64_t, int, int, int, float, float*, int64_t, \
-                                                  const OutBFP*, hipStream_t);
+#define FASTBFP_MX_DECLARE(NA, NB, FA, FB, G)                                                          \
+  extern template hipError_t launch_mx_t<NA, NB, FA, FB, G>(const uint8_t*, const uint8_t*, int64_t,       \
+                                                            const uint8_t*, const uint8_t*, int64_t, int, int, \
+                                                            int, float, float*, int64_t, const OutBFP*,         \
+                                                            hipStream_t);
+#define FASTBFP_MX_INSTANTIATE(NA, NB, FA, FB, G)                                                           \
+  template hipError_t launch_mx_t<NA, NB, FA, FB, G>(const uint8_t*, const uint8_t*, int64_t, const uint8_t*, \
+                                                     const uint8_t*, int64_t, int, int, int, float, float*,     \
+                                                     int64_t, const OutBFP*, hipStream_t);
 
 }  // namespace fastbfp

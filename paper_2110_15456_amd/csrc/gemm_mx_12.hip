@@ -1,12 +1,12 @@
-// gemm_mx_12.hip -- the BFP GEMM with 1 chunk plane(s) of A and 2 of B, every
-// plane-0 format (FP6 or FP4 codes) of either operand.
+// gemm_mx_12.hip -- the BFP GEMM with 1 chunk plane(s) of A and 2 of B, groups of
+// 16, every plane-0 format (FP6 or FP4 codes) of either operand.
 #include "gemm_mx.h"
 
 namespace fastbfp {
 
-FASTBFP_MX_INSTANTIATE(1, 2, 0, 0)
-FASTBFP_MX_INSTANTIATE(1, 2, 0, 1)
-FASTBFP_MX_INSTANTIATE(1, 2, 1, 0)
-FASTBFP_MX_INSTANTIATE(1, 2, 1, 1)
+FASTBFP_MX_INSTANTIATE(1, 2, 0, 0, 16)
+FASTBFP_MX_INSTANTIATE(1, 2, 0, 1, 16)
+FASTBFP_MX_INSTANTIATE(1, 2, 1, 0, 16)
+FASTBFP_MX_INSTANTIATE(1, 2, 1, 1, 16)
 
 }  // namespace fastbfp

@@ -45,15 +45,16 @@ hipError_t launch_weight_update(const float* w, const float* dw, float alpha, fl
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
                              float* y, hipStream_t s);
 // a_m / b_m: the stored operands' widths (they fix the plane formats and
-// plane stride); na / nb: chunk planes read (1 or 2).  scale_log2 =
-// 4 - m_a - m_b.
+// plane stride); na / nb: chunk planes read (1 or 2); g: 16 or 32.
+// scale_log2 = 4 - m_a - m_b.
 hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
-                          const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
-                          float* C, int64_t ldc, hipStream_t s);
+                          const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int g,
+                          int scale_log2, float* C, int64_t ldc, hipStream_t s);
 // bfp_gemm with the output converted in the epilogue: groups of 16 along each
 // row of C at c_m bits (rounding mode and Philox seed as for quantize).
 hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
-                              const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int scale_log2,
+                              const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int g,
+                              int scale_log2,
                               int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status,
                               hipStream_t s);
 hipError_t launch_group_partials(const uint8_t* a_mant, int a_m, int na, const uint8_t* b_mant, int b_m, int nb,

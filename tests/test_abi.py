@@ -215,7 +215,7 @@ def test_gemm_bfp_validation(lib):
     assert gb(lib, K=40) == E_SHAPE
     assert gb(lib, cm=0) == E_PREC and gb(lib, cm=9) == E_PREC
     assert gb(lib, am=8, ma=5) == E_PREC
-    assert gb(lib, g=32, K=64) == E_UNSUP
+    assert gb(lib, g=8, K=64) == E_UNSUP
     assert gb(lib, cmant=ctypes.c_void_p(0x100002)) == E_ARG
     assert gb(lib, st=ctypes.c_void_p(0x100001)) == E_ARG
     assert gb(lib, M=0) == OK and gb(lib, N=0) == OK

@@ -19,10 +19,10 @@ TOL = 1e-6
 
 
 def operands(xa, xb, m_a_st, m_b_st, a_axis=-1, b_axis=-1, mode_a="nearest", mode_b="nearest", seed=0,
-             rows=None):
+             rows=None, g=16):
     """GPU BFP tensors plus the oracle's own quantization of the same inputs."""
-    A, qa, ea = check_quantize(xa, a_axis, 16, m_a_st, mode_a, seed=seed, rows=None)
-    B, qb, eb = check_quantize(xb, b_axis, 16, m_b_st, mode_b, seed=seed + 1)
+    A, qa, ea = check_quantize(xa, a_axis, g, m_a_st, mode_a, seed=seed, rows=None)
+    B, qb, eb = check_quantize(xb, b_axis, g, m_b_st, mode_b, seed=seed + 1)
     return A, B, (qa, ea), (qb, eb)
 
 
@@ -33,7 +33,7 @@ def check_gemm(A, B, oa, ob, m_a=None, m_b=None, rows=None, partials=False):
     torch.cuda.synchronize()
     Cg = C.cpu().numpy().astype(np.float64)
     idx = np.arange(A.rows) if rows is None else np.asarray(rows)
-    Co, S = oracle.gemm(oa[0], oa[1], A.m, ob[0], ob[1], B.m, g=16, m_a=m_a, m_b=m_b, rows=idx, threads=THREADS)
+    Co, S = oracle.gemm(oa[0], oa[1], A.m, ob[0], ob[1], B.m, g=A.g, m_a=m_a, m_b=m_b, rows=idx, threads=THREADS)
     err = np.abs(Cg[idx] - Co)
     ratio = err / np.maximum(S, 1e-300)
     worst = np.unravel_index(np.argmax(ratio), ratio.shape)
@@ -41,7 +41,7 @@ def check_gemm(A, B, oa, ob, m_a=None, m_b=None, rows=None, partials=False):
         ratio[worst], worst, Cg[idx][worst], Co[worst])
     if partials:
         P = fb.gemm_group_partials(A, B, m_a, m_b).cpu().numpy()
-        Po = oracle.group_partials(oa[0], A.m, ob[0], B.m, g=16, m_a=m_a, m_b=m_b, rows=idx)
+        Po = oracle.group_partials(oa[0], A.m, ob[0], B.m, g=A.g, m_a=m_a, m_b=m_b, rows=idx)
         assert np.array_equal(P[:, idx, :].astype(np.int64), Po)
     return float(ratio.max())
 
@@ -160,3 +160,47 @@ def test_ffn_backward_shapes_sampled():
     qa, ea, _ = oracle.quantize(x, axis=0, g=16, m=6, threads=THREADS)
     qb, eb, _ = oracle.quantize(dy, axis=0, g=16, m=6, mode="stochastic", seed=7, threads=THREADS)
     check_gemm(A, B, (qa, ea), (qb, eb), rows=rows)
+
+
+# Groups of 32: one whole group per MFMA block (no padding), every kernel
+# variant, full and ragged K slabs, at sizes spanning several tiles.
+G32_SHAPES = [(300, 200, 608), (257, 129, 512), (1, 1, 32), (64, 300, 4096)]
+
+
+@pytest.mark.parametrize("K", [32, 64, 96])
+def test_g32_tiny_all_precisions(K):
+    x = synth.draw("normal", (8, K), 700 + K)
+    for am in range(1, 9):
+        for bm in range(1, 9):
+            announce("gemm g=32 tiny K=%d stored (%d,%d)" % (K, am, bm))
+            A, B, oa, ob = operands(x[:4], x[4:], am, bm, g=32)
+            for m_a in sorted({am, am - 4} - {-3, -2, -1, 0}):
+                for m_b in sorted({bm, bm - 4} - {-3, -2, -1, 0}):
+                    check_gemm(A, B, oa, ob, m_a, m_b, partials=True)
+
+
+@pytest.mark.parametrize("shape", G32_SHAPES)
+def test_g32_ragged_shapes(shape):
+    M, N, K = shape
+    xa = synth.draw("half_normal", (M, K), 710 + M + K)
+    xb = synth.draw("grads", (N, K), 720 + N + K)
+    for pa, pb in PAIRS:
+        announce("gemm g=32 %dx%dx%d (%d,%d)" % (M, N, K, pa, pb))
+        A, B, oa, ob = operands(xa, xb, pa, pb, g=32, mode_b="stochastic", seed=4)
+        check_gemm(A, B, oa, ob, partials=(M * N * K <= 64 * 64 * 2048))
+
+
+def test_g32_ffn_shape_sampled():
+    """The FFN up-projection (8192 x 16384 x 4096) with groups of 32 at (4,4) and
+    (6,6): sampled rows against the oracle."""
+    M, N, K = 8192, 16384, 4096
+    xa = synth.draw("half_normal", (M, K), 730)
+    xb = synth.draw("weights", (N, K), 731)
+    rows = np.random.default_rng(5).choice(M, 48, replace=False)
+    for pair in [(4, 4), (6, 6)]:
+        announce("gemm g=32 ffn_up %s" % (pair,))
+        A = fb.quantize(torch.from_numpy(xa).cuda(), g=32, m=pair[0])
+        B = fb.quantize(torch.from_numpy(xb).cuda(), g=32, m=pair[1])
+        qa, ea, _ = oracle.quantize(xa, g=32, m=pair[0], threads=THREADS, rows=None)
+        qb, eb, _ = oracle.quantize(xb, g=32, m=pair[1], threads=THREADS)
+        check_gemm(A, B, (qa, ea), (qb, eb), rows=rows)

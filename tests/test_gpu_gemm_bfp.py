@@ -120,3 +120,20 @@ def test_fused_full_size_sampled():
     rows = torch.from_numpy(np.random.default_rng(1).choice(M, 256, replace=False)).cuda()
     assert torch.equal(tm[rows], rm[rows])
     assert torch.equal(T.mant, R.mant)
+
+
+def test_fused_with_g32_operands():
+    """Operands grouped by 32 (the output is still grouped by 16 along N)."""
+    M, N, K = 200, 208, 640
+    a = synth.draw("half_normal", (M, K), 4300)
+    b = synth.draw("weights", (N, K), 4301)
+    for m_a, m_b in ((4, 4), (2, 6), (8, 3)):
+        A = fb.quantize(torch.from_numpy(a).cuda(), g=32, m=m_a)
+        B = fb.quantize(torch.from_numpy(b).cuda(), g=32, m=m_b)
+        C = fb.gemm(A, B)
+        for c_m in (2, 4, 6):
+            announce("gemm_bfp g=32 operands (%d,%d) -> m=%d" % (m_a, m_b, c_m))
+            T = fb.gemm_bfp(A, B, c_m, rounding="stochastic", seed=8)
+            R = fb.quantize(C, g=16, m=c_m, rounding="stochastic", seed=8)
+            torch.cuda.synchronize()
+            assert torch.equal(T.exp, R.exp) and torch.equal(T.mant, R.mant)
