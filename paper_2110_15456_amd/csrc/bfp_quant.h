@@ -14,9 +14,26 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
   return __builtin_fmaf((float)c, neg_half, 0.0f);  // 0 * -0.5 + 0 = +0
 }
 
-// Quantize one group whose FP32 bit patterns are in b[].  Writes the packed
-// chunk planes to w[plane][...] and the shared exponent to E_out; nonfinite is
-// set if any input was Inf/NaN.
+typedef float v16f_t __attribute__((ext_vector_type(16)));
+typedef uint32_t v6u_t __attribute__((ext_vector_type(6)));
+
+// The gfx950 FP6 converter (32 FP32 values -> 32 packed E2M3 codes, scale
+// 1), issued with an early-clobber result: its destination must not overlap
+// its sources, which the compiler otherwise allows -- a destination placed a
+// few registers into a source gave wrong codes (it overwrote inputs before
+// they were read).
+__device__ __forceinline__ v6u_t cvt_fp6_x32(v16f_t a, v16f_t b) {
+  v6u_t r;
+  asm("v_cvt_scalef32_2xpk16_fp6_f32 %0, %1, %2, 1.0" : "=&v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Quantize NG consecutive groups (gid, gid + 1, ...) whose FP32 bit patterns
+// are in b[], packed together as one run of NG * G values.  Writes the packed
+// chunk planes to w[plane][...] and the shared exponents to E_out; nonfinite
+// is set if any input was Inf/NaN.  Two 16-value groups fill the 32 inputs of
+// the FP6 converter exactly, and their codes are the two groups' codes side by
+// side, as stored.
 //
 // Alignment is done in floating point, exactly: with the shared exponent E,
 // one LSB is 2^(E-127-(m-1)), so a = |x| / LSB = ldexp(|x|, 127 + (m-1) - E)
@@ -40,38 +57,52 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
 // chunk is discarded, q >> 2; s_lo and s_hi return the group's sums of q & 3
 // and q >> 2 (the magnitudes BFP(X,4) - BFP(X,2) and BFP(X,2) in units of
 // 2^(E-130) and 2^(E-128)).
-template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ = false>
-__device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
-                                               uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
-                                               bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
+template <int G, int NG, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ>
+__device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uint32_t m, uint64_t gid, uint32_t key0,
+                                                uint32_t key1, uint32_t (&w)[NCH][NG * G * 6 / 32],
+                                                uint32_t (&E_out)[NG], bool& nonfinite, uint32_t& s_lo,
+                                                uint32_t& s_hi) {
+  static_assert(NG == 1 || (!ADAPT && G == 16), "several groups per call: 16-value groups, not adaptive");
   constexpr bool FP4[2] = {F0, F1};
+  constexpr int LEN = NG * G;  // values converted together (one packing unit)
   s_lo = 0u;
   s_hi = 0u;
-  // (a) shared exponent: the largest biased exponent field in the group.
-  uint32_t E = 0;
+  nonfinite = false;
+  // (a) shared exponent of each group: the largest biased exponent field.
+  uint32_t E[NG];
 #pragma unroll
-  for (int t = 0; t < G; ++t) E = max(E, (b[t] >> 23) & 0xFFu);
-  E_out = E;
-  nonfinite = (E == 255u);
+  for (int gi = 0; gi < NG; ++gi) {
+    E[gi] = 0;
+#pragma unroll
+    for (int t = 0; t < G; ++t) E[gi] = max(E[gi], (b[gi * G + t] >> 23) & 0xFFu);
+    E_out[gi] = E[gi];
+    nonfinite |= (E[gi] == 255u);
+  }
 
-  uint32_t noise[G / 4];
+  uint32_t noise[LEN / 4];
   if (MODE == kStochastic) {
 #pragma unroll
-    for (int blk = 0; blk < G / 16; ++blk) {
-      const uint4 r = philox4x32_10(make_uint4((uint32_t)gid, (uint32_t)(gid >> 32), (uint32_t)blk, 0u), key0, key1);
-      noise[4 * blk + 0] = r.x;
-      noise[4 * blk + 1] = r.y;
-      noise[4 * blk + 2] = r.z;
-      noise[4 * blk + 3] = r.w;
-    }
+    for (int gi = 0; gi < NG; ++gi)
+#pragma unroll
+      for (int blk = 0; blk < G / 16; ++blk) {
+        const uint64_t id = gid + (uint64_t)gi;
+        const uint4 r = philox4x32_10(make_uint4((uint32_t)id, (uint32_t)(id >> 32), (uint32_t)blk, 0u), key0, key1);
+        noise[gi * G / 4 + 4 * blk + 0] = r.x;
+        noise[gi * G / 4 + 4 * blk + 1] = r.y;
+        noise[gi * G / 4 + 4 * blk + 2] = r.z;
+        noise[gi * G / 4 + 4 * blk + 3] = r.w;
+      }
   }
 
   const uint32_t qmax = (1u << m) - 1u;
-  // (b) the exponent that aligns a value to the group's LSB (times 2 for
+  // (b) the exponent that aligns a value to its group's LSB (times 2 for
   // nearest, 256 for stochastic rounding).
-  const int align = 127 + (int)m - 1 - (int)E + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
+  int align[NG];
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi)
+    align[gi] = 127 + (int)m - 1 - (int)E[gi] + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
   typedef float v16f __attribute__((ext_vector_type(16)));
-  constexpr int NH = G / 32 + (G % 32 != 0);
+  constexpr int NH = LEN / 32 + (LEN % 32 != 0);
   v16f ev[NCH][NH], od[NCH][NH];
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
@@ -81,14 +112,14 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
       od[p][h] = v16f{};
     }
 #pragma unroll
-    for (int i = 0; i < G * 6 / 32; ++i) w[p][i] = 0u;
+    for (int i = 0; i < LEN * 6 / 32; ++i) w[p][i] = 0u;
   }
 #pragma unroll
-  for (int t = 0; t < G; ++t) {
+  for (int t = 0; t < LEN; ++t) {
     // subnormals read as zero: by the FP32 flush mode of the including file
     // (FTZ), or explicitly
     const uint32_t abits = (FTZ || ((b[t] >> 23) & 0xFFu)) ? (b[t] & 0x7FFFFFFFu) : 0u;
-    const float mag = __builtin_ldexpf(__uint_as_float(abits), align);
+    const float mag = __builtin_ldexpf(__uint_as_float(abits), align[t / G]);
     const uint32_t fl = (uint32_t)mag;  // truncating conversion: floor
     uint32_t q;
     if (MODE == kNearest) {
@@ -135,11 +166,22 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
     if (FP4[p]) continue;
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
-      const v6u cv = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(ev[p][h], od[p][h], 1.0f);
+      const v6u cv = cvt_fp6_x32(ev[p][h], od[p][h]);
 #pragma unroll
-      for (int i = 0; i < 6 && 6 * h + i < G * 6 / 32; ++i) w[p][6 * h + i] = cv[i];
+      for (int i = 0; i < 6 && 6 * h + i < LEN * 6 / 32; ++i) w[p][6 * h + i] = cv[i];
     }
   }
+}
+
+
+// One group (the common case).
+template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ = false>
+__device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
+                                               uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
+                                               bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
+  uint32_t E[1];
+  quantize_groups<G, 1, MODE, NCH, ADAPT, F0, F1, FTZ>(b, m, gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
+  E_out = E[0];
 }
 
 // Stores plane p's codes of group gid (from quantize_group) at

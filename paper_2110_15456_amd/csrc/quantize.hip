@@ -71,11 +71,13 @@ __global__ __launch_bounds__(256) void k_improvement_finalize(double* sums, int6
 }
 
 // Groups along the contiguous last axis: group gid covers x[gid*G, gid*G+G).
-// Each wave owns 64 consecutive groups.  Their FP32 values are brought into
-// the wave's LDS region by direct global->LDS 16-byte loads, each of which
-// reads 1 KB contiguous (one lane per 16-byte chunk), and every lane then reads
-// its own group back.  The chunk j of group l lands in 16-byte slot
-// CPG*l + (j ^ swz(l)): the XOR spreads the 16 lanes served together across
+// A lane owns GPL consecutive groups (two of 16 -- one 32-value packing unit
+// of the FP6 converter -- or one of 32; one of 16 on the adaptive path), a
+// wave 64 * GPL groups.  Their FP32 values are brought into the wave's LDS
+// region by direct global->LDS 16-byte loads, each of which reads 1 KB
+// contiguous (one lane per 16-byte chunk), and every lane then reads its own
+// groups back.  The chunk c of lane l's run lands in 16-byte slot
+// CPL*l + (c ^ swz(l)): the XOR spreads the 16 lanes served together across
 // all 64 banks on the read-back.  (Reading 64 contiguous bytes per lane
 // straight from global memory instead leaves each load instruction touching
 // 64 scattered 16-byte pieces, which costs about a third of HBM bandwidth.)
@@ -84,51 +86,64 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
                                                        uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
                                                        uint32_t* status, double* sums) {
-  constexpr int CPG = G / 4;             // 16-byte chunks per group
-  constexpr int LANES_PER_SWZ = 16 / CPG;
-  __shared__ __attribute__((aligned(16))) uint32_t stage[4][64 * G];
+  constexpr int GPL = (G == 16 && !ADAPT) ? 2 : 1;  // groups per lane
+  constexpr int CPG = G / 4;                         // 16-byte chunks per group
+  constexpr int CPL = GPL * CPG;                     // 16-byte chunks per lane
+  constexpr int LANES_PER_SWZ = 16 / CPL;
+  __shared__ __attribute__((aligned(16))) uint32_t stage[4][64 * 4 * CPL];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t g0 = ((int64_t)blockIdx.x * 4 + wave) * 64;  // first group of this wave
+  const int64_t g0 = ((int64_t)blockIdx.x * 4 + wave) * 64 * GPL;  // first group of this wave
   if (!ADAPT && g0 >= ngroups) return;  // (the adaptive path keeps every wave for its block sums)
-  const int64_t nvalid = max((int64_t)0, min((int64_t)64, ngroups - g0));
+  const int nvalid = (int)max((int64_t)0, min((int64_t)(64 * GPL), ngroups - g0));
   typedef __attribute__((address_space(3))) void lds_void;
-  const uint8_t* base = reinterpret_cast<const uint8_t*>(x) + g0 * (G * 4);
+  // (a wave with no valid group, kept by the adaptive path, reads x's first groups)
+  const uint8_t* base = reinterpret_cast<const uint8_t*>(x) + (nvalid > 0 ? g0 * (G * 4) : 0);
+  const int qmax_chunk = max(nvalid, 1) * CPG - 1;  // the wave's last valid chunk
 #pragma unroll
-  for (int k = 0; k < CPG; ++k) {
+  for (int k = 0; k < CPL; ++k) {
     const int slot = 64 * k + lane;
-    const int l = slot / CPG;
-    const int j = (slot % CPG) ^ ((l / LANES_PER_SWZ) % CPG);
-    // chunks of groups past the end read the wave's first chunk instead (unused)
-    const int64_t off = (l < nvalid) ? (int64_t)(l * CPG + j) * 16 : -g0 * (G * 4);  // x's first chunk
+    const int l = slot / CPL;
+    const int c = (slot % CPL) ^ ((l / LANES_PER_SWZ) % CPL);
+    // chunks of groups past the end reread the wave's last valid chunk (unused)
+    const int off = min(l * CPL + c, qmax_chunk) * 16;
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + off),
                                      (lds_void*)(&stage[wave][64 * 4 * k]), 16, 0, 0);
   }
   __builtin_amdgcn_s_waitcnt(0);  // the wave reads back what its own loads wrote
-  const bool valid = lane < nvalid;
-  if (!ADAPT && !valid) return;  // (the adaptive path keeps every lane for its wave sums)
-  uint32_t b[G];
+  const int nmine = min(GPL, max(0, nvalid - lane * GPL));  // this lane's valid groups
+  if (!ADAPT && nmine == 0) return;  // (the adaptive path keeps every lane for its wave sums)
+  uint32_t b[GPL * G];
 #pragma unroll
-  for (int j = 0; j < CPG; ++j) {
-    const int slot = CPG * lane + (j ^ ((lane / LANES_PER_SWZ) % CPG));
+  for (int c = 0; c < CPL; ++c) {
+    const int slot = CPL * lane + (c ^ ((lane / LANES_PER_SWZ) % CPL));
     const u32x4 v = *reinterpret_cast<const u32x4*>(&stage[wave][4 * slot]);
-    b[4 * j + 0] = v[0];
-    b[4 * j + 1] = v[1];
-    b[4 * j + 2] = v[2];
-    b[4 * j + 3] = v[3];
+    b[4 * c + 0] = v[0];
+    b[4 * c + 1] = v[1];
+    b[4 * c + 2] = v[2];
+    b[4 * c + 3] = v[3];
   }
-  const int64_t gid = g0 + lane;
-  uint32_t w[NCH][G * 6 / 32];
-  uint32_t E, s_lo, s_hi;
+  const int64_t gid = g0 + lane * GPL;
+  uint32_t w[NCH][GPL * G * 6 / 32];
+  uint32_t E[GPL], s_lo, s_hi;
   bool nonfinite;
-  quantize_group<G, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
-  if (valid) {
-    exps[gid] = (uint8_t)E;
-    store_group<G, NCH, F0, F1>(mant0, mant1, gid, w);
+  quantize_groups<G, GPL, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo,
+                                                          s_hi);
+  if (GPL == 2 && nmine == 2) {
+    // both groups: one packing unit of 32 values (its bytes are the two
+    // groups' bytes side by side) and two exponent bytes
+    *reinterpret_cast<uint16_t*>(exps + gid) = (uint16_t)(E[0] | (E[GPL - 1] << 8));
+    store_group<GPL * G, NCH, F0, F1>(mant0, mant1, gid / GPL, w);
+    if (status && nonfinite) atomicOr(status, 1u);
+  } else if (nmine > 0) {
+    // one group (GPL = 1, or the last group of an odd count): its own bytes
+    exps[gid] = (uint8_t)E[0];
+    store_plane<G, F0>(mant0, gid, w[0]);
+    if (NCH == 2) store_plane<G, F1>(mant1, gid, w[NCH - 1]);
     if (status && nonfinite) atomicOr(status, 1u);
   }
   if (ADAPT)
-    block_improvement(valid ? ldexp((double)s_lo, (int)E - 130) : 0.0, valid ? ldexp((double)s_hi, (int)E - 128) : 0.0,
-                      sums + 2);
+    block_improvement(nmine ? ldexp((double)s_lo, (int)E[0] - 130) : 0.0,
+                      nmine ? ldexp((double)s_hi, (int)E[0] - 128) : 0.0, sums + 2);
 }
 
 // Groups down the columns of x[R][C] (transpose-on-quantize).  Output row c is
@@ -247,7 +262,8 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
 template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
 static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
                                 uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
-  const int64_t blocks = (ngroups + 255) / 256;
+  constexpr int GPL = (G == 16 && !ADAPT) ? 2 : 1;  // groups per lane (as in the kernel)
+  const int64_t blocks = (ngroups + 256 * GPL - 1) / (256 * GPL);
   hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, F0, F1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
                      (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
   return hipGetLastError();
