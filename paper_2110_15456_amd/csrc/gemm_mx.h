@@ -268,6 +268,64 @@ __device__ __forceinline__ v8i op_b(const u32x4& y, int ks) {
 // template constant: the intrinsic needs a literal).
 template <int FP4> struct mfma_fmt { static constexpr int value = FP4 ? 4 : 2; };
 
+#ifndef FASTBFP_MX_TIED
+#define FASTBFP_MX_TIED 1
+#endif
+typedef int v6i __attribute__((ext_vector_type(6)));
+// acc += the block-scaled product of one K-step (A format FA, B format FB,
+// block scales sa / sb).  The intrinsic's instruction form does not tie the
+// result to the accumulator input, so with 256 accumulator registers live the
+// register allocator moves accumulators between registers every slab (several
+// hundred accumulator moves per 128 MFMAs).  The tied form below keeps every
+// accumulator in one register quad for the whole loop.  Written as inline
+// assembly the instruction is invisible to the compiler's hazard tracking, so
+// it carries its own wait states: two for a VALU write of an operand just
+// before it; the accumulators are only ever written by these instructions
+// inside the loop (back-to-back accumulation into the same registers needs no
+// wait), and mma_drain() covers the reads after it.  The statement is not
+// volatile: a volatile one would also keep the scheduler from moving fragment
+// reads across it.
+template <int FA, int FB>
+__device__ __forceinline__ void mma(v4f& acc, const v8i& a, const v8i& b, int sa, int sb) {
+#if FASTBFP_MX_TIED
+  const v4i a4 = __builtin_shufflevector(a, a, 0, 1, 2, 3);
+  const v4i b4 = __builtin_shufflevector(b, b, 0, 1, 2, 3);
+  const v6i a6 = __builtin_shufflevector(a, a, 0, 1, 2, 3, 4, 5);
+  const v6i b6 = __builtin_shufflevector(b, b, 0, 1, 2, 3, 4, 5);
+  if constexpr (FA && FB)
+    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:4"
+                 : "+a"(acc) : "v"(a4), "v"(b4), "v"(sa), "v"(sb));
+  else if constexpr (FA)
+    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:2"
+                 : "+a"(acc) : "v"(a4), "v"(b6), "v"(sa), "v"(sb));
+  else if constexpr (FB)
+    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:2 blgp:4"
+                 : "+a"(acc) : "v"(a6), "v"(b4), "v"(sa), "v"(sb));
+  else
+    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:2 blgp:2"
+                 : "+a"(acc) : "v"(a6), "v"(b6), "v"(sa), "v"(sb));
+#else
+  acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, mfma_fmt<FA>::value, mfma_fmt<FB>::value, 0, sa, 0,
+                                                         sb);
+#endif
+}
+// Wait states between the last MFMA and any other read of its accumulators
+// (a 16x16x128 block-scaled MFMA needs at most 19).  Every accumulator then
+// passes through an empty statement that comes after them (volatile
+// statements keep their order), so that every later read -- including copies
+// the register allocator places at block boundaries, which no scheduling
+// barrier orders -- depends on it.
+template <int TM, int TN>
+__device__ __forceinline__ void mma_drain(v4f (&acc)[TM][TN]) {
+#if FASTBFP_MX_TIED
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));
+#endif
+}
+
 // Where the epilogue puts C: FP32 rows (QNCH = 0), or BFP with groups of 16
 // along each row of C (the next GEMM's K) at c_m bits in QNCH chunk planes --
 // the converter of section V-C applied to the FP32 results in the epilogue.
@@ -534,9 +592,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
         }
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af[blk & 1], bf[ph & 1][j], acc[i][j],
-                                                                       mfma_fmt<FA>::value, mfma_fmt<FB>::value, 0,
-                                                                       ae[blk & 1], 0, be[ph & 1][j]);
+          mma<FA, FB>(acc[i][j], af[blk & 1], bf[ph & 1][j], ae[blk & 1], be[ph & 1][j]);
         __builtin_amdgcn_sched_barrier(0);
       }
     } else if constexpr (CF::G == 32) {
@@ -559,8 +615,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
             const int ea = (int)cur[ea_lane + i * 16 * CF::EK] + 4 * (NA - 1 - ca);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-                  av, bv[j], acc[i][j], mfma_fmt<fa>::value, mfma_fmt<fb>::value, 0, ea, 0, eb[j]);
+              mma<fa, fb>(acc[i][j], av, bv[j], ea, eb[j]);
           }
         });
       });
@@ -586,8 +641,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
               const int ea = (int)cur[ea_lane + i * 16 * CF::EK + ks] + 4 * (NA - 1 - ca);
 #pragma unroll
               for (int j = 0; j < TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-                    av, op_b<fa, fb>(y[j], ks), acc[i][j], mfma_fmt<fa>::value, mfma_fmt<fb>::value, 0, ea, 0, eb[j]);
+                mma<fa, fb>(acc[i][j], av, op_b<fa, fb>(y[j], ks), ea, eb[j]);
             }
           });
         });
@@ -602,6 +656,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     step(stage1, stage0, s + 1);
   }
   if (s < nslabs) step(stage0, stage1, s);
+  mma_drain(acc);
 
   // Epilogue: lane holds rows 4*lb + r, column lr of each 16x16 tile.
   if constexpr (QNCH == 0) {
