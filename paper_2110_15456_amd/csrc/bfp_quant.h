@@ -14,6 +14,23 @@ __device__ __forceinline__ float signed_half(uint32_t c, float neg_half) {
   return __builtin_fmaf((float)c, neg_half, 0.0f);  // 0 * -0.5 + 0 = +0
 }
 
+// Cache policy of the streaming accesses of the conversion kernels (every
+// input element is read once and every output byte written once): nt, so the
+// lines do not displace others in L2.  Measured on the row quantizer: 72-78%
+// of HBM peak against 64-71% with the default policy.  Only for loads, and for
+// stores whose wave writes whole contiguous lines: stores of scattered groups
+// (the two-grouping conversion's 12-byte groups) rely on L2 to merge partial
+// lines from neighbouring workgroups, and as nt stores ran 2-3x slower.
+constexpr int kStreamPolicy = 2;
+template <class T>
+__device__ __forceinline__ void stream_store(T* p, T v) {
+  __builtin_nontemporal_store(v, p);
+}
+template <class T>
+__device__ __forceinline__ T stream_load(const T* p) {
+  return __builtin_nontemporal_load(p);
+}
+
 typedef float v16f_t __attribute__((ext_vector_type(16)));
 typedef uint32_t v6u_t __attribute__((ext_vector_type(6)));
 
@@ -186,16 +203,25 @@ __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t 
 
 // Stores plane p's codes of group gid (from quantize_group) at
 // mant_p + gid * bytes-per-group: 8 or 12 bytes per 16 values.
-template <int G, bool FP4>
+template <class T, bool STREAM>
+__device__ __forceinline__ void put(T* p, T v) {
+  if constexpr (STREAM) stream_store(p, v);
+  else *p = v;
+}
+// STREAM: nt stores (for a wave that writes whole contiguous lines).
+template <int G, bool FP4, bool STREAM = false>
 __device__ __forceinline__ void store_plane(uint8_t* __restrict__ mant, int64_t gid, const uint32_t* w) {
+  typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+  typedef uint32_t u3 __attribute__((ext_vector_type(3)));
   if (FP4) {
-    uint2* dst = reinterpret_cast<uint2*>(mant + gid * (G / 2));
+    u2* dst = reinterpret_cast<u2*>(mant + gid * (G / 2));
 #pragma unroll
-    for (int i = 0; i < G / 16; ++i) dst[i] = make_uint2(w[2 * i], w[2 * i + 1]);
+    for (int i = 0; i < G / 16; ++i) put<u2, STREAM>(dst + i, u2{w[2 * i], w[2 * i + 1]});
   } else {
-    uint3* dst = reinterpret_cast<uint3*>(mant + gid * (G * 3 / 4));
+    uint8_t* dst = mant + gid * (G * 3 / 4);
 #pragma unroll
-    for (int i = 0; i < G / 16; ++i) dst[i] = make_uint3(w[3 * i], w[3 * i + 1], w[3 * i + 2]);
+    for (int i = 0; i < G / 16; ++i)
+      put<u3, STREAM>(reinterpret_cast<u3*>(dst + 12 * i), u3{w[3 * i], w[3 * i + 1], w[3 * i + 2]});
   }
 }
 

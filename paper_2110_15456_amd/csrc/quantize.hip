@@ -16,11 +16,11 @@ namespace fastbfp {
 
 // Plane p of the group goes to mant_p (plane 1 of a two-chunk tensor, or the
 // separate 2-bit tensor of the adaptive path).
-template <int G, int NCH, bool F0, bool F1>
+template <int G, int NCH, bool F0, bool F1, bool STREAM = false>
 __device__ __forceinline__ void store_group(uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1, int64_t gid,
                                             const uint32_t (&w)[NCH][G * 6 / 32]) {
-  store_plane<G, F0>(mant0, gid, w[0]);
-  if (NCH == 2) store_plane<G, F1>(mant1, gid, w[NCH - 1]);
+  store_plane<G, F0, STREAM>(mant0, gid, w[0]);
+  if (NCH == 2) store_plane<G, F1, STREAM>(mant1, gid, w[NCH - 1]);
 }
 
 // Writes the block's Eq. 2 partial sums to part[2 * blockIdx.x + {0, 1}]:
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
     // chunks of groups past the end reread the wave's last valid chunk (unused)
     const int off = min(l * CPL + c, qmax_chunk) * 16;
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(base + off),
-                                     (lds_void*)(&stage[wave][64 * 4 * k]), 16, 0, 0);
+                                     (lds_void*)(&stage[wave][64 * 4 * k]), 16, 0, kStreamPolicy);
   }
   __builtin_amdgcn_s_waitcnt(0);  // the wave reads back what its own loads wrote
   const int nmine = min(GPL, max(0, nvalid - lane * GPL));  // this lane's valid groups
@@ -131,14 +131,14 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   if (GPL == 2 && nmine == 2) {
     // both groups: one packing unit of 32 values (its bytes are the two
     // groups' bytes side by side) and two exponent bytes
-    *reinterpret_cast<uint16_t*>(exps + gid) = (uint16_t)(E[0] | (E[GPL - 1] << 8));
-    store_group<GPL * G, NCH, F0, F1>(mant0, mant1, gid / GPL, w);
+    stream_store(reinterpret_cast<uint16_t*>(exps + gid), (uint16_t)(E[0] | (E[GPL - 1] << 8)));
+    store_group<GPL * G, NCH, F0, F1, true>(mant0, mant1, gid / GPL, w);
     if (status && nonfinite) atomicOr(status, 1u);
   } else if (nmine > 0) {
     // one group (GPL = 1, or the last group of an odd count): its own bytes
     exps[gid] = (uint8_t)E[0];
-    store_plane<G, F0>(mant0, gid, w[0]);
-    if (NCH == 2) store_plane<G, F1>(mant1, gid, w[NCH - 1]);
+    store_plane<G, F0, true>(mant0, gid, w[0]);
+    if (NCH == 2) store_plane<G, F1, true>(mant1, gid, w[NCH - 1]);
     if (status && nonfinite) atomicOr(status, 1u);
   }
   if (ADAPT)
@@ -180,7 +180,7 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       uint32_t b[G];
       const float* src = x + (j * G) * C + c;
 #pragma unroll
-      for (int t = 0; t < G; ++t) b[t] = __float_as_uint(src[t * C]);
+      for (int t = 0; t < G; ++t) b[t] = __float_as_uint(stream_load(src + t * C));
       uint32_t w[NCH][WPG];
       uint32_t E, s_lo, s_hi;
       bool nonfinite;
@@ -421,8 +421,8 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
     if constexpr (UPD) {
       const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<float*>(dx + r0 * C), (short)0, (int)(rows * C * 4), 0x00020000);
-      const v4i a = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
-      const v4i d = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rd, off, 0, 0));
+      const v4i a = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, kStreamPolicy));
+      const v4i d = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rd, off, 0, kStreamPolicy));
       float4 v;
       {
         // Two roundings, never a fused multiply-add.
@@ -433,9 +433,13 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
         v.w = __int_as_float(a[3]) + alpha * __int_as_float(d[3]);
       }
       *reinterpret_cast<float4*>(&tile[4 * q]) = v;
-      if (row < rows && c0 + 4 * g < C) *reinterpret_cast<float4*>(x_out + (r0 + row) * C + c0 + 4 * g) = v;
+      if (row < rows && c0 + 4 * g < C) {
+        typedef float f4 __attribute__((ext_vector_type(4)));
+        stream_store(reinterpret_cast<f4*>(x_out + (r0 + row) * C + c0 + 4 * g), f4{v.x, v.y, v.z, v.w});
+      }
     } else {
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)&tile[4 * 64 * (4 * wave + n)], 16, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_void*)&tile[4 * 64 * (4 * wave + n)], 16, off, 0, 0,
+                                               kStreamPolicy);
     }
   }
   if constexpr (!UPD) __builtin_amdgcn_s_waitcnt(0);  // this wave's direct loads have landed
