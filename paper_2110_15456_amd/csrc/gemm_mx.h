@@ -37,11 +37,13 @@
 // the 16-byte fragment reads of 16 rows hit all 64 banks, while each load
 // instruction still reads whole runs of consecutive rows.  Slabs are double
 // buffered in two LDS objects: the loads of slab s+1 are issued right after
-// the barrier that publishes slab s and have all of slab s's MFMAs to land,
-// and slab s+2 is touched in L2 at the same time.  A 256-thread workgroup
-// (2x2 waves) computes a 256x256 tile (128 along an operand with two chunk
-// planes); tiles are ordered so that neighbours share panels in L2 on the
-// same XCD.
+// the barrier that publishes slab s and have all of slab s's MFMAs to land.
+// The direct loads are issue-rate bound (about 31 cycles per instruction per
+// CU from L2, whatever their width), so the kernel issues no load it does not
+// need (an L2 prefetch of slab s+2 cost more than it saved).  A 256-thread
+// workgroup (2x2 waves) computes a 256x256 tile (128 along an operand with two
+// chunk planes); tiles are ordered so that neighbours share panels in L2 on
+// the same XCD.
 #pragma once
 #include "bfp_quant.h"
 
@@ -220,22 +222,6 @@ __device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, rs
   }
 }
 
-// L2 prefetch of one slab of one operand plane, two slabs ahead of use: each
-// row's run of GB-byte groups is touched at its first and last dword (the one
-// or two 128-byte lines it spans) by a direct load into a sink that is never
-// read.  ROWS rows take 2 * ROWS / 256 instructions per wave.
-template <int ROWS, int GB>
-__device__ __forceinline__ void prefetch_plane(uint8_t* lds_sink, rsrc_t rsrc, uint32_t row_bytes, int slab, int tid) {
-  static_assert((2 * ROWS) % mx::NT == 0, "touches split evenly over the threads");
-#pragma unroll
-  for (int u = 0; u < 2 * ROWS / mx::NT; ++u) {
-    const int t = tid + u * mx::NT;
-    const uint32_t off =
-        (uint32_t)(t >> 1) * row_bytes + (uint32_t)slab * (mx::KG * GB) + (uint32_t)(t & 1) * (mx::KG * GB - 4);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)lds_sink, 4, off, 0, 0, 0);
-  }
-}
-
 // MFMA operands of one K-step from the 16-byte slots read for A (x) and B (y).
 // A lane's block is values 0..15 (half 0) and 16..31 (half 1).  An FP6 slot
 // has its group in half 0 (dwords 0-2; dword 3 is the slot's zero dword and
@@ -350,7 +336,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // does not wait for the next slab's loads before computing on this one.
   __shared__ __attribute__((aligned(16))) uint8_t stage0[CF::STAGE];
   __shared__ __attribute__((aligned(16))) uint8_t stage1[CF::STAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t pf_sink[4 * 256];  // prefetch destination, never read
+  __shared__ __attribute__((aligned(16))) uint8_t sink[4 * 256];  // destination of padding loads, never read
   constexpr int TM = CF::TM, TN = CF::TN, NA = CF::NA, NB = CF::NB, FA = CF::FA, FB = CF::FB;
   const int tid = threadIdx.x;
   int tm, tn;
@@ -425,7 +411,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // a whole step is one basic block and the MFMAs cannot be moved past the
   // next step's barrier.
   const rsrc_t rnull = make_rsrc(a_exp, 0u);
-  auto issue = [&](uint8_t* stage, int slab, bool live, bool pf_live, uint2 (&e)[CF::EXP_ROWS_PER_T]) {
+  auto issue = [&](uint8_t* stage, int slab, bool live, uint2 (&e)[CF::EXP_ROWS_PER_T]) {
     if constexpr (!EXP_FULL) {
 #pragma unroll
       for (int k = 0; k < CF::EXP_ROWS_PER_T; ++k) {
@@ -458,29 +444,12 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
                                       wave);
     }
     if constexpr (EXP_FULL) {
-      load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, pf_sink + wave * 256, e_lane_off,
+      load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, sink + wave * 256, e_lane_off,
                                     ng_e, slab, wave);
-      load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, pf_sink + wave * 256, e_lane_off,
+      load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, sink + wave * 256, e_lane_off,
                                     ng_e, slab, wave);
-    }
-    // Last: the NPF prefetches of slab + 1, which the next step does not wait for.
-#pragma unroll
-    for (int p = 0; p < NA; ++p) {
-      if (mx::a_fp4<CF>(p))
-        prefetch_plane<CF::BM, 8>(pf_sink + wave * 256, pf_live ? ra[p] : rnull, rb4, slab + 1, tid);
-      else
-        prefetch_plane<CF::BM, 12>(pf_sink + wave * 256, pf_live ? ra[p] : rnull, rb6, slab + 1, tid);
-    }
-#pragma unroll
-    for (int p = 0; p < NB; ++p) {
-      if (mx::b_fp4<CF>(p))
-        prefetch_plane<CF::BN, 8>(pf_sink + wave * 256, pf_live ? rb[p] : rnull, rb4, slab + 1, tid);
-      else
-        prefetch_plane<CF::BN, 12>(pf_sink + wave * 256, pf_live ? rb[p] : rnull, rb6, slab + 1, tid);
     }
   };
-  constexpr int NPF = NA * 2 * CF::BM / mx::NT + NB * 2 * CF::BN / mx::NT;
-  static_assert(NPF < 16, "prefetches fit the vmcnt field of s_waitcnt");
   // Branch-free, so that it stays behind the MFMAs in one basic block: rows
   // past BM + BN write to a spare 8 bytes after the exponents.
   auto put_exps = [&](uint8_t* stage, const uint2 (&e)[CF::EXP_ROWS_PER_T]) {
@@ -499,7 +468,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 
   uint2 e_regs[CF::EXP_ROWS_PER_T];
   if (nslabs > 0) {
-    issue(stage0, 0, true, nslabs > 1, e_regs);
+    issue(stage0, 0, true, e_regs);
     put_exps(stage0, e_regs);
   }
 
@@ -510,19 +479,15 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   auto step = [&](const uint8_t* cur, uint8_t* nxt, int s) {
     // Every wave's direct loads into cur must have landed before any wave
     // passes the barrier (the compiler only orders them against this wave's
-    // own LDS reads): wait for them explicitly.  Loads complete in order, so
-    // vmcnt = NPF leaves only the last step's prefetches in flight
-    // (s_waitcnt immediate: vmcnt in bits 3:0, expcnt and lgkmcnt zero).
-    __builtin_amdgcn_s_waitcnt(NPF);
-    // No fence (a release fence would also wait for the prefetches, which
-    // write LDS): the empty asm statements keep the compiler from moving
-    // memory accesses across the barrier, the s_waitcnt above orders the
-    // hardware.
+    // own LDS reads): wait for them explicitly (s_waitcnt 0: vmcnt, expcnt
+    // and lgkmcnt zero).  The empty asm statements keep the compiler from
+    // moving memory accesses across the barrier.
+    __builtin_amdgcn_s_waitcnt(0);
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     const bool more = s + 1 < nslabs;
-    issue(nxt, more ? s + 1 : s, more, s + 2 < nslabs, e_regs);
+    issue(nxt, more ? s + 1 : s, more, e_regs);
     __builtin_amdgcn_sched_barrier(0);
     // Fragment addresses.  Row rl = wr*WM + 16*i + lr has the FP6 swizzle
     // ((rl >> 1) & 7) = ((lr >> 1) & 7) and the FP4 swizzle ((rl >> 2) & 3) =
