@@ -514,13 +514,28 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     asm volatile("" ::: "memory");
     const bool more = s + 1 < nslabs;
     const int nslab = more ? s + 1 : s;
-    // With an FP6 operand the loads are issue-rate bound: with the explicit
-    // pipeline they go out in NPART parts, one after each of the first NPART
-    // blocks of MFMAs, so that the wave keeps issuing MFMAs while the load
-    // path works through them (FP6 x FP6: 10-14% faster).  FP4 x FP4 slabs
-    // have half the load instructions, and there issuing them all at once,
-    // here, is faster (their latency, not their issue, is what shows).
-    constexpr int NPART = (CF::PIPE && !(FA && FB)) ? (NLOAD < FASTBFP_MX_SPREAD ? NLOAD : FASTBFP_MX_SPREAD) : 1;
+    // With an FP6 operand the loads are issue-rate bound: they go out in NPART
+    // parts between the blocks of MFMAs, so that the wave keeps issuing MFMAs
+    // while the load path works through them (FP6 x FP6: 10-14% faster, two
+    // chunk planes 1-12%).  FP4 x FP4 slabs have half the load instructions,
+    // and there issuing them all at once, here, is faster (their latency, not
+    // their issue, is what shows).
+    // (The same holds for groups of 32, whose slabs are one K-step: there
+    // spreading was 1-4% slower.)
+    constexpr int NPART = ((NA == 1 && NB == 1 && FA && FB) || CF::G == 32)
+                              ? 1
+                              : (NLOAD < FASTBFP_MX_SPREAD ? NLOAD : FASTBFP_MX_SPREAD);
+    // The parts go after MFMA blocks spread over the first half of the slab's
+    // nblk blocks (part k after block k * (nblk / 2) / NPART), each fenced so
+    // that the compiler keeps it there.
+    auto issue_after = [&](int b, int nblk) {
+#pragma unroll
+      for (int k = 0; k < NPART; ++k)
+        if (NPART > 1 && k * (nblk / 2) / NPART == b) {
+          issue(nxt, nslab, more, e_regs, k, NPART);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    };
     if constexpr (NPART == 1) issue(nxt, nslab, more, e_regs);
     __builtin_amdgcn_sched_barrier(0);
     // Fragment addresses.  Row rl = wr*WM + 16*i + lr has the FP6 swizzle
@@ -592,7 +607,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
         for (int j = 0; j < TN; ++j)
           mma<FA, FB>(acc[i][j], af[blk & 1], bf[ph & 1][j], ae[blk & 1], be[ph & 1][j]);
-        if (NPART > 1 && blk < NPART) issue(nxt, nslab, more, e_regs, blk, NPART);
+        issue_after(blk, NPH * BPP);
         __builtin_amdgcn_sched_barrier(0);
       }
     } else if constexpr (CF::G == 32) {
@@ -616,6 +631,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
             for (int j = 0; j < TN; ++j)
               mma<fa, fb>(acc[i][j], av, bv[j], ea, eb[j]);
+            issue_after((cb * NA + ca) * TM + i, NB * NA * TM);
           }
         });
       });
@@ -642,6 +658,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
               for (int j = 0; j < TN; ++j)
                 mma<fa, fb>(acc[i][j], av, op_b<fa, fb>(y[j], ks), ea, eb[j]);
+              issue_after(((ks * NB + cb) * NA + ca) * TM + i, 2 * NB * NA * TM);
             }
           });
         });
