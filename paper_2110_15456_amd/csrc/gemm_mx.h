@@ -636,31 +636,37 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
         });
       });
     } else {
-      // Compiler-scheduled: per K-step and B chunk, the B fragments, then each
-      // A fragment against them.
+      // Compiler-scheduled: per K-step, the B fragments of every chunk plane,
+      // then each A fragment (read once, its exponent byte once) against
+      // them.  A block is one A fragment's MFMAs; the load parts go between
+      // blocks.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
+        u32x4 y[NB][TN];
+        int eb[NB][TN];
         static_for<NB>([&](auto cbc) {
           constexpr int cb = decltype(cbc)::value, fb = mx::b_fp4<CF>(cb);
-          u32x4 y[TN];
-          int eb[TN];
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
-            y[j] = rd(slot_addr(mx::b_plane<CF>(cb), fb, b_r, j, ks));
-            eb[j] = (int)cur[eb_lane + j * 16 * CF::EK + ks] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
+            y[cb][j] = rd(slot_addr(mx::b_plane<CF>(cb), fb, b_r, j, ks));
+            // +4 per chunk of significance
+            eb[cb][j] = (int)cur[eb_lane + j * 16 * CF::EK + ks] + 4 * (NB - 1 - cb);
           }
-          static_for<NA>([&](auto cac) {
-            constexpr int ca = decltype(cac)::value, fa = mx::a_fp4<CF>(ca);
+        });
+        static_for<NA>([&](auto cac) {
+          constexpr int ca = decltype(cac)::value, fa = mx::a_fp4<CF>(ca);
 #pragma unroll
-            for (int i = 0; i < TM; ++i) {
-              const v8i av = op_a<fa, fb>(rd(slot_addr(mx::a_plane<CF>(ca), fa, a_r, i, ks)), ks);
-              const int ea = (int)cur[ea_lane + i * 16 * CF::EK + ks] + 4 * (NA - 1 - ca);
+          for (int i = 0; i < TM; ++i) {
+            const u32x4 x = rd(slot_addr(mx::a_plane<CF>(ca), fa, a_r, i, ks));
+            const int ea = (int)cur[ea_lane + i * 16 * CF::EK + ks] + 4 * (NA - 1 - ca);
+            static_for<NB>([&](auto cbc) {
+              constexpr int cb = decltype(cbc)::value, fb = mx::b_fp4<CF>(cb);
+              const v8i av = op_a<fa, fb>(x, ks);
 #pragma unroll
-              for (int j = 0; j < TN; ++j)
-                mma<fa, fb>(acc[i][j], av, op_b<fa, fb>(y[j], ks), ea, eb[j]);
-              issue_after(((ks * NB + cb) * NA + ca) * TM + i, 2 * NB * NA * TM);
-            }
-          });
+              for (int j = 0; j < TN; ++j) mma<fa, fb>(acc[i][j], av, op_b<fa, fb>(y[cb][j], ks), ea, eb[cb][j]);
+            });
+            issue_after((ks * NA + ca) * TM + i, 2 * NA * TM);
+          }
         });
       }
     }
