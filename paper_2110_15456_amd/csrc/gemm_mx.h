@@ -35,7 +35,9 @@
 // of K-step ks works on group 2 lb + ks, so an FP4 lane reads one slot for
 // both K-steps.  Slot order within a row is XOR-swizzled by the row so that
 // the 16-byte fragment reads of 16 rows hit all 64 banks, while each load
-// instruction still reads whole runs of consecutive rows.  Slabs are double
+// instruction still reads whole runs of consecutive rows.  With full slabs of
+// groups of 16, the exponents of two slabs come in one 16-byte load per row
+// into a buffer of their own.  Slabs are double
 // buffered in two LDS objects: the loads of slab s+1 are issued right after
 // the barrier that publishes slab s and have all of slab s's MFMAs to land.
 // The direct loads are issue-rate bound (about 31 cycles per instruction per
@@ -234,6 +236,26 @@ __device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, rs
   }
 }
 
+// Direct loads of the exponents of one slab pair (EK = 8 bytes for each of
+// two slabs: 16 contiguous bytes per row) for ROWS rows, one row per lane:
+// row r lands at lds_x + 16 r.  lane_off is lane * ng.  When the instructions
+// do not split evenly over the four waves, the extra waves repeat the last one
+// (the same bytes to the same place).
+template <int ROWS>
+constexpr int pair_loads() { return (ROWS / 64 + 3) / 4; }  // per wave
+template <int ROWS>
+__device__ __forceinline__ void load_exps_pair(uint8_t* lds_x, rsrc_t rsrc, uint32_t lane_off, int ng, int pair,
+                                               int wave, int u0, int u1) {
+  constexpr int INSTR = ROWS / 64;
+#pragma unroll
+  for (int u = 0; u < (INSTR + 3) / 4; ++u) {
+    if (u < u0 || u >= u1) continue;
+    const int blk = min(wave + 4 * u, INSTR - 1);
+    const uint32_t off = lane_off + (uint32_t)blk * 64u * (uint32_t)ng + (uint32_t)pair * 16u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_x + blk * 1024), 16, off, 0, 0, 0);
+  }
+}
+
 // MFMA operands of one K-step from the 16-byte slots read for A (x) and B (y).
 // A lane's block is values 0..15 (half 0) and 16..31 (half 1).  An FP6 slot
 // has its group in half 0 (dwords 0-2; dword 3 is the slot's zero dword and
@@ -343,13 +365,26 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
                                                  const uint8_t* __restrict__ b_exp, int64_t b_plane_stride, int M,
                                                  int N, int ng, float scale, float* __restrict__ C, int64_t ldc,
                                                  int tiles_m, int tiles_n, OutBFP qo) {
-  // Two stages as two LDS objects: the compiler then knows that the direct
-  // loads into one stage do not alias the fragment reads of the other, and
-  // does not wait for the next slab's loads before computing on this one.
-  __shared__ __attribute__((aligned(16))) uint8_t stage0[CF::STAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t stage1[CF::STAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t sink[4 * 256];  // destination of padding loads, never read
   constexpr int TM = CF::TM, TN = CF::TN, NA = CF::NA, NB = CF::NB, FA = CF::FA, FB = CF::FB;
+  // Groups of 16 with full slabs (XP): the exponents of slab pair p (slabs 2p
+  // and 2p + 1: 16 contiguous bytes per row) come in one 16-byte load per row,
+  // with slab 2p's mantissas, into their own buffer xe[p % 2] -- a quarter of
+  // the load instructions of per-slab dword loads (the loads are issue-rate
+  // bound).  The stages then hold only mantissas (and the converted output's
+  // strips).  Otherwise each stage holds its slab's exponents.
+  constexpr bool XP = EXP_FULL && CF::G == 16;
+  constexpr int STRIP_BYTES = QNCH ? 4 * 16 * (CF::WN + 4) * 4 : 0;
+  constexpr int SB = XP ? (CF::OFF_EA > STRIP_BYTES ? CF::OFF_EA : STRIP_BYTES) : CF::STAGE;
+  constexpr int XEB = XP ? (CF::BM + CF::BN) * 16 : 16;
+  // Two stages (and two exponent buffers) as separate LDS objects: the
+  // compiler then knows that the direct loads into one do not alias the
+  // fragment reads of the other, and does not wait for the next slab's loads
+  // before computing on this one.
+  __shared__ __attribute__((aligned(16))) uint8_t stage0[SB];
+  __shared__ __attribute__((aligned(16))) uint8_t stage1[SB];
+  __shared__ __attribute__((aligned(16))) uint8_t xe0[XEB];
+  __shared__ __attribute__((aligned(16))) uint8_t xe1[XEB];
+  __shared__ __attribute__((aligned(16))) uint8_t sink[4 * 256];  // destination of padding loads, never read
   const int tid = threadIdx.x;
   int tm, tn;
   tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
@@ -360,7 +395,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 
   // Zero both stages once: the slot dwords that the 12-byte loads never write
   // are the zero padding of the FP6 operands.
-  for (int i = tid; i < CF::STAGE / 16; i += mx::NT) {
+  for (int i = tid; i < SB / 16; i += mx::NT) {
     reinterpret_cast<u32x4*>(stage0)[i] = u32x4{0u, 0u, 0u, 0u};
     reinterpret_cast<u32x4*>(stage1)[i] = u32x4{0u, 0u, 0u, 0u};
   }
@@ -412,6 +447,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   const rsrc_t reb = make_rsrc(b_exp + (int64_t)col0 * ng_e, (uint32_t)(b_rows * ng_e));
   constexpr int DPR = CF::EK / 4;
   const uint32_t e_lane_off = (uint32_t)(lane / DPR) * (uint32_t)ng_e + (uint32_t)(lane % DPR) * 4u;
+  const uint32_t x_lane_off = (uint32_t)lane * (uint32_t)ng_e;
 
   // Exponents: with full slabs, direct loads like the mantissas.  Otherwise
   // through registers (zeros are needed past K): this thread handles rows
@@ -427,12 +463,15 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // planes, then the exponents of A and B); part `part` of `nparts` issues the
   // instructions [part * NLOAD / nparts, (part + 1) * NLOAD / nparts) of that
   // order (the register exponent loads of the ragged path go with part 0).
+  // XP: the exponent loads are those of a slab pair, issued only where xe
+  // (their destination) is given.
   constexpr int LA0 = plane_loads<CF::BM>(mx::a_fp4<CF>(0)), LA1 = NA == 2 ? plane_loads<CF::BM>(false) : 0;
   constexpr int LB0 = plane_loads<CF::BN>(mx::b_fp4<CF>(0)), LB1 = NB == 2 ? plane_loads<CF::BN>(false) : 0;
-  constexpr int LEA = EXP_FULL ? exps_loads<CF::BM, CF::EK>() : 0, LEB = EXP_FULL ? exps_loads<CF::BN, CF::EK>() : 0;
+  constexpr int LEA = XP ? pair_loads<CF::BM>() : EXP_FULL ? exps_loads<CF::BM, CF::EK>() : 0;
+  constexpr int LEB = XP ? pair_loads<CF::BN>() : EXP_FULL ? exps_loads<CF::BN, CF::EK>() : 0;
   constexpr int OFS[6] = {0, LA0, LA0 + LA1, LA0 + LA1 + LB0, LA0 + LA1 + LB0 + LB1, LA0 + LA1 + LB0 + LB1 + LEA};
   constexpr int NLOAD = OFS[5] + LEB;
-  auto issue = [&](uint8_t* stage, int slab, bool live, uint2 (&e)[CF::EXP_ROWS_PER_T], int part = 0,
+  auto issue = [&](uint8_t* stage, int slab, bool live, uint2 (&e)[CF::EXP_ROWS_PER_T], uint8_t* xe, int part = 0,
                    int nparts = 1) {
     const int lo = part * NLOAD / nparts, hi = (part + 1) * NLOAD / nparts;
     // the range of loader q's own instructions that falls in [lo, hi)
@@ -469,7 +508,12 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
         load_plane<CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m_lane_off, rb6, slab, g_ok,
                                       wave, u0(2 + p), u1(2 + p));
     }
-    if constexpr (EXP_FULL) {
+    if constexpr (XP) {
+      if (xe) {
+        load_exps_pair<CF::BM>(xe, live ? rea : rnull, x_lane_off, ng_e, slab / 2, wave, u0(4), u1(4));
+        load_exps_pair<CF::BN>(xe + CF::BM * 16, live ? reb : rnull, x_lane_off, ng_e, slab / 2, wave, u0(5), u1(5));
+      }
+    } else if constexpr (EXP_FULL) {
       load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, sink + wave * 256, e_lane_off,
                                     ng_e, slab, wave, u0(4), u1(4));
       load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, sink + wave * 256, e_lane_off,
@@ -494,7 +538,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 
   uint2 e_regs[CF::EXP_ROWS_PER_T];
   if (nslabs > 0) {
-    issue(stage0, 0, true, e_regs);
+    issue(stage0, 0, true, e_regs, XP ? xe0 : nullptr);
     put_exps(stage0, e_regs);
   }
 
@@ -502,7 +546,10 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // every wave), start the loads of slab s + 1 into the other stage (which
   // held slab s - 1, finished by every wave), compute slab s, then write the
   // next slab's exponents.
-  auto step = [&](const uint8_t* cur, uint8_t* nxt, int s) {
+  // XP: xcur is the exponent buffer of slab s's pair, xnext (or null) the one
+  // that receives the next pair with slab s + 1, half = s & 1.  Otherwise the
+  // exponents are in cur.
+  auto step = [&](const uint8_t* cur, uint8_t* nxt, int s, const uint8_t* xcur, uint8_t* xnext, int half) {
     // Every wave's direct loads into cur must have landed before any wave
     // passes the barrier (the compiler only orders them against this wave's
     // own LDS reads): wait for them explicitly (s_waitcnt 0: vmcnt, expcnt
@@ -532,11 +579,11 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
       for (int k = 0; k < NPART; ++k)
         if (NPART > 1 && k * (nblk / 2) / NPART == b) {
-          issue(nxt, nslab, more, e_regs, k, NPART);
+          issue(nxt, nslab, more, e_regs, xnext, k, NPART);
           __builtin_amdgcn_sched_barrier(0);
         }
     };
-    if constexpr (NPART == 1) issue(nxt, nslab, more, e_regs);
+    if constexpr (NPART == 1) issue(nxt, nslab, more, e_regs, xnext);
     __builtin_amdgcn_sched_barrier(0);
     // Fragment addresses.  Row rl = wr*WM + 16*i + lr has the FP6 swizzle
     // ((rl >> 1) & 7) = ((lr >> 1) & 7) and the FP4 swizzle ((rl >> 2) & 3) =
@@ -550,8 +597,10 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     const int a_r = wr * CF::WM + lr, b_r = wc * CF::WN + lr;
     // the exponent of lane block lb's group in K-step ks: group 2 lb + ks
     // (G = 16) or lb (G = 32, one K-step)
-    const int ea_lane = CF::OFF_EA + a_r * CF::EK + (CF::G == 16 ? 2 * lb : lb);
-    const int eb_lane = CF::OFF_EB + b_r * CF::EK + (CF::G == 16 ? 2 * lb : lb);
+    // (XP: rows of 16 bytes in the pair buffer, this slab's 8 at half * 8.)
+    constexpr int ER = XP ? 16 : CF::EK;  // exponent bytes per row
+    const int ea_lane = (XP ? 0 : CF::OFF_EA) + a_r * ER + (XP ? 8 * half : 0) + (CF::G == 16 ? 2 * lb : lb);
+    const int eb_lane = (XP ? 16 * CF::BM : CF::OFF_EB) + b_r * ER + (XP ? 8 * half : 0) + (CF::G == 16 ? 2 * lb : lb);
     // Byte offset of the 16-byte slot of row tile t, K-step ks, in a plane of
     // format fp4 starting at plane_off, for a lane of row r.
     auto slot_addr = [&](int plane_off, int fp4, int r, int t, int ks) {
@@ -580,12 +629,12 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
       auto read_b = [&](int ks, int j) {
         bf[ks & 1][j] = CF::G == 16 ? op_b<FA, FB>(rd(slot_addr(CF::OFF_B, FB, b_r, j, ks)), ks)
                                     : op32(FB, CF::OFF_B, b_r, j);
-        be[ks & 1][j] = (int)cur[eb_lane + j * 16 * CF::EK + ks];
+        be[ks & 1][j] = (int)xcur[eb_lane + j * 16 * ER + ks];
       };
       auto read_a = [&](int blk) {
         const int ks = blk / BPP, i = blk % BPP;
         af[blk & 1] = CF::G == 16 ? op_a<FA, FB>(rd(slot_addr(0, FA, a_r, i, ks)), ks) : op32(FA, 0, a_r, i);
-        ae[blk & 1] = (int)cur[ea_lane + i * 16 * CF::EK + ks];
+        ae[blk & 1] = (int)xcur[ea_lane + i * 16 * ER + ks];
       };
 #pragma unroll
       for (int j = 0; j < TN; ++j) read_b(0, j);
@@ -620,14 +669,14 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           bv[j] = op32(fb, mx::b_plane<CF>(cb), b_r, j);
-          eb[j] = (int)cur[eb_lane + j * 16 * CF::EK] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
+          eb[j] = (int)xcur[eb_lane + j * 16 * ER] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
         }
         static_for<NA>([&](auto cac) {
           constexpr int ca = decltype(cac)::value, fa = mx::a_fp4<CF>(ca);
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const v8i av = op32(fa, mx::a_plane<CF>(ca), a_r, i);
-            const int ea = (int)cur[ea_lane + i * 16 * CF::EK] + 4 * (NA - 1 - ca);
+            const int ea = (int)xcur[ea_lane + i * 16 * ER] + 4 * (NA - 1 - ca);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
               mma<fa, fb>(acc[i][j], av, bv[j], ea, eb[j]);
@@ -650,7 +699,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
           for (int j = 0; j < TN; ++j) {
             y[cb][j] = rd(slot_addr(mx::b_plane<CF>(cb), fb, b_r, j, ks));
             // +4 per chunk of significance
-            eb[cb][j] = (int)cur[eb_lane + j * 16 * CF::EK + ks] + 4 * (NB - 1 - cb);
+            eb[cb][j] = (int)xcur[eb_lane + j * 16 * ER + ks] + 4 * (NB - 1 - cb);
           }
         });
         static_for<NA>([&](auto cac) {
@@ -658,7 +707,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
             const u32x4 x = rd(slot_addr(mx::a_plane<CF>(ca), fa, a_r, i, ks));
-            const int ea = (int)cur[ea_lane + i * 16 * CF::EK + ks] + 4 * (NA - 1 - ca);
+            const int ea = (int)xcur[ea_lane + i * 16 * ER + ks] + 4 * (NA - 1 - ca);
             static_for<NB>([&](auto cbc) {
               constexpr int cb = decltype(cbc)::value, fb = mx::b_fp4<CF>(cb);
               const v8i av = op_a<fa, fb>(x, ks);
@@ -674,11 +723,24 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     put_exps(nxt, e_regs);  // stale but harmless after the last slab
   };
   int s = 0;
-  for (; s + 2 <= nslabs; s += 2) {
-    step(stage0, stage1, s);
-    step(stage1, stage0, s + 1);
+  if constexpr (XP) {
+    // Unrolled by four: slab s in stage s % 2, its exponents in xe[(s / 2) % 2].
+    for (; s + 4 <= nslabs; s += 4) {
+      step(stage0, stage1, s, xe0, nullptr, 0);
+      step(stage1, stage0, s + 1, xe0, xe1, 1);
+      step(stage0, stage1, s + 2, xe1, nullptr, 0);
+      step(stage1, stage0, s + 3, xe1, xe0, 1);
+    }
+    if (s < nslabs) step(stage0, stage1, s, xe0, nullptr, 0);
+    if (s + 1 < nslabs) step(stage1, stage0, s + 1, xe0, xe1, 1);
+    if (s + 2 < nslabs) step(stage0, stage1, s + 2, xe1, nullptr, 0);
+  } else {
+    for (; s + 2 <= nslabs; s += 2) {
+      step(stage0, stage1, s, stage0, nullptr, 0);
+      step(stage1, stage0, s + 1, stage1, nullptr, 1);
+    }
+    if (s < nslabs) step(stage0, stage1, s, stage0, nullptr, 0);
   }
-  if (s < nslabs) step(stage0, stage1, s);
   mma_drain(acc);
 
   // Epilogue: lane holds rows 4*lb + r, column lr of each 16x16 tile.
@@ -702,7 +764,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     // the same FP32 values and the same noise addressing (gid = the group's
     // index in the output exponent array) as converting C separately.
     constexpr int SROW = CF::WN + 4;  // strip row stride in floats (padding spreads the banks)
-    static_assert(4 * 16 * SROW * 4 <= CF::STAGE, "four strips fit in one stage");
+    static_assert(4 * 16 * SROW * 4 <= SB, "four strips fit in one stage");
     // Every wave is done with the stages, and no direct load (the last
     // steps' no-op loads included) can still write them.
     __builtin_amdgcn_s_waitcnt(0);
