@@ -600,7 +600,8 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     // (XP: rows of 16 bytes in the pair buffer, this slab's 8 at half * 8.)
     constexpr int ER = XP ? 16 : CF::EK;  // exponent bytes per row
     const int ea_lane = (XP ? 0 : CF::OFF_EA) + a_r * ER + (XP ? 8 * half : 0) + (CF::G == 16 ? 2 * lb : lb);
-    const int eb_lane = (XP ? 16 * CF::BM : CF::OFF_EB) + b_r * ER + (XP ? 8 * half : 0) + (CF::G == 16 ? 2 * lb : lb);
+    const int eb_lane =
+        (XP ? 16 * CF::BM : CF::OFF_EB) + b_r * ER + (XP ? 8 * half : 0) + (CF::G == 16 ? 2 * lb : lb);
     // Byte offset of the 16-byte slot of row tile t, K-step ks, in a plane of
     // format fp4 starting at plane_off, for a lane of row r.
     auto slot_addr = [&](int plane_off, int fp4, int r, int t, int ks) {
@@ -778,15 +779,16 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
       uint32_t w[QNCH][16 * 6 / 32];
       uint32_t E, s_lo, s_hi;
       bool nonfinite;
+      const uint32_t m = (uint32_t)qo.m;
       if (qo.mode == kStochastic)
-        quantize_group<16, kStochastic, QNCH, false, F0, false>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w,
-                                                                E, nonfinite, s_lo, s_hi);
+        quantize_group<16, kStochastic, QNCH, false, F0, false>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+                                                                s_lo, s_hi);
       else if (qo.mode == kNearest)
-        quantize_group<16, kNearest, QNCH, false, F0, false>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E,
-                                                             nonfinite, s_lo, s_hi);
+        quantize_group<16, kNearest, QNCH, false, F0, false>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+                                                             s_lo, s_hi);
       else
-        quantize_group<16, kTruncate, QNCH, false, F0, false>(b, (uint32_t)qo.m, (uint64_t)gid, qo.key0, qo.key1, w, E,
-                                                              nonfinite, s_lo, s_hi);
+        quantize_group<16, kTruncate, QNCH, false, F0, false>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+                                                              s_lo, s_hi);
       qo.exps[gid] = (uint8_t)E;
       store_plane<16, F0>(qo.mant0, gid, w[0]);
       if (QNCH == 2) store_plane<16, false>(qo.mant1, gid, w[QNCH - 1]);
