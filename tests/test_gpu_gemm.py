@@ -89,6 +89,20 @@ def test_ragged_shapes(shape):
         check_gemm(A, B, oa, ob, partials=(M * N * K <= 64 * 64 * 2048))
 
 
+@pytest.mark.parametrize("nslabs", range(1, 10))
+def test_full_slab_counts(nslabs):
+    """K = 128 * nslabs (full slabs: exponents by direct loads, two slabs' per
+    16-byte load, and the slab loop unrolled by four): every slab count mod 4
+    (the loop's tail) for each kernel family, with ragged M and N."""
+    M, N, K = 260, 136, 128 * nslabs
+    xa = synth.draw("normal", (M, K), 700 + nslabs)
+    xb = synth.draw("weights", (N, K), 800 + nslabs)
+    for pa, pb in [(2, 2), (4, 4), (2, 4), (4, 2), (6, 6), (4, 6), (6, 3), (8, 8)]:
+        announce("gemm full slabs %dx%dx%d (%d,%d)" % (M, N, K, pa, pb))
+        A, B, oa, ob = operands(xa, xb, pa, pb)
+        check_gemm(A, B, oa, ob)
+
+
 def test_precision_lowering():
     xa = synth.draw("half_normal", (130, 320), 5)
     xb = synth.draw("grads", (70, 320), 6)
