@@ -64,6 +64,9 @@ namespace mx {
 #ifndef FASTBFP_MX_SPREAD
 #define FASTBFP_MX_SPREAD 8  // parts a slab's loads are spread over (explicit pipeline)
 #endif
+#ifndef FASTBFP_MX_X3
+#define FASTBFP_MX_X3 1  // one MFMA for both cross products of two-chunk operands
+#endif
 #ifndef FASTBFP_MX11_BM
 #define FASTBFP_MX11_BM FASTBFP_MX_BM
 #endif
@@ -307,6 +310,9 @@ typedef int v6i __attribute__((ext_vector_type(6)));
 // reads across it.
 template <int FA, int FB>
 __device__ __forceinline__ void mma(v4f& acc, const v8i& a, const v8i& b, int sa, int sb) {
+  // B's fragment is the instruction's first operand and A's the second, so
+  // the result is the tile of C transposed: a lane's four accumulators are
+  // four consecutive columns of one row of C (see the epilogue).
 #if FASTBFP_MX_TIED
   const v4i a4 = __builtin_shufflevector(a, a, 0, 1, 2, 3);
   const v4i b4 = __builtin_shufflevector(b, b, 0, 1, 2, 3);
@@ -314,19 +320,19 @@ __device__ __forceinline__ void mma(v4f& acc, const v8i& a, const v8i& b, int sa
   const v6i b6 = __builtin_shufflevector(b, b, 0, 1, 2, 3, 4, 5);
   if constexpr (FA && FB)
     asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:4"
-                 : "+a"(acc) : "v"(a4), "v"(b4), "v"(sa), "v"(sb));
+        : "+a"(acc) : "v"(b4), "v"(a4), "v"(sb), "v"(sa));
   else if constexpr (FA)
-    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:2"
-                 : "+a"(acc) : "v"(a4), "v"(b6), "v"(sa), "v"(sb));
-  else if constexpr (FB)
     asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:2 blgp:4"
-                 : "+a"(acc) : "v"(a6), "v"(b4), "v"(sa), "v"(sb));
+        : "+a"(acc) : "v"(b6), "v"(a4), "v"(sb), "v"(sa));
+  else if constexpr (FB)
+    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:2"
+        : "+a"(acc) : "v"(b4), "v"(a6), "v"(sb), "v"(sa));
   else
     asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:2 blgp:2"
-                 : "+a"(acc) : "v"(a6), "v"(b6), "v"(sa), "v"(sb));
+        : "+a"(acc) : "v"(b6), "v"(a6), "v"(sb), "v"(sa));
 #else
-  acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, mfma_fmt<FA>::value, mfma_fmt<FB>::value, 0, sa, 0,
-                                                         sb);
+  acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b, a, acc, mfma_fmt<FB>::value, mfma_fmt<FA>::value, 0, sb, 0,
+                                                         sa);
 #endif
 }
 // Wait states between the last MFMA and any other read of its accumulators
@@ -373,6 +379,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // bound).  The stages then hold only mantissas (and the converted output's
   // strips).  Otherwise each stage holds its slab's exponents.
   constexpr bool XP = EXP_FULL && CF::G == 16;
+  constexpr bool X3 = FASTBFP_MX_X3 && NA == 2 && NB == 2 && CF::G == 16 && !CF::PIPE && !FA && !FB;
   constexpr int STRIP_BYTES = QNCH ? 4 * 16 * (CF::WN + 4) * 4 : 0;
   constexpr int SB = XP ? (CF::OFF_EA > STRIP_BYTES ? CF::OFF_EA : STRIP_BYTES) : CF::STAGE;
   constexpr int XEB = XP ? (CF::BM + CF::BN) * 16 : 16;
@@ -685,6 +692,44 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
           }
         });
       });
+    } else if constexpr (X3) {
+      // Both operands in two chunk planes: the cross products (A's upper
+      // chunk with B's lower, A's lower with B's upper) carry the same weight,
+      // one chunk of significance, and with groups of 16 each fills only half
+      // of a 32-value block, so the two share one MFMA: A's block holds its
+      // upper group then its lower one, B's block its lower then its upper,
+      // both as FP6, and the scales are those of the cross weight.  Three
+      // MFMAs per fragment pair and K-step instead of four.
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        u32x4 y0[TN], y1[TN];
+        int eb[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          y0[j] = rd(slot_addr(mx::b_plane<CF>(0), FB, b_r, j, ks));
+          y1[j] = rd(slot_addr(mx::b_plane<CF>(1), 0, b_r, j, ks));
+          eb[j] = (int)xcur[eb_lane + j * 16 * ER + ks];
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const u32x4 x0 = rd(slot_addr(mx::a_plane<CF>(0), FA, a_r, i, ks));
+          const u32x4 x1 = rd(slot_addr(mx::a_plane<CF>(1), 0, a_r, i, ks));
+          const int ea = (int)xcur[ea_lane + i * 16 * ER + ks];
+          const v8i a0 = op_a<FA, FB>(x0, ks), a1 = op_a<0, 0>(x1, ks);
+#pragma unroll
+          for (int j = 0; j < TN; ++j) mma<FA, FB>(acc[i][j], a0, op_b<FA, FB>(y0[j], ks), ea + 4, eb[j] + 4);
+#pragma unroll
+          for (int j = 0; j < TN; ++j) mma<0, 0>(acc[i][j], a1, op_b<0, 0>(y1[j], ks), ea, eb[j]);
+          const v8i ax = v8i{(int)x0[0], (int)x0[1], (int)x0[2], (int)x1[0], (int)x1[1], (int)x1[2], 0, 0};
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const v8i bx = v8i{(int)y1[j][0], (int)y1[j][1], (int)y1[j][2], (int)y0[j][0], (int)y0[j][1],
+                               (int)y0[j][2], 0, 0};
+            mma<0, 0>(acc[i][j], ax, bx, ea + 4, eb[j]);
+          }
+          issue_after(ks * TM + i, 2 * TM);
+        }
+      }
     } else {
       // Compiler-scheduled: per K-step, the B fragments of every chunk plane,
       // then each A fragment (read once, its exponent byte once) against
@@ -744,22 +789,32 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   }
   mma_drain(acc);
 
-  // Epilogue: lane holds rows 4*lb + r, column lr of each 16x16 tile.
+  // Epilogue: lane holds row lr, columns 4*lb .. 4*lb + 3 of each 16x16
+  // tile (B was the MFMAs' first operand): one 16-byte store per tile where
+  // C's rows are 16-byte aligned and the four columns exist.
   if constexpr (QNCH == 0) {
+    const bool vec = (ldc & 3) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
+      const int row = row0 + wr * CF::WM + i * 16 + lr;
+      if (row >= M) continue;
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        const int col = col0 + wc * CF::WN + j * 16 + lr;
+        const int col = col0 + wc * CF::WN + j * 16 + 4 * lb;
+        float* p = C + (int64_t)row * ldc + col;
+        if (vec && col + 3 < N) {
+          *reinterpret_cast<float4*>(p) =
+              make_float4(acc[i][j][0] * scale, acc[i][j][1] * scale, acc[i][j][2] * scale, acc[i][j][3] * scale);
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = row0 + wr * CF::WM + i * 16 + lb * 4 + r;
-          if (row < M && col < N) C[(int64_t)row * ldc + col] = acc[i][j][r] * scale;
+          for (int r = 0; r < 4; ++r)
+            if (col + r < N) p[r] = acc[i][j][r] * scale;
         }
       }
+    }
   } else {
     // Converted output.  A row group of C (16 consecutive columns) is spread
-    // over the 16 lanes of one lane block, so each wave stages one 16-row
+    // over the four lane blocks, so each wave stages one 16-row
     // strip of its tile at a time in LDS (the stage memory, free now), and
     // then every lane converts whole groups with the quantizer's converter:
     // the same FP32 values and the same noise addressing (gid = the group's
@@ -801,8 +856,8 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) strip[(lb * 4 + r) * SROW + j * 16 + lr] = acc[i][j][r] * scale;
+        *reinterpret_cast<float4*>(&strip[lr * SROW + j * 16 + 4 * lb]) =
+            make_float4(acc[i][j][0] * scale, acc[i][j][1] * scale, acc[i][j][2] * scale, acc[i][j][3] * scale);
       __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's strip writes are done
       __builtin_amdgcn_wave_barrier();
       for (int gi = lane; gi < 16 * TN; gi += 64) {
