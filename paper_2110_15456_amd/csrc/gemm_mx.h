@@ -67,6 +67,9 @@ namespace mx {
 #ifndef FASTBFP_MX_X3
 #define FASTBFP_MX_X3 1  // one MFMA for both cross products of two-chunk operands
 #endif
+#ifndef FASTBFP_MX_GM
+#define FASTBFP_MX_GM (CF::BM > CF::BN ? 4 : 8)
+#endif
 #ifndef FASTBFP_MX11_BM
 #define FASTBFP_MX11_BM FASTBFP_MX_BM
 #endif
@@ -131,9 +134,11 @@ __device__ __forceinline__ void static_for(F&& f) {
 // Workgroup id -> (tile_m, tile_n).  Dispatch places consecutive workgroup ids
 // on consecutive XCDs; the remap gives each XCD a contiguous run of logical
 // tiles, and logical tiles are walked in column-major groups of GROUP_M tile
-// rows so that concurrently running workgroups share A and B panels in L2.
+// rows so that concurrently running workgroups share A and B panels in L2:
+// the 32 workgroups an XCD runs at once cover GROUP_M x (32 / GROUP_M) tiles.
+template <int GROUP_M>
 __device__ __forceinline__ void tile_of(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
-  constexpr int NXCD = 8, GROUP_M = 8;
+  constexpr int NXCD = 8;
   int lid = bid;
   if (nblocks % NXCD == 0) lid = (bid % NXCD) * (nblocks / NXCD) + bid / NXCD;
   const int per_group = GROUP_M * tiles_n;
@@ -394,7 +399,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   __shared__ __attribute__((aligned(16))) uint8_t sink[4 * 256];  // destination of padding loads, never read
   const int tid = threadIdx.x;
   int tm, tn;
-  tile_of(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+  tile_of<FASTBFP_MX_GM>(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int row0 = tm * CF::BM, col0 = tn * CF::BN;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index in an SGPR
   const int wr = wave / mx::WGN, wc = wave % mx::WGN;
