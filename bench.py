@@ -41,6 +41,14 @@ def planes(m):
     return 1 if m <= 4 else 2
 
 
+def mfma_passes(pa, pb, g=G):
+    """MFMAs the GEMM issues per K-step and fragment pair: one per pair of
+    chunk planes, except that with groups of 16 two FP6 upper planes (m >= 7
+    on both sides) share one MFMA between the two cross products."""
+    n = planes(pa) * planes(pb)
+    return n - 1 if g == 16 and pa >= 7 and pb >= 7 else n
+
+
 def code_bits(m):
     """Mantissa bits per value: 4-bit codes for a chunk of at most 2 bits, 6-bit
     codes otherwise (plane 0 of m = 1, 2, 5, 6 is the 4-bit one)."""
@@ -67,6 +75,10 @@ def parse():
     p.add_argument("--no-sweeps", action="store_true", help="skip the GEMM and quantize sweeps")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--quiet", action="store_true")
+    p.add_argument("--gemm-only", action="store_true",
+                   help="run only the GEMM sweep and print its JSON (no step, no bench line)")
+    p.add_argument("--gemm-pairs", choices=("default", "all"), default="default",
+                   help="GEMM sweep: six pairs on four shapes, or all 16 operand-format pairs on ffn_up")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 256 MiB device copy (torch) whose profiler counters calibrate HBM bytes")
     return p.parse_args()
@@ -144,6 +156,11 @@ def gemm_sweep(torch, fb, synth, dev, args):
     shapes = {"qkv": (8192, 12288, 4096), "out_proj": (8192, 4096, 4096), "ffn_up": (8192, 16384, 4096),
               "ffn_down": (8192, 4096, 16384)}
     pairs = [(2, 2), (2, 4), (4, 4), (4, 6), (6, 8), (8, 8)]
+    if args.gemm_pairs == "all":
+        # one pair per kernel variant (the four operand formats on each side:
+        # m = 2 FP4, 4 FP6, 6 FP4 + FP6, 8 FP6 + FP6) on the FFN up-projection
+        shapes = {"ffn_up": shapes["ffn_up"]}
+        pairs = [(pa, pb) for pa in (2, 4, 6, 8) for pb in (2, 4, 6, 8)]
     X = torch.from_numpy(synth.bf16_round(synth.draw("normal", (8192, 16384), 41))).to(dev)
     Wt = torch.from_numpy(synth.bf16_round(synth.draw("weights", (16384, 16384), 42))).to(dev)
     out = {}
@@ -165,13 +182,16 @@ def gemm_sweep(torch, fb, synth, dev, args):
             torch.cuda.synchronize()
             ms = a.elapsed_time(z) / reps
             tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
-            issued = tops * planes(pa) * planes(pb) * 2  # zero-padded half blocks, chunk passes
+            issued = tops * mfma_passes(pa, pb) * 2  # zero-padded half blocks, chunk passes
             out["%s(%d,%d)" % (name, pa, pb)] = {
                 "M": M, "N": N, "K": K, "ms": round(ms, 4), "eff_tops": round(tops, 1),
                 "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4),
                 "mfma_issued_tflops": round(issued, 1), "frac_fp6_peak_issued": round(issued / PEAK_FP6_TFLOPS, 4)}
             log(args, "gemm %s (%d,%d): %.3f ms, %.0f eff TOPS" % (name, pa, pb, ms, tops))
         del C
+    if args.gemm_pairs == "all":
+        del X, Wt
+        return out
     # groups of 32 (the sensitivity study's other group size): one whole group
     # per MFMA block, no zero padding
     M, N, K = shapes["ffn_up"]
@@ -189,7 +209,7 @@ def gemm_sweep(torch, fb, synth, dev, args):
         torch.cuda.synchronize()
         ms = a.elapsed_time(z) / 5
         tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
-        issued = tops * planes(pa) * planes(pb)  # chunk passes, no padding
+        issued = tops * mfma_passes(pa, pb, 32)  # chunk passes, no padding
         out["ffn_up_g32(%d,%d)" % (pa, pb)] = {
             "M": M, "N": N, "K": K, "g": 32, "ms": round(ms, 4), "eff_tops": round(tops, 1),
             "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4), "mfma_issued_tflops": round(issued, 1),
@@ -360,6 +380,9 @@ def main():
         sys.exit(2)
     fb._lib.load()  # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
+    if args.gemm_only:
+        print(json.dumps({"gemm_sweep": gemm_sweep(torch, fb, synth, dev, args)}), flush=True)
+        return
     step = Step(torch, fb, synth, dev)
     log(args, "inputs generated in %.1f s" % step.gen_s)
     for s in range(args.warmup):
@@ -414,7 +437,7 @@ def main():
     d = kernels[dom]
     if dom.startswith("gemm"):
         mdom = int(dom.split("_m")[1])
-        issue = planes(mdom) * planes(mdom) * (2 if G == 16 else 1)  # chunk passes x zero-padded half blocks
+        issue = mfma_passes(mdom, mdom) * (2 if G == 16 else 1)  # chunk passes x zero-padded half blocks
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_FP6_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(d["achieved"] / PEAK_FP6_TFLOPS, 4), "traffic": measured_traffic(dom),
                 "work_per_launch": "2*M*N*K = %.4g FLOP (BFP MACs, algorithmic)" % GEMM_OPS,
