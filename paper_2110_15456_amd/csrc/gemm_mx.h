@@ -67,6 +67,9 @@ namespace mx {
 #ifndef FASTBFP_MX_X3
 #define FASTBFP_MX_X3 1  // one MFMA for both cross products of two-chunk operands
 #endif
+#ifndef FASTBFP_MX_PROD
+#define FASTBFP_MX_PROD 1  // a fifth wave issues the direct loads of the two-chunk kernels
+#endif
 #ifndef FASTBFP_MX_GM
 #define FASTBFP_MX_GM (CF::BM > CF::BN ? 4 : 8)
 #endif
@@ -118,6 +121,19 @@ template <class CF> __device__ constexpr int a_plane(int p) { return p ? CF::OFF
 template <class CF> __device__ constexpr int b_plane(int p) { return p ? CF::OFF_B1 : CF::OFF_B; }
 template <class CF> __device__ constexpr int a_fp4(int p) { return p == 0 && CF::FA; }
 template <class CF> __device__ constexpr int b_fp4(int p) { return p == 0 && CF::FB; }
+// Load-issuing wave: with both operands in an FP4 and an FP6 chunk plane
+// (256x128 tiles, at most 256 registers per wave, so a fifth wave fits beside
+// the four MFMA waves), full slabs of groups of 16 and FP32 output, one extra
+// wave issues every direct load and the four MFMA waves issue none.  (The
+// kernels with fewer MFMAs per load -- one chunk plane on a side, or FP6
+// upper planes with 128x128 tiles -- were 5-12% slower this way: one wave
+// issuing all of a slab's loads then sets the pace.)
+template <class CF, bool EXP_FULL, int QNCH>
+constexpr bool producer() {
+  return FASTBFP_MX_PROD && EXP_FULL && CF::G == 16 && QNCH == 0 && CF::NA == 2 && CF::NB == 2 && CF::FA && CF::FB;
+}
+template <class CF, bool EXP_FULL, int QNCH>
+constexpr int threads() { return producer<CF, EXP_FULL, QNCH>() ? NT + 64 : NT; }
 }  // namespace mx
 
 // Calls f(ic<0>{}), ..., f(ic<N-1>{}): a loop whose index is a constant
@@ -371,7 +387,7 @@ struct OutBFP {
 };
 
 template <class CF, bool EXP_FULL, int QNCH>
-__global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
+__global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
                                                  int64_t a_plane_stride, const uint8_t* __restrict__ b_mant,
                                                  const uint8_t* __restrict__ b_exp, int64_t b_plane_stride, int M,
                                                  int N, int ng, float scale, float* __restrict__ C, int64_t ldc,
@@ -385,6 +401,8 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   // strips).  Otherwise each stage holds its slab's exponents.
   constexpr bool XP = EXP_FULL && CF::G == 16;
   constexpr bool X3 = FASTBFP_MX_X3 && NA == 2 && NB == 2 && CF::G == 16 && !CF::PIPE && !FA && !FB;
+  constexpr bool PROD = mx::producer<CF, EXP_FULL, QNCH>();
+  constexpr int NTHR = mx::threads<CF, EXP_FULL, QNCH>();
   constexpr int STRIP_BYTES = QNCH ? 4 * 16 * (CF::WN + 4) * 4 : 0;
   constexpr int SB = XP ? (CF::OFF_EA > STRIP_BYTES ? CF::OFF_EA : STRIP_BYTES) : CF::STAGE;
   constexpr int XEB = XP ? (CF::BM + CF::BN) * 16 : 16;
@@ -407,7 +425,7 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
 
   // Zero both stages once: the slot dwords that the 12-byte loads never write
   // are the zero padding of the FP6 operands.
-  for (int i = tid; i < SB / 16; i += mx::NT) {
+  for (int i = tid; i < SB / 16; i += NTHR) {
     reinterpret_cast<u32x4*>(stage0)[i] = u32x4{0u, 0u, 0u, 0u};
     reinterpret_cast<u32x4*>(stage1)[i] = u32x4{0u, 0u, 0u, 0u};
   }
@@ -447,8 +465,6 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   }
   // FP6: lane -> (row lane / 8 of the instruction's 8, slot lane % 8), loading
   // the group that the row's swizzle puts in that slot.
-  const int g_lane = (lane & 7) ^ ((4 * (wave & 1) + (lane >> 4)) & 7);
-  const uint32_t m_lane_off = (uint32_t)(lane >> 3) * rb6 + (uint32_t)g_lane * 12u;
   // FP4: lane -> (row lane / 4 of the instruction's 16, slot lane % 4), the
   // slot of row r holding pair slot ^ ((r >> 2) & 3).
   const int p_lane = (lane & 3) ^ ((lane >> 4) & 3);
@@ -483,8 +499,13 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   constexpr int LEB = XP ? pair_loads<CF::BN>() : EXP_FULL ? exps_loads<CF::BN, CF::EK>() : 0;
   constexpr int OFS[6] = {0, LA0, LA0 + LA1, LA0 + LA1 + LB0, LA0 + LA1 + LB0 + LB1, LA0 + LA1 + LB0 + LB1 + LEA};
   constexpr int NLOAD = OFS[5] + LEB;
+  // vw: the wave whose share of the instructions is issued (the calling wave,
+  // or each of the four in turn for the load-issuing wave).
   auto issue = [&](uint8_t* stage, int slab, bool live, uint2 (&e)[CF::EXP_ROWS_PER_T], uint8_t* xe, int part = 0,
-                   int nparts = 1) {
+                   int nparts = 1, int vw = -1) {
+    if (vw < 0) vw = wave;
+    const int g_lane = (lane & 7) ^ ((4 * (vw & 1) + (lane >> 4)) & 7);
+    const uint32_t m_lane_off = (uint32_t)(lane >> 3) * rb6 + (uint32_t)g_lane * 12u;
     const int lo = part * NLOAD / nparts, hi = (part + 1) * NLOAD / nparts;
     // the range of loader q's own instructions that falls in [lo, hi)
     auto u0 = [&](int q) { return lo > OFS[q] ? lo - OFS[q] : 0; };
@@ -506,30 +527,30 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     for (int p = 0; p < NA; ++p) {
       if (mx::a_fp4<CF>(p))
         load_plane4<CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m4_lane_off, rb4, slab, p_ok,
-                                       wave, u0(p), u1(p));
+                                       vw, u0(p), u1(p));
       else
         load_plane<CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m_lane_off, rb6, slab, g_ok,
-                                      wave, u0(p), u1(p));
+                                      vw, u0(p), u1(p));
     }
 #pragma unroll
     for (int p = 0; p < NB; ++p) {
       if (mx::b_fp4<CF>(p))
         load_plane4<CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m4_lane_off, rb4, slab, p_ok,
-                                       wave, u0(2 + p), u1(2 + p));
+                                       vw, u0(2 + p), u1(2 + p));
       else
         load_plane<CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m_lane_off, rb6, slab, g_ok,
-                                      wave, u0(2 + p), u1(2 + p));
+                                      vw, u0(2 + p), u1(2 + p));
     }
     if constexpr (XP) {
       if (xe) {
-        load_exps_pair<CF::BM>(xe, live ? rea : rnull, x_lane_off, ng_e, slab / 2, wave, u0(4), u1(4));
-        load_exps_pair<CF::BN>(xe + CF::BM * 16, live ? reb : rnull, x_lane_off, ng_e, slab / 2, wave, u0(5), u1(5));
+        load_exps_pair<CF::BM>(xe, live ? rea : rnull, x_lane_off, ng_e, slab / 2, vw, u0(4), u1(4));
+        load_exps_pair<CF::BN>(xe + CF::BM * 16, live ? reb : rnull, x_lane_off, ng_e, slab / 2, vw, u0(5), u1(5));
       }
     } else if constexpr (EXP_FULL) {
-      load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, sink + wave * 256, e_lane_off,
-                                    ng_e, slab, wave, u0(4), u1(4));
-      load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, sink + wave * 256, e_lane_off,
-                                    ng_e, slab, wave, u0(5), u1(5));
+      load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, sink + vw * 256, e_lane_off,
+                                    ng_e, slab, vw, u0(4), u1(4));
+      load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, sink + vw * 256, e_lane_off,
+                                    ng_e, slab, vw, u0(5), u1(5));
     }
   };
   // Branch-free, so that it stays behind the MFMAs in one basic block: rows
@@ -549,7 +570,30 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
   };
 
   uint2 e_regs[CF::EXP_ROWS_PER_T];
-  if (nslabs > 0) {
+  if constexpr (PROD) {
+    if (wave == mx::WGM * mx::WGN) {
+      // The load-issuing wave: slab 0, then after the barrier that publishes
+      // slab s the loads of slab s + 1 into the other stage (every MFMA wave
+      // has passed that barrier, so is done with slab s - 1 there), and the
+      // exponents of a slab pair with its even slab into xe[pair % 2] (which
+      // held pair - 2).  It passes the same barriers as the MFMA waves (one
+      // per slab), each after waiting for all of its loads.
+      auto issue_all = [&](uint8_t* stage, int slab, uint8_t* xe) {
+#pragma unroll
+        for (int v = 0; v < mx::WGM * mx::WGN; ++v) issue(stage, slab, true, e_regs, xe, 0, 1, v);
+      };
+      if (nslabs > 0) issue_all(stage0, 0, xe0);
+      for (int s = 0; s < nslabs; ++s) {
+        __builtin_amdgcn_s_waitcnt(0);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        const int t = s + 1;
+        if (t < nslabs) issue_all((t & 1) ? stage1 : stage0, t, (t & 1) ? nullptr : ((t >> 1) & 1) ? xe1 : xe0);
+      }
+      return;
+    }
+  } else if (nslabs > 0) {
     issue(stage0, 0, true, e_regs, XP ? xe0 : nullptr);
     put_exps(stage0, e_regs);
   }
@@ -590,12 +634,12 @@ __global__ __launch_bounds__(256) void k_gemm_mx(const uint8_t* __restrict__ a_m
     auto issue_after = [&](int b, int nblk) {
 #pragma unroll
       for (int k = 0; k < NPART; ++k)
-        if (NPART > 1 && k * (nblk / 2) / NPART == b) {
+        if (!PROD && NPART > 1 && k * (nblk / 2) / NPART == b) {
           issue(nxt, nslab, more, e_regs, xnext, k, NPART);
           __builtin_amdgcn_sched_barrier(0);
         }
     };
-    if constexpr (NPART == 1) issue(nxt, nslab, more, e_regs, xnext);
+    if constexpr (NPART == 1 && !PROD) issue(nxt, nslab, more, e_regs, xnext);
     __builtin_amdgcn_sched_barrier(0);
     // Fragment addresses.  Row rl = wr*WM + 16*i + lr has the FP6 swizzle
     // ((rl >> 1) & 7) = ((lr >> 1) & 7) and the FP4 swizzle ((rl >> 2) & 3) =
@@ -897,7 +941,7 @@ static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64
   const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
   const dim3 grid((unsigned)(tiles_m * tiles_n)), block(mx::NT);
   if (!qo)
-    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
+    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, dim3(mx::threads<CF, EXP_FULL, 0>()), 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
                        ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
   else if (qo->m > 4)
     hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 2>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
