@@ -40,12 +40,15 @@
 // into a buffer of their own.  Slabs are double
 // buffered in two LDS objects: the loads of slab s+1 are issued right after
 // the barrier that publishes slab s and have all of slab s's MFMAs to land.
-// The direct loads are issue-rate bound (about 31 cycles per instruction per
-// CU from L2, whatever their width), so the kernel issues no load it does not
-// need (an L2 prefetch of slab s+2 cost more than it saved).  A 256-thread
-// workgroup (2x2 waves) computes a 256x256 tile (128 along an operand with two
-// chunk planes); tiles are ordered so that neighbours share panels in L2 on
-// the same XCD.
+// Every load instruction costs the MFMA waves that issue it time (the load
+// path takes about 31 cycles per instruction per CU, whatever the width, and
+// the issuing wave stalls behind it), so the kernel issues no load it does not
+// need (an L2 prefetch of slab s+2 cost more than it saved), spreads a slab's
+// loads between blocks of MFMAs, and where the registers allow (256x128 tiles
+// of FP4 + FP6 operands) hands them to a fifth wave that only issues loads.  A
+// 256-thread workgroup (2x2 MFMA waves) computes a 256x256 tile (128 along an
+// operand with two chunk planes); tiles are ordered so that neighbours share
+// panels in L2 on the same XCD.
 #pragma once
 #include "bfp_quant.h"
 
@@ -399,8 +402,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   // Groups of 16 with full slabs (XP): the exponents of slab pair p (slabs 2p
   // and 2p + 1: 16 contiguous bytes per row) come in one 16-byte load per row,
   // with slab 2p's mantissas, into their own buffer xe[p % 2] -- a quarter of
-  // the load instructions of per-slab dword loads (the loads are issue-rate
-  // bound).  The stages then hold only mantissas (and the converted output's
+  // the load instructions of per-slab dword loads.  The stages then hold only mantissas (and the converted output's
   // strips).  Otherwise each stage holds its slab's exponents.
   constexpr bool XP = EXP_FULL && CF::G == 16;
   constexpr bool X3 = FASTBFP_MX_X3 && NA == 2 && NB == 2 && CF::G == 16 && !CF::PIPE && !FA && !FB;
@@ -621,9 +623,9 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     asm volatile("" ::: "memory");
     const bool more = s + 1 < nslabs;
     const int nslab = more ? s + 1 : s;
-    // With an FP6 operand the loads are issue-rate bound: they go out in NPART
-    // parts between the blocks of MFMAs, so that the wave keeps issuing MFMAs
-    // while the load path works through them (FP6 x FP6: 10-14% faster, two
+    // With an FP6 operand the loads go out in NPART parts between the blocks
+    // of MFMAs, so that the wave keeps issuing MFMAs while the load path works
+    // through them (FP6 x FP6: 10-14% faster, two
     // chunk planes 1-12%).  FP4 x FP4 slabs have half the load instructions,
     // and there issuing them all at once, here, is faster (their latency, not
     // their issue, is what shows).
