@@ -407,7 +407,8 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   constexpr bool XP = EXP_FULL && CF::G == 16;
   constexpr bool X3 = FASTBFP_MX_X3 && NA == 2 && NB == 2 && CF::G == 16 && !CF::PIPE && !FA && !FB;
   constexpr bool PROD = mx::producer<CF, EXP_FULL, QNCH>();
-  constexpr bool PIPE2 = FASTBFP_MX_PIPE2 && PROD;  // explicit pipeline of the two-chunk loop
+  // explicit pipeline of the two-chunk loop
+  constexpr bool PIPE2 = FASTBFP_MX_PIPE2 && (NA == 2 || NB == 2) && CF::G == 16 && !X3;
   constexpr int NTHR = mx::threads<CF, EXP_FULL, QNCH>();
   constexpr int STRIP_BYTES = QNCH ? 4 * 16 * (CF::WN + 4) * 4 : 0;
   constexpr int SB = XP ? (CF::OFF_EA > STRIP_BYTES ? CF::OFF_EA : STRIP_BYTES) : CF::STAGE;
@@ -748,51 +749,55 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
         });
       });
     } else if constexpr (PIPE2) {
-      // Software pipeline of the two-chunk kernel with the load-issuing wave
-      // (no loads here; both operands have an FP4 upper plane).  A block is
-      // one A fragment (row tile i, chunk plane ca) against the B fragments of
-      // both chunk planes: 2 TN MFMAs; a K-step is the blocks (i, 0), (i, 1)
-      // for each i.  Each block first reads the next block's A fragment (and
-      // with it, for the upper plane, the row's exponent byte, which serves
-      // both planes), and the blocks of K-step 0 also read a share of K-step
-      // 1's B fragments, so that every LDS read has a block of MFMAs to land
-      // in; a scheduling barrier closes each block.  B's FP4 slot holds the
-      // group pair of both K-steps and is read once.
-      static_assert(FA && FB, "upper planes in FP4");
-      constexpr int BPK = 2 * TM;    // blocks per K-step
+      // Software pipeline of the two-chunk kernels (an operand in two chunk
+      // planes, groups of 16).  A block is one A fragment (row tile i, chunk
+      // plane ca) against the B fragments of every chunk plane: NB TN MFMAs;
+      // a K-step is the blocks (i, 0 .. NA-1) for each i.  Each block first
+      // reads the next block's A fragment (and with a row's first plane its
+      // exponent byte, which serves every plane), and the blocks of K-step 0
+      // also read a share of K-step 1's B fragments, so that every LDS read
+      // has a block of MFMAs to land in; the next slab's load parts go
+      // between blocks (none with the load-issuing wave), and a scheduling
+      // barrier closes each block.  A B plane of FP4 slots holds the group
+      // pairs of both K-steps and is read once.
+      constexpr int BPK = NA * TM;   // blocks per K-step
       constexpr int NBLK = 2 * BPK;  // blocks per slab
-      u32x4 y4[TN], y6[2][TN], xa[2];
+      u32x4 yb[2][NB][TN], xa[2];
       int ebr[2][TN], ear[2];
       auto read_b = [&](int ks, int j) {
-        if (ks == 0) y4[j] = rd(slot_addr(mx::b_plane<CF>(0), 1, b_r, j, 0));
-        y6[ks][j] = rd(slot_addr(mx::b_plane<CF>(1), 0, b_r, j, ks));
+        static_for<NB>([&](auto cbc) {
+          constexpr int cb = decltype(cbc)::value, fb = mx::b_fp4<CF>(cb);
+          if (!fb || ks == 0) yb[ks][cb][j] = rd(slot_addr(mx::b_plane<CF>(cb), fb, b_r, j, fb ? 0 : ks));
+        });
         ebr[ks][j] = (int)xcur[eb_lane + j * 16 * ER + ks];
       };
       auto read_a = [&](int blk) {
-        const int ks = blk / BPK, i = (blk % BPK) / 2, ca = blk % 2;
-        xa[blk & 1] = rd(slot_addr(ca ? mx::a_plane<CF>(1) : mx::a_plane<CF>(0), ca ? 0 : 1, a_r, i, ks));
-        if (ca == 0) ear[(blk / 2) & 1] = (int)xcur[ea_lane + i * 16 * ER + ks];
+        const int ks = blk / BPK, i = (blk % BPK) / NA, ca = blk % NA;
+        xa[blk & 1] = rd(slot_addr(mx::a_plane<CF>(ca), mx::a_fp4<CF>(ca), a_r, i, ks));
+        if (ca == 0) ear[(blk / NA) & 1] = (int)xcur[ea_lane + i * 16 * ER + ks];
       };
 #pragma unroll
       for (int j = 0; j < TN; ++j) read_b(0, j);
       read_a(0);
       static_for<NBLK>([&](auto bc) {
         constexpr int blk = decltype(bc)::value;
-        constexpr int ks = blk / BPK, i = (blk % BPK) / 2, ca = blk % 2;
+        constexpr int ks = blk / BPK, i = (blk % BPK) / NA, ca = blk % NA;
         constexpr int fa = mx::a_fp4<CF>(ca);
         if constexpr (blk + 1 < NBLK) read_a(blk + 1);
         if constexpr (ks == 0) {
 #pragma unroll
           for (int j = blk * TN / BPK; j < (blk + 1) * TN / BPK; ++j) read_b(1, j);
         }
-        const int ea = ear[(blk / 2) & 1] + (ca ? 0 : 4);  // +4 per chunk of significance
-        static_for<2>([&](auto cbc) {
+        const int ea = ear[(blk / NA) & 1] + 4 * (NA - 1 - ca);  // +4 per chunk of significance
+        static_for<NB>([&](auto cbc) {
           constexpr int cb = decltype(cbc)::value, fb = mx::b_fp4<CF>(cb);
           const v8i av = op_a<fa, fb>(xa[blk & 1], ks);
 #pragma unroll
           for (int j = 0; j < TN; ++j)
-            mma<fa, fb>(acc[i][j], av, op_b<fa, fb>(cb ? y6[ks][j] : y4[j], ks), ea, ebr[ks][j] + (cb ? 0 : 4));
+            mma<fa, fb>(acc[i][j], av, op_b<fa, fb>(yb[fb ? 0 : ks][cb][j], ks), ea,
+                        ebr[ks][j] + 4 * (NB - 1 - cb));
         });
+        issue_after(blk, NBLK);
         __builtin_amdgcn_sched_barrier(0);
       });
     } else if constexpr (X3) {
