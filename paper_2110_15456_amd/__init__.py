@@ -14,6 +14,7 @@ runs in the library's HIP kernels; there is no CPU path.
 from __future__ import annotations
 
 import ctypes
+import math
 from dataclasses import dataclass
 
 import torch
@@ -100,7 +101,7 @@ def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rou
     ax = group_axis % nd
     if ax == nd - 1:
         C = x.shape[-1]
-        R = x.numel() // C if C else 0
+        R = math.prod(x.shape[:-1])  # leading axes flattened into rows (also when C = 0)
         axis_flag, rows, length = 1, R, C
     elif nd == 2 and ax == 0:
         R, C = x.shape
@@ -205,7 +206,7 @@ def quantize_adaptive(x: torch.Tensor, group_axis: int = -1, g: int = 16, roundi
     ax = group_axis % nd
     if ax == nd - 1:
         C = x.shape[-1]
-        R = x.numel() // C if C else 0
+        R = math.prod(x.shape[:-1])  # leading axes flattened into rows (also when C = 0)
         axis_flag, rows, length = 1, R, C
     elif nd == 2 and ax == 0:
         R, C = x.shape

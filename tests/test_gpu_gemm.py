@@ -103,6 +103,27 @@ def test_full_slab_counts(nslabs):
         check_gemm(A, B, oa, ob)
 
 
+@pytest.mark.parametrize("g", [16, 32])
+def test_degenerate_shapes(g):
+    """K = 0: every kernel family (one chunk, two chunks, the cross-product
+    and the load-issuing-wave variants) runs zero slabs and writes C = 0;
+    M = 0 or N = 0: an empty C, nothing launched."""
+    for pa, pb in [(2, 2), (4, 4), (2, 4), (4, 6), (6, 6), (8, 8)]:
+        announce("gemm K=0 g=%d (%d,%d)" % (g, pa, pb))
+        A = fb.quantize(torch.zeros((300, 0), device="cuda"), g=g, m=pa)
+        B = fb.quantize(torch.zeros((200, 0), device="cuda"), g=g, m=pb)
+        C = fb.gemm(A, B)
+        torch.cuda.synchronize()
+        assert tuple(C.shape) == (300, 200) and not torch.any(C != 0).item()
+        announce("gemm M=0 / N=0 g=%d (%d,%d)" % (g, pa, pb))
+        xa = torch.ones((0, 256), device="cuda")
+        xb = torch.ones((64, 256), device="cuda")
+        A0, B1 = fb.quantize(xa, g=g, m=pa), fb.quantize(xb, g=g, m=pb)
+        assert tuple(fb.gemm(A0, B1).shape) == (0, 64)
+        assert tuple(fb.gemm(B1, fb.quantize(xa, g=g, m=pb)).shape) == (64, 0)
+        torch.cuda.synchronize()
+
+
 def test_precision_lowering():
     xa = synth.draw("half_normal", (130, 320), 5)
     xb = synth.draw("grads", (70, 320), 6)
