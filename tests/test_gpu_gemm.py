@@ -124,6 +124,35 @@ def test_degenerate_shapes(g):
         torch.cuda.synchronize()
 
 
+def test_strided_output():
+    """bfp_gemm through the C-ABI into a wider row-major buffer (ldc > N): at a
+    16-byte-aligned base with ldc a multiple of 4 (the 16-byte store path) and
+    at a 4-byte-aligned base with an odd ldc (the 4-byte path).  The values are
+    the oracle's, and the columns between the rows and the words around the
+    output stay untouched."""
+    import ctypes
+    M, N, K = 130, 72, 384
+    xa = synth.draw("normal", (M, K), 901)
+    xb = synth.draw("weights", (N, K), 902)
+    lib = fb._lib.load()
+    P = ctypes.c_void_p
+    for pa, pb in [(2, 2), (4, 4), (2, 4), (4, 6), (6, 6), (8, 8)]:
+        A, B, oa, ob = operands(xa, xb, pa, pb)
+        Co, S = oracle.gemm(oa[0], oa[1], A.m, ob[0], ob[1], B.m, g=16, rows=np.arange(M), threads=THREADS)
+        for off, ldc in [(4, 80), (1, 81)]:
+            announce("gemm strided out (%d,%d) offset %d ldc %d" % (pa, pb, off, ldc))
+            big = torch.full((off + M * ldc + 8,), -7.0, dtype=torch.float32, device="cuda")
+            rc = lib.bfp_gemm(P(A.mant.data_ptr()), P(A.exp.data_ptr()), A.m, P(B.mant.data_ptr()),
+                              P(B.exp.data_ptr()), B.m, M, N, K, 16, A.m, B.m, P(big.data_ptr() + 4 * off), ldc,
+                              P(torch.cuda.current_stream().cuda_stream))
+            assert rc == 0
+            torch.cuda.synchronize()
+            h = big.cpu().numpy()
+            Cw = h[off:off + M * ldc].reshape(M, ldc).astype(np.float64)
+            assert np.all(np.abs(Cw[:, :N] - Co) <= TOL * S)
+            assert np.all(Cw[:, N:] == -7.0) and np.all(h[:off] == -7.0) and np.all(h[off + M * ldc:] == -7.0)
+
+
 def test_precision_lowering():
     xa = synth.draw("half_normal", (130, 320), 5)
     xb = synth.draw("grads", (70, 320), 6)
