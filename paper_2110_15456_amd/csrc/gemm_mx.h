@@ -85,8 +85,6 @@ namespace mx {
 #ifndef FASTBFP_MX11_BN
 #define FASTBFP_MX11_BN FASTBFP_MX_BN
 #endif
-constexpr int WGM = 2, WGN = 2;  // wave grid along M and N
-constexpr int NT = 64 * WGM * WGN;
 constexpr int KG = 8;            // groups per K slab (two MFMA K-steps)
 // NA / NB: chunk planes of A / B read; FA / FB: 1 if plane 0 of A / B holds
 // FP4 codes (plane 1 always holds FP6 codes).
@@ -95,9 +93,13 @@ constexpr int KG = 8;            // groups per K slab (two MFMA K-steps)
 // those of a g = 16 tensor with twice the groups (each group is its two
 // 16-value halves), so the staging works in 16-value halves either way; EK
 // exponent bytes per row and slab.
-template <int BM_, int BN_, int NA_, int NB_, int FA_, int FB_, int G_ = 16>
+// WGM x WGN: the MFMA wave grid (2 x 2: 256 accumulator registers per wave
+// for a 256x256 tile).  A 2 x 4 grid (128 each, two waves per SIMD) compiles
+// too; for the one-chunk kernels it was no faster (-4% to +2%).
+template <int BM_, int BN_, int NA_, int NB_, int FA_, int FB_, int G_ = 16, int WGN_ = 2>
 struct Cfg {
   static constexpr int BM = BM_, BN = BN_, NA = NA_, NB = NB_, FA = FA_, FB = FB_, G = G_;
+  static constexpr int WGM = 2, WGN = WGN_, NW = WGM * WGN, NT = 64 * NW;  // MFMA wave grid, threads
   static constexpr int EK = KG * 16 / G;      // exponents per row and slab
   static constexpr int KSTEPS = G == 16 ? 2 : 1;  // MFMA K-steps per slab
   static_assert(G == 16 || G == 32, "group size 16 or 32");
@@ -120,6 +122,7 @@ struct Cfg {
   static_assert(TM * 16 * WGM == BM && TN * 16 * WGN == BN, "wave tiles cover the tile");
   static_assert((BM + BN) % 64 == 0 && BM % 64 == 0 && BN % 64 == 0,
                 "loads split evenly over the waves; whole waves skip exponent rows past BM + BN");
+  static_assert((BN / 16) % NW == 0 && (BM / 16) % NW == 0, "plane loads split evenly over the waves");
   static_assert(2 * STAGE <= 160 * 1024, "two stages fit in LDS");
 };
 // LDS offset of plane p of A / B within a stage, and its format.
@@ -139,7 +142,7 @@ constexpr bool producer() {
   return FASTBFP_MX_PROD && EXP_FULL && CF::G == 16 && QNCH == 0 && CF::NA == 2 && CF::NB == 2 && CF::FA && CF::FB;
 }
 template <class CF, bool EXP_FULL, int QNCH>
-constexpr int threads() { return producer<CF, EXP_FULL, QNCH>() ? NT + 64 : NT; }
+constexpr int threads() { return producer<CF, EXP_FULL, QNCH>() ? CF::NT + 64 : CF::NT; }
 }  // namespace mx
 
 // Calls f(ic<0>{}), ..., f(ic<N-1>{}): a loop whose index is a constant
@@ -208,16 +211,16 @@ __device__ __forceinline__ rsrc_t make_rsrc(const uint8_t* p, uint32_t bytes) {
 // resource and read zero.
 // (Every loader issues its per-wave instructions u in [u0, u1) only, so that
 // a slab's loads can be spread over the MFMAs of the previous slab.)
-template <int ROWS>
-constexpr int plane_loads(bool fp4) { return fp4 ? ROWS / 64 : ROWS * mx::KG / 256; }  // per wave
-template <int ROWS, bool RAGGED>
+template <int NW, int ROWS>
+constexpr int plane_loads(bool fp4) { return (fp4 ? ROWS / 16 : ROWS * mx::KG / 64) / NW; }  // per wave
+template <int NW, int ROWS, bool RAGGED>
 __device__ __forceinline__ void load_plane(uint8_t* lds_plane, rsrc_t rsrc, uint32_t lane_off, uint32_t row_bytes,
                                            int slab, bool g_ok, int wave, int u0, int u1) {
   constexpr int INSTR = ROWS * mx::KG / 64;
 #pragma unroll
-  for (int u = 0; u < INSTR / 4; ++u) {
+  for (int u = 0; u < INSTR / NW; ++u) {
     if (u < u0 || u >= u1) continue;
-    const int blk = wave + 4 * u;
+    const int blk = wave + NW * u;
     uint32_t off = lane_off + (uint32_t)blk * 8u * row_bytes + (uint32_t)slab * (mx::KG * 12);
     if (RAGGED && !g_ok) off = 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_plane + blk * 64 * 16), 12, off, 0, 0, 0);
@@ -230,14 +233,14 @@ __device__ __forceinline__ void load_plane(uint8_t* lds_plane, rsrc_t rsrc, uint
 // K read zero; the second group of a pair that straddles K reads whatever
 // follows, which meets a zero exponent (a product scale of 2^-254 or less
 // leaves an FP32 accumulator unchanged).
-template <int ROWS, bool RAGGED>
+template <int NW, int ROWS, bool RAGGED>
 __device__ __forceinline__ void load_plane4(uint8_t* lds_plane, rsrc_t rsrc, uint32_t lane_off, uint32_t row_bytes,
                                             int slab, bool p_ok, int wave, int u0, int u1) {
   constexpr int INSTR = ROWS / 16;
 #pragma unroll
-  for (int u = 0; u < INSTR / 4; ++u) {
+  for (int u = 0; u < INSTR / NW; ++u) {
     if (u < u0 || u >= u1) continue;
-    const int blk = wave + 4 * u;
+    const int blk = wave + NW * u;
     uint32_t off = lane_off + (uint32_t)blk * 16u * row_bytes + (uint32_t)slab * (mx::KG * 8);
     if (RAGGED && !p_ok) off = 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_plane + blk * 64 * 16), 16, off, 0, 0, 0);
@@ -249,17 +252,17 @@ __device__ __forceinline__ void load_plane4(uint8_t* lds_plane, rsrc_t rsrc, uin
 // lane_off is (lane / DPR) * ng + (lane % DPR) * 4.  Instructions past the
 // last (when they do not split evenly over the four waves) go through the
 // zero-length resource rnull into the sink.
-template <int ROWS, int EK>
-constexpr int exps_loads() { return (ROWS * (EK / 4) / 64 + 3) / 4; }  // per wave
-template <int ROWS, int EK>
+template <int NW, int ROWS, int EK>
+constexpr int exps_loads() { return (ROWS * (EK / 4) / 64 + NW - 1) / NW; }  // per wave
+template <int NW, int ROWS, int EK>
 __device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, rsrc_t rnull, uint8_t* sink,
                                               uint32_t lane_off, int ng, int slab, int wave, int u0, int u1) {
   constexpr int DPR = EK / 4, INSTR = ROWS * DPR / 64;
 #pragma unroll
-  for (int u = 0; u < (INSTR + 3) / 4; ++u) {
+  for (int u = 0; u < (INSTR + NW - 1) / NW; ++u) {
     if (u < u0 || u >= u1) continue;
-    const int blk = wave + 4 * u;
-    const bool ok = INSTR % 4 == 0 || blk < INSTR;
+    const int blk = wave + NW * u;
+    const bool ok = INSTR % NW == 0 || blk < INSTR;
     const uint32_t off = lane_off + (uint32_t)blk * (64u / DPR) * (uint32_t)ng + (uint32_t)slab * EK;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(ok ? rsrc : rnull, (lds_void*)(ok ? lds_exps + blk * 256 : sink), 4, off,
                                              0, 0, 0);
@@ -271,16 +274,16 @@ __device__ __forceinline__ void load_exps_lds(uint8_t* lds_exps, rsrc_t rsrc, rs
 // row r lands at lds_x + 16 r.  lane_off is lane * ng.  When the instructions
 // do not split evenly over the four waves, the extra waves repeat the last one
 // (the same bytes to the same place).
-template <int ROWS>
-constexpr int pair_loads() { return (ROWS / 64 + 3) / 4; }  // per wave
-template <int ROWS>
+template <int NW, int ROWS>
+constexpr int pair_loads() { return (ROWS / 64 + NW - 1) / NW; }  // per wave
+template <int NW, int ROWS>
 __device__ __forceinline__ void load_exps_pair(uint8_t* lds_x, rsrc_t rsrc, uint32_t lane_off, int ng, int pair,
                                                int wave, int u0, int u1) {
   constexpr int INSTR = ROWS / 64;
 #pragma unroll
-  for (int u = 0; u < (INSTR + 3) / 4; ++u) {
+  for (int u = 0; u < (INSTR + NW - 1) / NW; ++u) {
     if (u < u0 || u >= u1) continue;
-    const int blk = min(wave + 4 * u, INSTR - 1);
+    const int blk = min(wave + NW * u, INSTR - 1);
     const uint32_t off = lane_off + (uint32_t)blk * 64u * (uint32_t)ng + (uint32_t)pair * 16u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_x + blk * 1024), 16, off, 0, 0, 0);
   }
@@ -410,7 +413,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   // explicit pipeline of the two-chunk loop
   constexpr bool PIPE2 = FASTBFP_MX_PIPE2 && (NA == 2 || NB == 2) && CF::G == 16 && !X3;
   constexpr int NTHR = mx::threads<CF, EXP_FULL, QNCH>();
-  constexpr int STRIP_BYTES = QNCH ? 4 * 16 * (CF::WN + 4) * 4 : 0;
+  constexpr int STRIP_BYTES = QNCH ? CF::NW * 16 * (CF::WN + 4) * 4 : 0;
   constexpr int SB = XP ? (CF::OFF_EA > STRIP_BYTES ? CF::OFF_EA : STRIP_BYTES) : CF::STAGE;
   constexpr int XEB = XP ? (CF::BM + CF::BN) * 16 : 16;
   // Two stages (and two exponent buffers) as separate LDS objects: the
@@ -421,13 +424,13 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   __shared__ __attribute__((aligned(16))) uint8_t stage1[SB];
   __shared__ __attribute__((aligned(16))) uint8_t xe0[XEB];
   __shared__ __attribute__((aligned(16))) uint8_t xe1[XEB];
-  __shared__ __attribute__((aligned(16))) uint8_t sink[4 * 256];  // destination of padding loads, never read
+  __shared__ __attribute__((aligned(16))) uint8_t sink[CF::NW * 256];  // destination of padding loads, never read
   const int tid = threadIdx.x;
   int tm, tn;
   tile_of<FASTBFP_MX_GM>(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
   const int row0 = tm * CF::BM, col0 = tn * CF::BN;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index in an SGPR
-  const int wr = wave / mx::WGN, wc = wave % mx::WGN;
+  const int wr = wave / CF::WGN, wc = wave % CF::WGN;
   const int lr = lane & 15, lb = lane >> 4;
 
   // Zero both stages once: the slot dwords that the 12-byte loads never write
@@ -446,7 +449,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
 
   const int nslabs = (ng + mx::KG - 1) / mx::KG;
   auto exp_row = [&](int k, const uint8_t*& src, int& grow, int& gend, int& lds) {
-    const int r = tid + k * mx::NT;
+    const int r = tid + k * CF::NT;
     const bool is_a = r < CF::BM;
     const int rr = is_a ? r : r - CF::BM;
     src = is_a ? a_exp : b_exp;
@@ -500,10 +503,10 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   // order (the register exponent loads of the ragged path go with part 0).
   // XP: the exponent loads are those of a slab pair, issued only where xe
   // (their destination) is given.
-  constexpr int LA0 = plane_loads<CF::BM>(mx::a_fp4<CF>(0)), LA1 = NA == 2 ? plane_loads<CF::BM>(false) : 0;
-  constexpr int LB0 = plane_loads<CF::BN>(mx::b_fp4<CF>(0)), LB1 = NB == 2 ? plane_loads<CF::BN>(false) : 0;
-  constexpr int LEA = XP ? pair_loads<CF::BM>() : EXP_FULL ? exps_loads<CF::BM, CF::EK>() : 0;
-  constexpr int LEB = XP ? pair_loads<CF::BN>() : EXP_FULL ? exps_loads<CF::BN, CF::EK>() : 0;
+  constexpr int LA0 = plane_loads<CF::NW, CF::BM>(mx::a_fp4<CF>(0)), LA1 = NA == 2 ? plane_loads<CF::NW, CF::BM>(false) : 0;
+  constexpr int LB0 = plane_loads<CF::NW, CF::BN>(mx::b_fp4<CF>(0)), LB1 = NB == 2 ? plane_loads<CF::NW, CF::BN>(false) : 0;
+  constexpr int LEA = XP ? pair_loads<CF::NW, CF::BM>() : EXP_FULL ? exps_loads<CF::NW, CF::BM, CF::EK>() : 0;
+  constexpr int LEB = XP ? pair_loads<CF::NW, CF::BN>() : EXP_FULL ? exps_loads<CF::NW, CF::BN, CF::EK>() : 0;
   constexpr int OFS[6] = {0, LA0, LA0 + LA1, LA0 + LA1 + LB0, LA0 + LA1 + LB0 + LB1, LA0 + LA1 + LB0 + LB1 + LEA};
   constexpr int NLOAD = OFS[5] + LEB;
   // vw: the wave whose share of the instructions is issued (the calling wave,
@@ -521,7 +524,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
 #pragma unroll
       for (int k = 0; k < CF::EXP_ROWS_PER_T; ++k) {
         e[k] = make_uint2(0u, 0u);
-        if (tid + k * mx::NT >= CF::BM + CF::BN) break;
+        if (tid + k * CF::NT >= CF::BM + CF::BN) break;
         const uint8_t* src;
         int grow, gend, lds;
         exp_row(k, src, grow, gend, lds);
@@ -533,30 +536,30 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
 #pragma unroll
     for (int p = 0; p < NA; ++p) {
       if (mx::a_fp4<CF>(p))
-        load_plane4<CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m4_lane_off, rb4, slab, p_ok,
+        load_plane4<CF::NW, CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m4_lane_off, rb4, slab, p_ok,
                                        vw, u0(p), u1(p));
       else
-        load_plane<CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m_lane_off, rb6, slab, g_ok,
+        load_plane<CF::NW, CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m_lane_off, rb6, slab, g_ok,
                                       vw, u0(p), u1(p));
     }
 #pragma unroll
     for (int p = 0; p < NB; ++p) {
       if (mx::b_fp4<CF>(p))
-        load_plane4<CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m4_lane_off, rb4, slab, p_ok,
+        load_plane4<CF::NW, CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m4_lane_off, rb4, slab, p_ok,
                                        vw, u0(2 + p), u1(2 + p));
       else
-        load_plane<CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m_lane_off, rb6, slab, g_ok,
+        load_plane<CF::NW, CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m_lane_off, rb6, slab, g_ok,
                                       vw, u0(2 + p), u1(2 + p));
     }
     if constexpr (XP) {
       if (xe) {
-        load_exps_pair<CF::BM>(xe, live ? rea : rnull, x_lane_off, ng_e, slab / 2, vw, u0(4), u1(4));
-        load_exps_pair<CF::BN>(xe + CF::BM * 16, live ? reb : rnull, x_lane_off, ng_e, slab / 2, vw, u0(5), u1(5));
+        load_exps_pair<CF::NW, CF::BM>(xe, live ? rea : rnull, x_lane_off, ng_e, slab / 2, vw, u0(4), u1(4));
+        load_exps_pair<CF::NW, CF::BN>(xe + CF::BM * 16, live ? reb : rnull, x_lane_off, ng_e, slab / 2, vw, u0(5), u1(5));
       }
     } else if constexpr (EXP_FULL) {
-      load_exps_lds<CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, sink + vw * 256, e_lane_off,
+      load_exps_lds<CF::NW, CF::BM, CF::EK>(stage + CF::OFF_EA, live ? rea : rnull, rnull, sink + vw * 256, e_lane_off,
                                     ng_e, slab, vw, u0(4), u1(4));
-      load_exps_lds<CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, sink + vw * 256, e_lane_off,
+      load_exps_lds<CF::NW, CF::BN, CF::EK>(stage + CF::OFF_EB, live ? reb : rnull, rnull, sink + vw * 256, e_lane_off,
                                     ng_e, slab, vw, u0(5), u1(5));
     }
   };
@@ -569,7 +572,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
         const uint8_t* src;
         int grow, gend, lds;
         exp_row(k, src, grow, gend, lds);
-        if (tid + k * mx::NT >= CF::BM + CF::BN) lds = CF::SPARE;
+        if (tid + k * CF::NT >= CF::BM + CF::BN) lds = CF::SPARE;
         if constexpr (CF::EK == 8) *reinterpret_cast<uint2*>(stage + lds) = e[k];
         else *reinterpret_cast<uint32_t*>(stage + lds) = e[k].x;
       }
@@ -578,7 +581,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
 
   uint2 e_regs[CF::EXP_ROWS_PER_T];
   if constexpr (PROD) {
-    if (wave == mx::WGM * mx::WGN) {
+    if (wave == CF::NW) {
       // The load-issuing wave: slab 0, then after the barrier that publishes
       // slab s the loads of slab s + 1 into the other stage (every MFMA wave
       // has passed that barrier, so is done with slab s - 1 there), and the
@@ -587,7 +590,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
       // per slab), each after waiting for all of its loads.
       auto issue_all = [&](uint8_t* stage, int slab, uint8_t* xe) {
 #pragma unroll
-        for (int v = 0; v < mx::WGM * mx::WGN; ++v) issue(stage, slab, true, e_regs, xe, 0, 1, v);
+        for (int v = 0; v < CF::NW; ++v) issue(stage, slab, true, e_regs, xe, 0, 1, v);
       };
       if (nslabs > 0) issue_all(stage0, 0, xe0);
       for (int s = 0; s < nslabs; ++s) {
@@ -928,7 +931,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     // the same FP32 values and the same noise addressing (gid = the group's
     // index in the output exponent array) as converting C separately.
     constexpr int SROW = CF::WN + 4;  // strip row stride in floats (padding spreads the banks)
-    static_assert(4 * 16 * SROW * 4 <= SB, "four strips fit in one stage");
+    static_assert(CF::NW * 16 * SROW * 4 <= SB, "a strip per wave fits in one stage");
     // Every wave is done with the stages, and no direct load (the last
     // steps' no-op loads included) can still write them.
     __builtin_amdgcn_s_waitcnt(0);
@@ -998,7 +1001,7 @@ static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64
                               const uint8_t* b_exp, int64_t b_ps, int M, int N, int ng, float scale, float* C,
                               int64_t ldc, const OutBFP* qo, hipStream_t s) {
   const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
-  const dim3 grid((unsigned)(tiles_m * tiles_n)), block(mx::NT);
+  const dim3 grid((unsigned)(tiles_m * tiles_n)), block(CF::NT);
   if (!qo)
     hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, dim3(mx::threads<CF, EXP_FULL, 0>()), 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
                        ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
