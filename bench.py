@@ -77,8 +77,9 @@ def parse():
     p.add_argument("--quiet", action="store_true")
     p.add_argument("--gemm-only", action="store_true",
                    help="run only the GEMM sweep and print its JSON (no step, no bench line)")
-    p.add_argument("--gemm-pairs", choices=("default", "all"), default="default",
-                   help="GEMM sweep: six pairs on four shapes, or all 16 operand-format pairs on ffn_up")
+    p.add_argument("--gemm-pairs", choices=("default", "all", "resnet"), default="default",
+                   help="GEMM sweep: six pairs on four shapes, all 16 operand-format pairs on ffn_up, or the "
+                        "ResNet-18 im2col shapes alone")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 256 MiB device copy (torch) whose profiler counters calibrate HBM bytes")
     return p.parse_args()
@@ -216,6 +217,54 @@ def gemm_sweep(torch, fb, synth, dev, args):
             "frac_fp6_peak_issued": round(issued / PEAK_FP6_TFLOPS, 4)}
         log(args, "gemm ffn_up g=32 (%d,%d): %.3f ms, %.0f eff TOPS" % (pa, pb, ms, tops))
     del X, Wt, C
+    return out
+
+
+def resnet_sweep(torch, fb, synth, dev, args):
+    """ResNet-18 convolutions at batch 256, 224x224 input, as im2col GEMMs
+    (C[M,N] = A[M,K] B[N,K]^T, g = 16 along K): half-normal activations, N(0, 0.02)
+    weights, round to nearest.  These shapes are HBM-bound: the roofline time is
+    max(2MNK / int8 MFMA peak, minimum bytes / HBM peak), with minimum bytes =
+    the BFP operands (codes + exponents) read once and the FP32 C written once."""
+    shapes = {"conv2_x": (256 * 56 * 56, 64, 576), "conv3_x": (256 * 28 * 28, 128, 1152),
+              "conv4_x": (256 * 14 * 14, 256, 2304), "conv5_x": (256 * 7 * 7, 512, 4608)}
+    pairs = [(2, 2), (2, 4), (4, 4)]
+    # one activation draw serves every shape: each A is a [M, K] view of its
+    # first M*K values (M*K shrinks from conv2_x on)
+    n_act = max(M * K for M, _, K in shapes.values())
+    act = torch.from_numpy(synth.draw("half_normal", (n_act,), 31)).to(dev)
+    out = {}
+    for i, (name, (M, N, K)) in enumerate(shapes.items()):
+        xa = act[:M * K].view(M, K)
+        wb = torch.from_numpy(synth.draw("weights", (N, K), 32 + i)).to(dev)
+        C = torch.empty((M, N), dtype=torch.float32, device=dev)
+        for pa, pb in pairs:
+            A = fb.quantize(xa, g=G, m=pa)
+            B = fb.quantize(wb, g=G, m=pb)
+            fb.gemm(A, B, out=C)
+            torch.cuda.synchronize()
+            reps = 10
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fb.gemm(A, B, out=C)
+            z.record()
+            torch.cuda.synchronize()
+            ms = a.elapsed_time(z) / reps
+            tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+            nbytes = (M * K * code_bits(pa) + N * K * code_bits(pb)) / 8.0 + (M + N) * K / G + 4.0 * M * N
+            gbs = nbytes / (ms * 1e-3) / 1e9
+            floor_ms = max(2.0 * M * N * K / (PEAK_INT8_TOPS * 1e12), nbytes / (PEAK_HBM_GBS * 1e9)) * 1e3
+            out["%s(%d,%d)" % (name, pa, pb)] = {
+                "M": M, "N": N, "K": K, "ms": round(ms, 4), "eff_tops": round(tops, 1),
+                "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4), "min_bytes": int(nbytes),
+                "GB_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                "roofline_ms": round(floor_ms, 4), "frac_roofline": round(floor_ms / ms, 4)}
+            log(args, "gemm %s (%d,%d): %.3f ms, %.0f eff TOPS, %.0f GB/s (%.0f%% of the roofline time)"
+                % (name, pa, pb, ms, tops, gbs, 100.0 * floor_ms / ms))
+            del A, B
+        del C, wb
+    del act
     return out
 
 
@@ -381,6 +430,9 @@ def main():
     fb._lib.load()  # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
     if args.gemm_only:
+        if args.gemm_pairs == "resnet":
+            print(json.dumps({"resnet_sweep": resnet_sweep(torch, fb, synth, dev, args)}), flush=True)
+            return
         print(json.dumps({"gemm_sweep": gemm_sweep(torch, fb, synth, dev, args)}), flush=True)
         return
     step = Step(torch, fb, synth, dev)
@@ -473,6 +525,8 @@ def main():
         del src, dst
     if not args.no_sweeps:
         result["gemm_sweep"] = gemm_sweep(torch, fb, synth, dev, args)
+        torch.cuda.empty_cache()
+        result["resnet_sweep"] = resnet_sweep(torch, fb, synth, dev, args)
         torch.cuda.empty_cache()
         result["quantize_sweep"] = quantize_sweep(torch, fb, synth, dev, args)
         result["epilogue_sweep"] = epilogue_sweep(torch, fb, synth, dev, args)

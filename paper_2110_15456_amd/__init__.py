@@ -265,21 +265,27 @@ def _gemm_args(A: BFPTensor, B: BFPTensor, m_a, m_b):
 
 
 def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = None,
-         out: torch.Tensor | None = None) -> torch.Tensor:
+         out: torch.Tensor | None = None, tile: int | None = None) -> torch.Tensor:
     """C = A . B^T in FP32 [A.rows, B.rows] for BFP A [M, K] and B [N, K].
 
     m_a / m_b: precision of each operand in the product (default: stored m;
     for a two-chunk operand, m - 4 drops the low chunk plane).
+    tile: None lets the library choose the workgroup tile from the shape
+    (bfp_gemm); 0..3 forces one (bfp_gemm_tiled: the default tile, 256x128,
+    256x64, 128x64 -- the last three for m_a, m_b <= 4 and g = 16 only).
     """
     m_a, m_b = _gemm_args(A, B, m_a, m_b)
     C = out if out is not None else torch.empty((A.rows, B.rows), dtype=torch.float32, device=A.device)
     _need_cuda(C, "out", torch.float32)
     if C.dim() != 2 or C.shape[0] != A.rows or C.shape[1] != B.rows:
         raise ValueError("out must be [%d, %d]" % (A.rows, B.rows))
-    check(load().bfp_gemm(ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
-                          ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows, B.rows,
-                          A.len, A.g, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0), _stream(A.device)),
-          "bfp_gemm")
+    args = (ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
+            ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows, B.rows,
+            A.len, A.g, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0))
+    if tile is None:
+        check(load().bfp_gemm(*args, _stream(A.device)), "bfp_gemm")
+    else:
+        check(load().bfp_gemm_tiled(*args, int(tile), _stream(A.device)), "bfp_gemm_tiled")
     return C
 
 

@@ -26,6 +26,7 @@ SIGNATURES = {
     "bfp_quantize": (_I, [_P, _I64, _I64, _I, _I, _I, _I, _U64, _P, _P, _P, _P]),
     "bfp_dequantize": (_I, [_P, _P, _I64, _I64, _I, _I, _P, _P]),
     "bfp_gemm": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _I64, _P]),
+    "bfp_gemm_tiled": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _I64, _I, _P]),
     "bfp_gemm_group_partials": (_I, [_P, _I, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _P]),
     "bfp_gemm_bfp": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _I, _I, _U64, _P, _P, _P, _P]),
     "bfp_quantize_dual": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P, _P]),
@@ -36,7 +37,7 @@ SIGNATURES = {
     "bfp_adaptive_threshold": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, _I64, _I64, _I64, _I64]),
     "bfp_adaptive_mantissa": (_I, [ctypes.c_double, ctypes.c_double, ctypes.c_double]),
 }
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 _lock = threading.Lock()
 _lib = None

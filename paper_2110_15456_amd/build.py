@@ -20,7 +20,7 @@ LIB = os.path.join(HERE, "libfastbfp.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 SOURCES = ["quantize.hip", "gemm_mx.hip", "gemm_i8.hip", "api.cpp"] + [
-    "gemm_mx_%s%s.hip" % (p, g) for g in ("", "_g32") for p in ("11", "12", "21", "22")]
+    "gemm_mx_%s%s.hip" % (p, g) for g in ("", "_g32") for p in ("11", "12", "21", "22")] + ["gemm_mx_11n.hip"]
 # Per-source extra flags: the quantizer aligns values with ldexp and relies on
 # FP32 denormal flushing to read subnormal inputs as zero.
 SOURCE_FLAGS = {"quantize.hip": ["-fgpu-flush-denormals-to-zero"]}

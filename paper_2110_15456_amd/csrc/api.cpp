@@ -117,17 +117,25 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
   return status_of(fastbfp::launch_dequantize(mant, exp, rows, len, g, m_bits, y, static_cast<hipStream_t>(stream)));
 }
 
-int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
-             int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, float* C, int64_t ldc,
-             void* stream) {
+int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant,
+                   const uint8_t* b_exp, int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b,
+                   float* C, int64_t ldc, int tile, void* stream) {
   int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
   if (st != BFP_OK) return st;
   if (ldc < N) return BFP_E_SHAPE;
+  if (tile < -1 || tile > 3) return BFP_E_ARG;
+  const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
+  if (tile > 0 && (g != 16 || na != 1 || nb != 1)) return BFP_E_UNSUPPORTED;
   if (M == 0 || N == 0) return BFP_OK;
   if (!C || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
-  const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
   return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K, g,
-                                           4 - m_a - m_b, C, ldc, static_cast<hipStream_t>(stream)));
+                                           4 - m_a - m_b, C, ldc, tile, static_cast<hipStream_t>(stream)));
+}
+
+int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+             int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, float* C, int64_t ldc,
+             void* stream) {
+  return bfp_gemm_tiled(a_mant, a_exp, a_m_bits, b_mant, b_exp, b_m_bits, M, N, K, g, m_a, m_b, C, ldc, -1, stream);
 }
 
 int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,

@@ -122,6 +122,20 @@ def test_gemm_validation(lib):
     assert gm(lib, M=0) == OK and gm(lib, N=0, ldc=0) == OK
 
 
+def gmt(lib, tile, a=FAKE, ae=FAKE, am=4, b=FAKE, be=FAKE, bm=4, M=8, N=8, K=64, g=16, ma=4, mb=4, C=FAKE, ldc=8):
+    return lib.bfp_gemm_tiled(a, ae, am, b, be, bm, M, N, K, g, ma, mb, C, ldc, tile, None)
+
+
+def test_gemm_tiled_validation(lib):
+    assert gmt(lib, 4) == E_ARG and gmt(lib, -2) == E_ARG
+    assert gmt(lib, 1, am=6, ma=6) == E_UNSUP            # two chunk planes: default tile only
+    assert gmt(lib, 2, bm=8, mb=8) == E_UNSUP
+    assert gmt(lib, 3, g=32) == E_UNSUP                  # groups of 32: default tile only
+    assert gmt(lib, 1, am=6, ma=2, M=0) == OK            # the low chunk dropped: one plane, empty
+    assert gmt(lib, 0, am=6, ma=6, M=0) == OK and gmt(lib, -1, g=32, N=0, ldc=0) == OK
+    assert gmt(lib, 2, K=40) == E_SHAPE and gmt(lib, 3, C=None) == E_ARG and gmt(lib, 1, ldc=7) == E_SHAPE
+
+
 def test_group_partials_validation(lib):
     f = lib.bfp_gemm_group_partials
     assert f(None, 4, FAKE, 4, 8, 8, 64, 16, 4, 4, FAKE, None) == E_ARG

@@ -26,10 +26,10 @@ def operands(xa, xb, m_a_st, m_b_st, a_axis=-1, b_axis=-1, mode_a="nearest", mod
     return A, B, (qa, ea), (qb, eb)
 
 
-def check_gemm(A, B, oa, ob, m_a=None, m_b=None, rows=None, partials=False):
+def check_gemm(A, B, oa, ob, m_a=None, m_b=None, rows=None, partials=False, tile=None):
     m_a = A.m if m_a is None else m_a
     m_b = B.m if m_b is None else m_b
-    C = fb.gemm(A, B, m_a, m_b)
+    C = fb.gemm(A, B, m_a, m_b, tile=tile)
     torch.cuda.synchronize()
     Cg = C.cpu().numpy().astype(np.float64)
     idx = np.arange(A.rows) if rows is None else np.asarray(rows)
@@ -87,6 +87,39 @@ def test_ragged_shapes(shape):
         announce("gemm %dx%dx%d (%d,%d)" % (M, N, K, pa, pb))
         A, B, oa, ob = operands(xa, xb, pa, pb)
         check_gemm(A, B, oa, ob, partials=(M * N * K <= 64 * 64 * 2048))
+
+
+@pytest.mark.parametrize("tile", [0, 1, 2, 3])
+def test_one_chunk_tiles(tile):
+    """Every workgroup tile of the one-chunk, g = 16 GEMM (256x256, 256x128,
+    256x64, 128x64), forced through bfp_gemm_tiled, on shapes that span several
+    tiles with ragged tails, partial and full slabs, and every one-plane operand
+    format pair (FP4 / FP6 codes, and an FP4 upper plane read alone)."""
+    for M, N, K in [(300, 200, 592), (520, 72, 1024), (129, 257, 144), (1, 1, 16), (5, 300, 4096),
+                    (384, 64, 128 * 5)]:
+        xa = synth.draw("half_normal", (M, K), 900 + M + K)
+        xb = synth.draw("weights", (N, K), 901 + N + K)
+        for am, bm, m_a, m_b in [(2, 2, 2, 2), (2, 4, 2, 4), (4, 2, 4, 2), (3, 4, 3, 4), (6, 1, 2, 1),
+                                 (4, 5, 4, 1)]:
+            announce("gemm tile %d %dx%dx%d stored (%d,%d) at (%d,%d)" % (tile, M, N, K, am, bm, m_a, m_b))
+            A, B, oa, ob = operands(xa, xb, am, bm)
+            check_gemm(A, B, oa, ob, m_a, m_b, tile=tile)
+
+
+def test_tiled_auto_matches_default_tile():
+    """bfp_gemm (tile chosen from the shape) and bfp_gemm_tiled with every
+    tile: the same products, per-group scales and per-output order of the
+    MFMA accumulations, so the FP32 results are identical."""
+    M, N, K = 700, 64, 576
+    xa = synth.draw("half_normal", (M, K), 951)
+    xb = synth.draw("weights", (N, K), 952)
+    A, B, oa, ob = operands(xa, xb, 2, 4)
+    announce("gemm auto tile %dx%dx%d" % (M, N, K))
+    check_gemm(A, B, oa, ob, partials=True)
+    ref = fb.gemm(A, B, tile=0).cpu().numpy()
+    for t in (1, 2, 3):
+        c = fb.gemm(A, B, tile=t).cpu().numpy()
+        assert np.array_equal(c, ref), "tile %d differs from the default tile" % t
 
 
 @pytest.mark.parametrize("nslabs", range(1, 10))
