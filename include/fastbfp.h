@@ -169,15 +169,16 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
  *   tile = -1 : chosen from M and N, exactly as bfp_gemm does;
  *   tile =  0 : the operand formats' default tile (256 x 256 for one chunk
  *               plane per operand);
- *   tile =  1, 2, 3 : 256 x 128, 256 x 64, 128 x 64 -- only for one chunk plane
- *               per operand (m_a, m_b <= 4) with g = 16, else
+ *   tile =  1, 2, 3, 4 : 256 x 128, 256 x 64, 128 x 64, 128 x 128 -- only for
+ *               one chunk plane per operand (m_a, m_b <= 4) with g = 16, else
  *               BFP_E_UNSUPPORTED.
- * For one-chunk, g = 16 products bfp_gemm picks 128 x 64 when N <= 64,
- * 256 x 128 when A's plane holds FP4 codes (A stored with m = 1, 2, 5 or 6)
- * or N <= 128, else 256 x 256, and steps down to a smaller tile while fewer
- * than 192 tiles would leave CUs idle.  Every tile computes the same products, per-group
- * scales and per-output accumulation order, so results do not depend on the
- * tile.  Any other tile value returns BFP_E_ARG.  For tests and tuning.
+ * For one-chunk, g = 16 products bfp_gemm picks 128 x 64 when N <= 64;
+ * 256 x 128 when A's plane holds FP4 codes (A stored with m = 1, 2, 5 or 6);
+ * otherwise 256 x 256, or 128 x 128 when N <= 128; and it steps down to a
+ * smaller tile while fewer than 192 tiles would leave CUs idle.  Every tile
+ * computes the same products, per-group scales and per-output accumulation
+ * order, so results do not depend on the tile.  Any other tile value returns
+ * BFP_E_ARG.  For tests and tuning.
  */
 int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant,
                    const uint8_t* b_exp, int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b,

@@ -271,8 +271,8 @@ def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = N
     m_a / m_b: precision of each operand in the product (default: stored m;
     for a two-chunk operand, m - 4 drops the low chunk plane).
     tile: None lets the library choose the workgroup tile from the shape
-    (bfp_gemm); 0..3 forces one (bfp_gemm_tiled: the default tile, 256x128,
-    256x64, 128x64 -- the last three for m_a, m_b <= 4 and g = 16 only).
+    (bfp_gemm); 0..4 forces one (bfp_gemm_tiled: the default tile, 256x128,
+    256x64, 128x64, 128x128 -- the last four for m_a, m_b <= 4 and g = 16 only).
     """
     m_a, m_b = _gemm_args(A, B, m_a, m_b)
     C = out if out is not None else torch.empty((A.rows, B.rows), dtype=torch.float32, device=A.device)

@@ -123,7 +123,7 @@ int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, co
   int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
   if (st != BFP_OK) return st;
   if (ldc < N) return BFP_E_SHAPE;
-  if (tile < -1 || tile > 3) return BFP_E_ARG;
+  if (tile < -1 || tile > 4) return BFP_E_ARG;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
   if (tile > 0 && (g != 16 || na != 1 || nb != 1)) return BFP_E_UNSUPPORTED;
   if (M == 0 || N == 0) return BFP_OK;

@@ -43,31 +43,32 @@ FASTBFP_MX_DECLARE(2, 2, 1, 1, 32)
 #define FASTBFP_MX11_TILES_DECLARE(FA, FB)      \
   FASTBFP_MX11_TILE_DECLARE(256, 128, FA, FB)   \
   FASTBFP_MX11_TILE_DECLARE(256, 64, FA, FB)    \
-  FASTBFP_MX11_TILE_DECLARE(128, 64, FA, FB)
+  FASTBFP_MX11_TILE_DECLARE(128, 64, FA, FB)    \
+  FASTBFP_MX11_TILE_DECLARE(128, 128, FA, FB)
 FASTBFP_MX11_TILES_DECLARE(0, 0)
 FASTBFP_MX11_TILES_DECLARE(0, 1)
 FASTBFP_MX11_TILES_DECLARE(1, 0)
 FASTBFP_MX11_TILES_DECLARE(1, 1)
 
-// Tile of the one-chunk, groups-of-16, FP32-output GEMM (0..3: 256x256,
-// 256x128, 256x64, 128x64), from measurements on MI355X over the transformer
-// and ResNet-18 im2col shapes:
+// Tile of the one-chunk, groups-of-16, FP32-output GEMM (0..4: 256x256,
+// 256x128, 256x64, 128x64, 128x128), from measurements on MI355X over the
+// transformer, FFN-step and ResNet-18 im2col shapes:
 //  * N <= 64: 128x64 (a wider tile is mostly padding; 256x64 was never the
 //    fastest);
 //  * A in FP4 codes: 256x128 (5-11% faster than 256x256 on the transformer
-//    shapes: its two LDS stages take 60 KB, so two workgroups share a CU);
-//  * A in FP6 codes: 256x256 (a 256x128 tile still needs 92-108 KB of LDS,
-//    one workgroup per CU, and was 30-40% slower), 256x128 for N <= 128;
-//  * then, while the tile count leaves over a quarter of the 256 CUs idle
-//    (fewer than 192 tiles), the next smaller of 256x256 -> 256x128 -> 128x64.
+//    shapes: its two LDS stages take 60-76 KB, so two workgroups share a CU);
+//  * A in FP6 codes: 256x256 (a 256x128 tile still takes 92-108 KB of LDS, one
+//    workgroup per CU, and ran 30-40% slower; 128x128, two per CU, 15-35%
+//    slower), but 128x128 for N <= 128 or when 256x256 tiles are too few;
+//  * too few: fewer than 192 tiles leave over a quarter of the 256 CUs idle;
+//    then the next smaller tile, down to 128x64.
 static int gemm_mx11_tile(int64_t M, int64_t N, int fa) {
   constexpr int64_t MIN_TILES = 192;
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (N <= 64) return 3;
-  int t = fa || N <= 128 ? 1 : 0;
-  if (t == 0 && tiles(256, 256) < MIN_TILES) t = 1;
-  if (t == 1 && tiles(256, 128) < MIN_TILES) t = 3;
-  return t;
+  if (fa) return tiles(256, 128) >= MIN_TILES ? 1 : 3;
+  if (N > 128 && tiles(256, 256) >= MIN_TILES) return 0;
+  return tiles(128, 128) >= MIN_TILES ? 4 : 3;
 }
 
 template <int FA, int FB>
@@ -76,6 +77,7 @@ static hipError_t launch_11_tile(int t, const uint8_t* a_mant, const uint8_t* a_
                                  hipStream_t s) {
   if (t == 1) return launch_mx_11_tile<256, 128, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
   if (t == 2) return launch_mx_11_tile<256, 64, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
+  if (t == 4) return launch_mx_11_tile<128, 128, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
   return launch_mx_11_tile<128, 64, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
 }
 

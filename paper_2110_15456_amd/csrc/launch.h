@@ -47,8 +47,8 @@ hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t r
 // a_m / b_m: the stored operands' widths (they fix the plane formats and
 // plane stride); na / nb: chunk planes read (1 or 2); g: 16 or 32.
 // scale_log2 = 4 - m_a - m_b.  tile: -1 chosen from the shape, 0 the default
-// tile of the operand formats, 1..3 256x128 / 256x64 / 128x64 (one chunk plane
-// per operand and g = 16 only; the caller checks).
+// tile of the operand formats, 1..4 256x128 / 256x64 / 128x64 / 128x128 (one
+// chunk plane per operand and g = 16 only; the caller checks).
 hipError_t launch_gemm_mx(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int na, const uint8_t* b_mant,
                           const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int g,
                           int scale_log2, float* C, int64_t ldc, int tile, hipStream_t s);

@@ -127,7 +127,7 @@ def gmt(lib, tile, a=FAKE, ae=FAKE, am=4, b=FAKE, be=FAKE, bm=4, M=8, N=8, K=64,
 
 
 def test_gemm_tiled_validation(lib):
-    assert gmt(lib, 4) == E_ARG and gmt(lib, -2) == E_ARG
+    assert gmt(lib, 5) == E_ARG and gmt(lib, -2) == E_ARG
     assert gmt(lib, 1, am=6, ma=6) == E_UNSUP            # two chunk planes: default tile only
     assert gmt(lib, 2, bm=8, mb=8) == E_UNSUP
     assert gmt(lib, 3, g=32) == E_UNSUP                  # groups of 32: default tile only

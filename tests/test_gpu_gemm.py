@@ -89,10 +89,10 @@ def test_ragged_shapes(shape):
         check_gemm(A, B, oa, ob, partials=(M * N * K <= 64 * 64 * 2048))
 
 
-@pytest.mark.parametrize("tile", [0, 1, 2, 3])
+@pytest.mark.parametrize("tile", [0, 1, 2, 3, 4])
 def test_one_chunk_tiles(tile):
     """Every workgroup tile of the one-chunk, g = 16 GEMM (256x256, 256x128,
-    256x64, 128x64), forced through bfp_gemm_tiled, on shapes that span several
+    256x64, 128x64, 128x128), forced through bfp_gemm_tiled, on shapes that span several
     tiles with ragged tails, partial and full slabs, and every one-plane operand
     format pair (FP4 / FP6 codes, and an FP4 upper plane read alone)."""
     for M, N, K in [(300, 200, 592), (520, 72, 1024), (129, 257, 144), (1, 1, 16), (5, 300, 4096),
@@ -117,7 +117,7 @@ def test_tiled_auto_matches_default_tile():
     announce("gemm auto tile %dx%dx%d" % (M, N, K))
     check_gemm(A, B, oa, ob, partials=True)
     ref = fb.gemm(A, B, tile=0).cpu().numpy()
-    for t in (1, 2, 3):
+    for t in (1, 2, 3, 4):
         c = fb.gemm(A, B, tile=t).cpu().numpy()
         assert np.array_equal(c, ref), "tile %d differs from the default tile" % t
 
