@@ -176,13 +176,23 @@ __device__ __forceinline__ void tile_of(int bid, int nblocks, int tiles_m, int t
 }
 
 // Exponents of one slab for one row (EK bytes of ng_e per row), zero past
-// the last group and for rows past the end.
+// the last group and for rows past the end.  dw: every row starts 4-byte
+// aligned and holds a multiple of 4 exponents (K a multiple of 4 groups), so
+// a slab's valid bytes are whole dwords: one dword load per 4 exponents
+// instead of one byte load each (the ragged-K ResNet shape, K = 576).
 template <int EK>
-__device__ __forceinline__ uint2 load_exps(const uint8_t* __restrict__ exps, int row, int row_end, int ng, int slab) {
+__device__ __forceinline__ uint2 load_exps(const uint8_t* __restrict__ exps, int row, int row_end, int ng, int slab,
+                                           bool dw) {
   const bool rok = row < row_end;
   const int64_t base = (int64_t)(rok ? row : 0) * ng + slab * EK;
   const int gvalid = min(EK, ng - slab * EK);
   uint32_t w[2] = {0u, 0u};
+  if (dw) {
+#pragma unroll
+    for (int k = 0; k < (EK + 3) / 4; ++k)
+      if (rok && 4 * k < gvalid) w[k] = *reinterpret_cast<const uint32_t*>(exps + base + 4 * k);
+    return make_uint2(w[0], w[1]);
+  }
 #pragma unroll
   for (int j = 0; j < EK; ++j) {
     const uint32_t b = exps[base + min(j, gvalid - 1)];
@@ -481,6 +491,8 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   const uint32_t m4_lane_off = (uint32_t)(lane >> 2) * rb4 + (uint32_t)p_lane * 16u;
   // Exponents: ng_e per row (one per group of G).
   const int ng_e = ng * 16 / CF::G;
+  const bool exp_dw = (ng_e & 3) == 0 && (reinterpret_cast<uintptr_t>(a_exp) & 3) == 0 &&
+                      (reinterpret_cast<uintptr_t>(b_exp) & 3) == 0;
   const rsrc_t rea = make_rsrc(a_exp + (int64_t)row0 * ng_e, (uint32_t)(a_rows * ng_e));
   const rsrc_t reb = make_rsrc(b_exp + (int64_t)col0 * ng_e, (uint32_t)(b_rows * ng_e));
   constexpr int DPR = CF::EK / 4;
@@ -528,7 +540,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
         const uint8_t* src;
         int grow, gend, lds;
         exp_row(k, src, grow, gend, lds);
-        e[k] = load_exps<CF::EK>(src, grow, gend, ng_e, slab);
+        e[k] = load_exps<CF::EK>(src, grow, gend, ng_e, slab, exp_dw);
       }
     }
     const bool g_ok = slab * mx::KG + g_lane < ng;

@@ -95,8 +95,10 @@ def test_one_chunk_tiles(tile):
     256x64, 128x64, 128x128), forced through bfp_gemm_tiled, on shapes that span several
     tiles with ragged tails, partial and full slabs, and every one-plane operand
     format pair (FP4 / FP6 codes, and an FP4 upper plane read alone)."""
+    # K = 576, 192, 64: ragged K whose exponent rows are whole dwords (the
+    # dword exponent loads, last slab half full); 592, 144, 16: byte loads
     for M, N, K in [(300, 200, 592), (520, 72, 1024), (129, 257, 144), (1, 1, 16), (5, 300, 4096),
-                    (384, 64, 128 * 5)]:
+                    (384, 64, 128 * 5), (260, 136, 576), (130, 70, 192), (70, 130, 64)]:
         xa = synth.draw("half_normal", (M, K), 900 + M + K)
         xb = synth.draw("weights", (N, K), 901 + N + K)
         for am, bm, m_a, m_b in [(2, 2, 2, 2), (2, 4, 2, 4), (4, 2, 4, 2), (3, 4, 3, 4), (6, 1, 2, 1),
