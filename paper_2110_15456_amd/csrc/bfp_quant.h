@@ -77,13 +77,16 @@ __device__ __forceinline__ v6u_t cvt_fp6_x32(v16f_t a, v16f_t b) {
 template <int G, int NG, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ>
 __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uint32_t m, uint64_t gid, uint32_t key0,
                                                 uint32_t key1, uint32_t (&w)[NCH][NG * G * 6 / 32],
-                                                uint32_t (&E_out)[NG], bool& nonfinite, uint32_t& s_lo,
-                                                uint32_t& s_hi) {
-  static_assert(NG == 1 || (!ADAPT && G == 16), "several groups per call: 16-value groups, not adaptive");
+                                                uint32_t (&E_out)[NG], bool& nonfinite, uint32_t (&s_lo)[NG],
+                                                uint32_t (&s_hi)[NG]) {
+  static_assert(NG == 1 || G == 16, "several groups per call: 16-value groups");
   constexpr bool FP4[2] = {F0, F1};
   constexpr int LEN = NG * G;  // values converted together (one packing unit)
-  s_lo = 0u;
-  s_hi = 0u;
+#pragma unroll
+  for (int gi = 0; gi < NG; ++gi) {
+    s_lo[gi] = 0u;
+    s_hi[gi] = 0u;
+  }
   nonfinite = false;
   // (a) shared exponent of each group: the largest biased exponent field.
   uint32_t E[NG];
@@ -149,8 +152,8 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
     }
     q = min(q, qmax);  // a group maximum that rounds up to 2^m saturates
     if (ADAPT) {
-      s_lo += q & 3u;
-      s_hi += q >> 2;
+      s_lo[t / G] += q & 3u;
+      s_hi[t / G] += q >> 2;
     }
     // the chunk of each plane
     uint32_t c[2];
@@ -196,9 +199,11 @@ template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ = fal
 __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
                                                uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
                                                bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
-  uint32_t E[1];
-  quantize_groups<G, 1, MODE, NCH, ADAPT, F0, F1, FTZ>(b, m, gid, key0, key1, w, E, nonfinite, s_lo, s_hi);
+  uint32_t E[1], lo[1], hi[1];
+  quantize_groups<G, 1, MODE, NCH, ADAPT, F0, F1, FTZ>(b, m, gid, key0, key1, w, E, nonfinite, lo, hi);
   E_out = E[0];
+  s_lo = lo[0];
+  s_hi = hi[0];
 }
 
 // Stores plane p's codes of group gid (from quantize_group) at

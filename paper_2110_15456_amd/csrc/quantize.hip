@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void k_improvement_finalize(double* sums, int6
 
 // Groups along the contiguous last axis: group gid covers x[gid*G, gid*G+G).
 // A lane owns GPL consecutive groups (two of 16 -- one 32-value packing unit
-// of the FP6 converter -- or one of 32; one of 16 on the adaptive path), a
+// of the FP6 converter, also on the adaptive path -- or one of 32), a
 // wave 64 * GPL groups.  Their FP32 values are brought into the wave's LDS
 // region by direct global->LDS 16-byte loads, each of which reads 1 KB
 // contiguous (one lane per 16-byte chunk), and every lane then reads its own
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
                                                        uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
                                                        uint32_t* status, double* sums) {
-  constexpr int GPL = (G == 16 && !ADAPT) ? 2 : 1;  // groups per lane
+  constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane
   constexpr int CPG = G / 4;                         // 16-byte chunks per group
   constexpr int CPL = GPL * CPG;                     // 16-byte chunks per lane
   constexpr int LANES_PER_SWZ = 16 / CPL;
@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   }
   const int64_t gid = g0 + lane * GPL;
   uint32_t w[NCH][GPL * G * 6 / 32];
-  uint32_t E[GPL], s_lo, s_hi;
+  uint32_t E[GPL], s_lo[GPL], s_hi[GPL];
   bool nonfinite;
   quantize_groups<G, GPL, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo,
                                                           s_hi);
@@ -141,9 +141,16 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
     if (NCH == 2) store_plane<G, F1, true>(mant1, gid, w[NCH - 1]);
     if (status && nonfinite) atomicOr(status, 1u);
   }
-  if (ADAPT)
-    block_improvement(nmine ? ldexp((double)s_lo, (int)E[0] - 130) : 0.0,
-                      nmine ? ldexp((double)s_hi, (int)E[0] - 128) : 0.0, sums + 2);
+  if (ADAPT) {
+    double num = 0.0, den = 0.0;
+#pragma unroll
+    for (int gi = 0; gi < GPL; ++gi)
+      if (gi < nmine) {
+        num += ldexp((double)s_lo[gi], (int)E[gi] - 130);
+        den += ldexp((double)s_hi[gi], (int)E[gi] - 128);
+      }
+    block_improvement(num, den, sums + 2);
+  }
 }
 
 // Groups down the columns of x[R][C] (transpose-on-quantize).  Output row c is
@@ -262,7 +269,7 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
 template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
 static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
                                 uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
-  constexpr int GPL = (G == 16 && !ADAPT) ? 2 : 1;  // groups per lane (as in the kernel)
+  constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane (as in the kernel)
   const int64_t blocks = (ngroups + 256 * GPL - 1) / (256 * GPL);
   hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, F0, F1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
                      (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
@@ -338,7 +345,10 @@ hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int
 
 int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g) {
   if (R == 0 || C == 0) return 0;
-  if (group_axis == 1) return (R * (C / g) + 255) / 256;  // one partial pair per k_quantize_rows block
+  if (group_axis == 1) {  // one partial pair per k_quantize_rows block (two groups per lane when g = 16)
+    const int64_t per_block = g == 16 ? 512 : 256;
+    return (R * (C / g) + per_block - 1) / per_block;
+  }
   const int64_t gpr = R / g;
   return ((C + 63) / 64) * ((gpr + 31) / 32);  // one per k_quantize_cols block (NGT = 8)
 }

@@ -209,8 +209,9 @@ def test_adaptive_sums_len(lib):
     assert lib.bfp_adaptive_sums_len(4, 40, 1, 16) == -1
     assert lib.bfp_adaptive_sums_len(4, 32, 1, 8) == -1
     assert lib.bfp_adaptive_sums_len(0, 64, 1, 16) == 2
-    assert lib.bfp_adaptive_sums_len(4, 32, 1, 16) == 4          # 8 groups: one workgroup of 256 groups
-    assert lib.bfp_adaptive_sums_len(8192, 8192, 1, 16) == 2 + 2 * (8192 * 512 // 256)
+    assert lib.bfp_adaptive_sums_len(4, 32, 1, 16) == 4          # 8 groups: one workgroup
+    assert lib.bfp_adaptive_sums_len(8192, 8192, 1, 16) == 2 + 2 * (8192 * 512 // 512)  # 512 groups a block
+    assert lib.bfp_adaptive_sums_len(8192, 8192, 1, 32) == 2 + 2 * (8192 * 256 // 256)  # 256 groups a block
     assert lib.bfp_adaptive_sums_len(512, 100, 0, 16) == 2 + 2 * (2 * 1)  # 2 column blocks x 1 group-row block
 
 
