@@ -11,6 +11,7 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 import subprocess
@@ -30,14 +31,39 @@ _lock = threading.Lock()
 _lib = None
 
 
-def build(force: bool = True) -> str:
-    """Compile oracle.c into liboracle.so next to it (gcc, no GPU code)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp%d" % os.getpid()
+def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
+    """Compile oracle.c (or another C source, e.g. a planted-mistake copy in a
+    test) into a shared library (gcc, no GPU code)."""
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fPIC", "-shared",
-                               _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+                               src, "-o", tmp, "-lm"])
+        os.replace(tmp, out)
+    return out
+
+
+def _bind(lib):
+    """Declare the ctypes signatures of the oracle's C functions on ``lib``."""
+    P = ctypes.c_void_p
+    i64, i32, u64 = ctypes.c_int64, ctypes.c_int, ctypes.c_uint64
+    lib.oracle_philox4x32_10.argtypes = [P, P, P]
+    lib.oracle_noise_byte.argtypes = [u64, u64, ctypes.c_uint32]
+    lib.oracle_noise_byte.restype = ctypes.c_uint32
+    lib.oracle_noise_bytes.argtypes = [u64, u64, i64, i32, P]
+    lib.oracle_quantize_group.argtypes = [P, i64, i32, i32, i32, P, P, i64, P]
+    lib.oracle_quantize_group.restype = i32
+    lib.oracle_quantize.argtypes = [P, i64, i64, i32, i32, i32, i32, u64, i64, i64, P, P]
+    lib.oracle_quantize.restype = i64
+    lib.oracle_dequantize.argtypes = [P, P, i64, i32, i32, i64, i64, P]
+    lib.oracle_gemm.argtypes = [P, P, i32, P, P, i32, i64, i64, i64, i32, i32, i32, P, i64, P, P]
+    lib.oracle_group_partials.argtypes = [P, i32, P, i32, i64, i64, i32, i32, i32, P, i64, P]
+    lib.oracle_relative_improvement.argtypes = [P, P, P, P, i64, i32, i64, i64, P, P]
+    lib.oracle_drop_low_chunk.argtypes = [P, i64, P]
+    lib.oracle_threshold.argtypes = [ctypes.c_double, ctypes.c_double, i64, i64, i64, i64]
+    lib.oracle_threshold.restype = ctypes.c_double
+    lib.oracle_select_mantissa.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double]
+    lib.oracle_select_mantissa.restype = ctypes.c_int
+    return lib
 
 
 def _load():
@@ -46,27 +72,24 @@ def _load():
         if _lib is None:
             if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
                 build(force=True)
-            lib = ctypes.CDLL(_LIB)
-            P = ctypes.c_void_p
-            i64, i32, u64 = ctypes.c_int64, ctypes.c_int, ctypes.c_uint64
-            lib.oracle_philox4x32_10.argtypes = [P, P, P]
-            lib.oracle_noise_byte.argtypes = [u64, u64, ctypes.c_uint32]
-            lib.oracle_noise_byte.restype = ctypes.c_uint32
-            lib.oracle_quantize_group.argtypes = [P, i64, i32, i32, i32, P, P, i64, P]
-            lib.oracle_quantize_group.restype = i32
-            lib.oracle_quantize.argtypes = [P, i64, i64, i32, i32, i32, i32, u64, i64, i64, P, P]
-            lib.oracle_quantize.restype = i64
-            lib.oracle_dequantize.argtypes = [P, P, i64, i32, i32, i64, i64, P]
-            lib.oracle_gemm.argtypes = [P, P, i32, P, P, i32, i64, i64, i64, i32, i32, i32, P, i64, P, P]
-            lib.oracle_group_partials.argtypes = [P, i32, P, i32, i64, i64, i32, i32, i32, P, i64, P]
-            lib.oracle_relative_improvement.argtypes = [P, P, P, P, i64, i32, i64, i64, P, P]
-            lib.oracle_drop_low_chunk.argtypes = [P, i64, P]
-            lib.oracle_threshold.argtypes = [ctypes.c_double, ctypes.c_double, i64, i64, i64, i64]
-            lib.oracle_threshold.restype = ctypes.c_double
-            lib.oracle_select_mantissa.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double]
-            lib.oracle_select_mantissa.restype = ctypes.c_int
-            _lib = lib
+            _lib = _bind(ctypes.CDLL(_LIB))
     return _lib
+
+
+@contextlib.contextmanager
+def use_library(path: str):
+    """Run the oracle's Python functions on another build of its C source (the
+    mutation test plants mistakes in copies of oracle.c this way); the
+    default library is restored on exit."""
+    global _lib
+    prev = _load()
+    with _lock:
+        _lib = _bind(ctypes.CDLL(path))
+    try:
+        yield
+    finally:
+        with _lock:
+            _lib = prev
 
 
 def _ptr(a: np.ndarray):
@@ -99,6 +122,13 @@ def philox4x32_10(counter, key) -> np.ndarray:
 def noise_byte(seed: int, gid: int, p: int) -> int:
     """Stochastic-rounding noise byte of position p in group gid."""
     return int(_load().oracle_noise_byte(seed, gid, p))
+
+
+def noise_bytes(seed: int, gid0: int, ngroups: int, g: int = 16) -> np.ndarray:
+    """Noise bytes of groups gid0 .. gid0 + ngroups - 1: uint8 [ngroups, g]."""
+    out = np.zeros((ngroups, g), np.uint8)
+    _load().oracle_noise_bytes(seed, gid0, ngroups, g, _ptr(out))
+    return out
 
 
 def quantize_group(x, m: int, mode="nearest", noise=None):

@@ -74,6 +74,15 @@ uint32_t oracle_noise_byte(uint64_t seed, uint64_t gid, uint32_t p) {
   return (w[(p / 4u) % 4u] >> (8u * (p % 4u))) & 0xFFu;
 }
 
+/*
+ * The noise bytes of ngroups consecutive groups gid0, gid0 + 1, ... with g
+ * positions each: out[i * g + p] = oracle_noise_byte(seed, gid0 + i, p).
+ */
+void oracle_noise_bytes(uint64_t seed, uint64_t gid0, int64_t ngroups, int g, uint8_t* out) {
+  for (int64_t i = 0; i < ngroups; ++i)
+    for (int p = 0; p < g; ++p) out[i * g + p] = (uint8_t)oracle_noise_byte(seed, gid0 + (uint64_t)i, (uint32_t)p);
+}
+
 /* ------------------------------------------------------------------------ */
 /* FP32 -> BFP conversion of one group (section III-A and the converter of   */
 /* section V-C).                                                             */
