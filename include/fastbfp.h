@@ -156,6 +156,11 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
  *   g            : 16 or 32 (both operands).  A group of 32 fills a whole
  *                  MFMA block; a group of 16 leaves half of it zero.
  *   C            : FP32 with row stride ldc >= N (elements).
+ *   Size limits  : M, N < 2^31, K <= 11184784 (256 rows of 12 bytes per 16
+ *                  values stay below 2^31 bytes: the kernels address operand
+ *                  tiles with 32-bit offsets), and
+ *                  ceil(M / 128) * ceil(N / 64) < 2^31; otherwise
+ *                  BFP_E_UNSUPPORTED.
  * Preconditions for the stated accuracy: every group exponent E is at most 250,
  * and every scaled group sum, partial sum and |C| stays in the FP32 normal range.
  */

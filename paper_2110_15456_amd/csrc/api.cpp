@@ -10,6 +10,9 @@ namespace {
 
 bool group_supported(int g) { return g == 16 || g == 32; }
 
+// Largest K the GEMM accepts: 256 * (K / 16) * 12 < 2^31.
+constexpr int64_t kMaxK = ((int64_t(1) << 31) / (256 * 12) - 1) * 16;
+
 int check_tensor(int64_t rows, int64_t len, int g, int m) {
   if (rows < 0 || len < 0) return BFP_E_ARG;
   if (m < 1 || m > 8) return BFP_E_PRECISION;
@@ -40,7 +43,13 @@ int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, i
   if (!group_supported(g)) return BFP_E_UNSUPPORTED;
   if (K % g != 0) return BFP_E_SHAPE;
   if (planes_used(a_m, m_a) == 0 || planes_used(b_m, m_b) == 0) return BFP_E_PRECISION;
-  if (M > 0x7fffffff || N > 0x7fffffff || K / g > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  // The kernels address a tile's operand rows through 32-bit buffer offsets:
+  // 256 rows of an FP6 plane (12 bytes per 16 values) must span less than
+  // 2^31 bytes (offsets at 2^31 and above are the zero-reading sentinel of
+  // groups past K), and the workgroup count of the smallest tile (128 x 64)
+  // must fit in 31 bits.
+  if (M > 0x7fffffff || N > 0x7fffffff || K > kMaxK) return BFP_E_UNSUPPORTED;
+  if (((M + 127) / 128) * ((N + 63) / 64) > 0x7fffffff) return BFP_E_UNSUPPORTED;
   if (!aligned(a_mant, 4) || !aligned(b_mant, 4)) return BFP_E_ARG;
   return BFP_OK;
 }

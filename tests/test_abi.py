@@ -120,6 +120,12 @@ def test_gemm_validation(lib):
     assert gm(lib, bm=6, mb=1) == E_PREC
     assert gm(lib, a=ctypes.c_void_p(0x100001)) == E_ARG
     assert gm(lib, M=0) == OK and gm(lib, N=0, ldc=0) == OK
+    # 32-bit tile offsets: K up to 11184784 (256 rows of FP6 codes < 2^31 bytes)
+    kmax = ((1 << 31) // (256 * 12) - 1) * 16
+    assert gm(lib, K=kmax + 16) == E_UNSUP and gm(lib, K=kmax + 16, g=32, ma=4, mb=4) == E_UNSUP
+    assert gm(lib, M=0, K=kmax) == OK
+    # workgroup count of the smallest tile beyond 31 bits
+    assert gm(lib, M=(1 << 31) - 1, N=(1 << 31) - 1, ldc=(1 << 31) - 1) == E_UNSUP
 
 
 def gmt(lib, tile, a=FAKE, ae=FAKE, am=4, b=FAKE, be=FAKE, bm=4, M=8, N=8, K=64, g=16, ma=4, mb=4, C=FAKE, ldc=8):
