@@ -80,6 +80,10 @@ def parse():
     p.add_argument("--gemm-pairs", choices=("default", "all", "resnet"), default="default",
                    help="GEMM sweep: six pairs on four shapes, all 16 operand-format pairs on ffn_up, or the "
                         "ResNet-18 im2col shapes alone")
+    p.add_argument("--quantize-only", action="store_true",
+                   help="run only the 64M quantize sweep (per distribution) and print its JSON")
+    p.add_argument("--cpu-only", action="store_true",
+                   help="run only the CPU oracle baseline (no GPU needed) and print its JSON")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="also run a plain 256 MiB device copy (torch) whose profiler counters calibrate HBM bytes")
     return p.parse_args()
@@ -269,50 +273,59 @@ def resnet_sweep(torch, fb, synth, dev, args):
 
 
 def quantize_sweep(torch, fb, synth, dev, args):
-    """64M-element quantize (8192 x 8192, g=16, last axis), three distributions
-    rotated so that consecutive launches read different 256 MB buffers."""
-    xs = [torch.from_numpy(synth.draw(d, (8192, 8192), s)).to(dev)
-          for d, s in (("half_normal", 21), ("weights", 22), ("grads", 23))]
+    """64M-element quantize (8192 x 8192, g=16, last axis) for each of the
+    three distributions separately.  Consecutive launches read three different
+    256 MB buffers holding the same values in different rows (the tensor and
+    two row rotations of it), so the 256 MB Infinity Cache cannot serve a
+    repeated read."""
     out = {}
     n = 8192 * 8192
-    for m in (2, 4, 6, 8):
+    dists = (("half_normal", 21), ("weights", 22), ("grads", 23))
+    for dist, seed in dists:
+        x0 = torch.from_numpy(synth.draw(dist, (8192, 8192), seed)).to(dev)
+        xs = [x0, torch.roll(x0, 2731, 0).contiguous(), torch.roll(x0, 5461, 0).contiguous()]
+        for m in (2, 4, 6, 8):
+            for mode in ("nearest", "stochastic"):
+                outs = [fb.BFPTensor.empty(8192, 8192, G, m, dev) for _ in range(3)]
+                for i in range(3):
+                    fb.quantize(xs[i], g=G, m=m, rounding=mode, seed=1234, out=outs[i])
+                torch.cuda.synchronize()
+                reps = 12
+                a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for r in range(reps):
+                    fb.quantize(xs[r % 3], g=G, m=m, rounding=mode, seed=1234, out=outs[r % 3])
+                z.record()
+                torch.cuda.synchronize()
+                ms = a.elapsed_time(z) / reps
+                gbs = q_bytes(n, m) / (ms * 1e-3) / 1e9
+                out["%s_m%d_%s" % (dist, m, mode)] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
+                                                      "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                                                      "bytes": int(q_bytes(n, m))}
+                log(args, "quantize %s m=%d %s: %.1f us, %.0f GB/s" % (dist, m, mode, ms * 1e3, gbs))
+                del outs
+        # The adaptive converter (Algorithm 1, Eq. 2): one pass writes BFP(X,4),
+        # the 2-bit tensor left by discarding the low chunk, and the two sums.
         for mode in ("nearest", "stochastic"):
-            outs = [fb.BFPTensor.empty(8192, 8192, G, m, dev) for _ in range(3)]
-            for i in range(3):
-                fb.quantize(xs[i], g=G, m=m, rounding=mode, seed=1234, out=outs[i])
+            for r in range(3):
+                fb.quantize_adaptive(xs[r], g=G, rounding=mode, seed=1234)
             torch.cuda.synchronize()
             reps = 12
             a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             for r in range(reps):
-                fb.quantize(xs[r % 3], g=G, m=m, rounding=mode, seed=1234, out=outs[r % 3])
+                fb.quantize_adaptive(xs[r % 3], g=G, rounding=mode, seed=1234)
             z.record()
             torch.cuda.synchronize()
             ms = a.elapsed_time(z) / reps
-            gbs = q_bytes(n, m) / (ms * 1e-3) / 1e9
-            out["m%d_%s" % (m, mode)] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
-                                         "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
-            log(args, "quantize m=%d %s: %.1f us, %.0f GB/s" % (m, mode, ms * 1e3, gbs))
-            del outs
-    # The adaptive converter (Algorithm 1, Eq. 2): one pass writes BFP(X,4),
-    # the 2-bit tensor left by discarding the low chunk, and the two sums.
-    for mode in ("nearest", "stochastic"):
-        for r in range(3):
-            fb.quantize_adaptive(xs[r], g=G, rounding=mode, seed=1234)
-        torch.cuda.synchronize()
-        reps = 12
-        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for r in range(reps):
-            fb.quantize_adaptive(xs[r % 3], g=G, rounding=mode, seed=1234)
-        z.record()
-        torch.cuda.synchronize()
-        ms = a.elapsed_time(z) / reps
-        gbs = n * (4 + 0.75 + 0.5 + 1.0 / G) / (ms * 1e-3) / 1e9
-        out["adaptive_m4m2_%s" % mode] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
-                                          "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
-        log(args, "adaptive m=4/2 %s: %.1f us, %.0f GB/s" % (mode, ms * 1e3, gbs))
-    del xs
+            nbytes = n * (4 + 0.75 + 0.5 + 1.0 / G)
+            gbs = nbytes / (ms * 1e-3) / 1e9
+            out["%s_adaptive_m4m2_%s" % (dist, mode)] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1),
+                                                         "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                                                         "bytes": int(nbytes)}
+            log(args, "adaptive %s m=4/2 %s: %.1f us, %.0f GB/s" % (dist, mode, ms * 1e3, gbs))
+        del xs, x0
+        torch.cuda.empty_cache()
     return out
 
 
@@ -354,6 +367,17 @@ def epilogue_sweep(torch, fb, synth, dev, args):
     return out
 
 
+def calibration_copy(torch, dev):
+    """A plain 256 MiB device copy (torch), three times: its profiler
+    counters calibrate the HBM byte counts of the other kernels."""
+    src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return {"read": src.numel() * 4, "write": dst.numel() * 4}
+
+
 def measured_traffic(key):
     """HBM bytes per launch of a bench kernel from the committed rocprofv3
     counter runs (profiles/traffic.json), or None if the kernel sources have
@@ -371,15 +395,38 @@ def measured_traffic(key):
     return round(entry["bytes_per_launch"]) if entry else None
 
 
+def host_threads():
+    """Threads for the oracle: the cores this process may run on, within the
+    CPU share the environment allots (OMP_NUM_THREADS; on a shared GPU host,
+    one GPU's share of its cores)."""
+    avail = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    return max(1, min(avail, share) if share > 0 else avail), avail
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(args):
-    """The oracle, untuned, on the host cores (at most the 16-thread CPU share
-    of one GPU): every conversion and the weight update of one m=4 step in full, plus the first
-    SAMPLE_ROWS output rows of each GEMM; the GEMM time is scaled to all rows
-    and the step rate reported in the bench's unit."""
+    """The oracle, untuned, on the host cores.  Reported value: one m=4 FFN
+    step in the bench's unit -- every conversion and the weight update in
+    full, plus the first SAMPLE_ROWS output rows of each GEMM, the GEMM time
+    scaled to all rows.  Also: the 64M-element quantize sweep in full for
+    every (distribution, m, rounding mode), and each transformer-block and
+    ResNet-18 im2col GEMM on a sample of output rows (scaled to all rows)."""
     import numpy as np
     import oracle
     from paper_2110_15456_amd import synth
-    threads = max(1, min(os.cpu_count() or 1, 16))
+    threads, avail = host_threads()
+    t_all = time.time()
     X = synth.draw("half_normal", (M_TOK, D_IN), 51)
     W = synth.draw("weights", (D_IN, D_FF), 52)
     dY = synth.draw("grads", (M_TOK, D_FF), 53)
@@ -390,7 +437,7 @@ def cpu_baseline(args):
     dya, dyt, _ = oracle.quantize_dual(dY, g=G, m=m, mode="stochastic", seed_rows=1000, seed_cols=1001,
                                        threads=threads)
     tq = time.time() - t0
-    SAMPLE_ROWS = 384
+    SAMPLE_ROWS = 128
     rows = np.arange(SAMPLE_ROWS)
     t1 = time.time()
     oracle.gemm(xa[0], xa[1], m, wb[0], wb[1], m, g=G, rows=rows, threads=threads)
@@ -403,16 +450,52 @@ def cpu_baseline(args):
     W2 = oracle.weight_update(W, dY[:D_IN, :D_FF], -LR)
     oracle.quantize_dual(W2, g=G, m=m, threads=threads)
     tq += time.time() - t2
+    del X, W, dY, W2, wk, wb, xa, xt, dya, dyt
     # rows sampled: SAMPLE_ROWS of 8192 (fwd, dX) and of 4096 (dW); the three
     # GEMMs have the same N*K per output row, so each took about tg / 3
     full_gemm_s = tg / 3 * (M_TOK + M_TOK + D_IN) / SAMPLE_ROWS
     step_s = tq + full_gemm_s
+
+    # the quantize sweep at full size (8192 x 8192, g = 16 along the last axis)
+    quant = {}
+    n = 8192 * 8192
+    for dist, seed in (("half_normal", 21), ("weights", 22), ("grads", 23)):
+        x = synth.draw(dist, (8192, 8192), seed)
+        for mq in (2, 4, 6, 8):
+            for mode in ("nearest", "stochastic"):
+                t = time.time()
+                oracle.quantize(x, g=G, m=mq, mode=mode, seed=1234, threads=threads)
+                dt = time.time() - t
+                quant["%s_m%d_%s" % (dist, mq, mode)] = {"s": round(dt, 3),
+                                                         "GB_s": round(q_bytes(n, mq) / dt / 1e9, 3)}
+        del x
+    # GEMMs on sampled output rows: transformer block at (4,4), ResNet-18
+    # im2col at (2,4); the oracle's time per output row does not depend on
+    # which rows
+    gemms = {}
+    shapes = [("qkv", 8192, 12288, 4096, 4, 4), ("out_proj", 8192, 4096, 4096, 4, 4),
+              ("ffn_up", 8192, 16384, 4096, 4, 4), ("ffn_down", 8192, 4096, 16384, 4, 4),
+              ("conv2_x", 802816, 64, 576, 2, 4), ("conv3_x", 200704, 128, 1152, 2, 4),
+              ("conv4_x", 50176, 256, 2304, 2, 4), ("conv5_x", 12544, 512, 4608, 2, 4)]
+    for name, Mg, Ng, Kg, pa, pb in shapes:
+        rows_g = max(16, min(Mg, (1 << 27) // (Ng * Kg)))  # about 2^27 MACs
+        xa_g = synth.draw("half_normal", (rows_g, Kg), 71)
+        xb_g = synth.draw("weights", (Ng, Kg), 72)
+        qa_g, ea_g, _ = oracle.quantize(xa_g, g=G, m=pa, threads=threads)
+        qb_g, eb_g, _ = oracle.quantize(xb_g, g=G, m=pb, threads=threads)
+        t = time.time()
+        oracle.gemm(qa_g, ea_g, pa, qb_g, eb_g, pb, g=G, threads=threads)
+        dt = (time.time() - t) * Mg / rows_g
+        gemms["%s(%d,%d)" % (name, pa, pb)] = {"rows_timed": rows_g, "est_s": round(dt, 2),
+                                               "eff_gops": round(2.0 * Mg * Ng * Kg / dt / 1e9, 3)}
     return {"value": round(STEP_OPS / step_s / 1e12, 6), "unit": "TOPS", "cores": threads, "kind": "oracle",
-            "sample": ("one m=4 FFN step: the conversions of X and dY and the weight update with its conversion in "
-                       "full (%.1f s) and the first %d output rows of each GEMM (%.1f s), GEMM time scaled by rows "
-                       "to the full step (est. %.0f s per step)"
-                       % (tq, SAMPLE_ROWS, tg, step_s)),
-            "cpu_seconds": round(tq + tg, 1)}
+            "sample": ("one m=4 FFN step: the conversions of X, dY and W and the weight update in full (%.1f s) and "
+                       "the first %d output rows of each GEMM (%.1f s), GEMM time scaled by rows to the full step "
+                       "(est. %.0f s per step)" % (tq, SAMPLE_ROWS, tg, step_s)),
+            "host": {"cpu_model": cpu_model(), "nproc": os.cpu_count(), "cores_available": avail,
+                     "threads_used": threads},
+            "quantize_64M": quant, "gemm_sampled": gemms,
+            "cpu_seconds": round(time.time() - t_all, 1)}
 
 
 def main():
@@ -421,6 +504,9 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path (--gpus %d requested)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
+    if args.cpu_only:
+        print(json.dumps({"cpu_baseline": cpu_baseline(args)}), flush=True)
+        return
     import torch
     import paper_2110_15456_amd as fb
     from paper_2110_15456_amd import synth
@@ -429,6 +515,12 @@ def main():
         sys.exit(2)
     fb._lib.load()  # fail loudly if the HIP library is missing
     dev = torch.device("cuda:0")
+    if args.quantize_only:
+        res = {"quantize_sweep": quantize_sweep(torch, fb, synth, dev, args)}
+        if args.calibrate_copy:
+            res["copy_calibration_bytes"] = calibration_copy(torch, dev)
+        print(json.dumps(res), flush=True)
+        return
     if args.gemm_only:
         if args.gemm_pairs == "resnet":
             print(json.dumps({"resnet_sweep": resnet_sweep(torch, fb, synth, dev, args)}), flush=True)
@@ -516,13 +608,7 @@ def main():
     del step
     torch.cuda.empty_cache()
     if args.calibrate_copy:
-        src = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        result["copy_calibration_bytes"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
-        del src, dst
+        result["copy_calibration_bytes"] = calibration_copy(torch, dev)
     if not args.no_sweeps:
         result["gemm_sweep"] = gemm_sweep(torch, fb, synth, dev, args)
         torch.cuda.empty_cache()

@@ -131,3 +131,77 @@ def test_stochastic_unbiased_over_1000_seeds():
     assert np.max(np.abs(z)) < 5.5
     pooled = (mean[live] - expect[live]).sum() / np.sqrt((var[live] / 1000).sum())
     assert abs(pooled) < 4.0
+
+
+def test_stochastic_rounding_frequencies_64M():
+    """Theorem 1 on the GPU's output of the 64M-element gradient tensor (SR,
+    Philox seed 1234, m = 4): a value whose magnitude is a LSBs, with
+    r = floor(256 * frac(a)), rounds up with probability exactly r / 256 (the
+    8-bit noise byte is uniform).  The round-up counts in each of the 255 bins
+    r = 1..255 are tested together (chi-square, 255 degrees of freedom);
+    values with r = 0 never round up.  Computed from the GPU's dequantized
+    output and the FP32 input only."""
+    from scipy import stats
+    m = 4
+    x = synth.draw("grads", (8192, 8192), 23)
+    announce("SR round-up frequencies, 8192x8192 grads m=%d" % m)
+    t = fb.quantize(torch.from_numpy(x).cuda(), g=16, m=m, rounding="stochastic", seed=1234)
+    y = np.abs(fb.dequantize(t).cpu().numpy().astype(np.float64)).ravel()
+    E = np.repeat(t.exp.cpu().numpy().astype(np.int64).ravel(), 16)
+    del t
+    lsb_exp = E - 127 - (m - 1)
+    a = np.ldexp(np.abs(x.astype(np.float64)).ravel(), -lsb_exp)
+    del x
+    fl = np.floor(a)
+    up = np.ldexp(y, -lsb_exp) - fl
+    r = np.floor(256.0 * (a - fl)).astype(np.int64)
+    live = (E > 0) & (fl < 2 ** m - 1)  # not saturated
+    assert np.all((up[live] == 0) | (up[live] == 1))
+    assert np.all(up[live & (r == 0)] == 0)
+    n_r = np.bincount(r[live], minlength=256)[1:]
+    ups = np.bincount(r[live], weights=up[live], minlength=256)[1:]
+    p = np.arange(1, 256) / 256.0
+    keep = n_r > 0
+    x2 = float((((ups - n_r * p) ** 2) / (n_r * p * (1 - p)))[keep].sum())
+    assert stats.chi2.sf(x2, int(keep.sum())) > 1e-7, "chi2 = %.1f over %d bins" % (x2, int(keep.sum()))
+    # and no bias overall
+    z = float((ups - n_r * p).sum() / np.sqrt((n_r * p * (1 - p)).sum()))
+    assert abs(z) < 5.0
+
+
+def test_stochastic_noise_independent_on_gpu():
+    """Every value sits exactly half an LSB above a grid point (r = 128), so it
+    rounds up exactly when its noise byte is at least 128: the round-up bits
+    are the noise bytes' top bits.  They must be balanced, and independent
+    between positions of a group (the same Philox word, neighbouring words,
+    the two 16-value blocks of a group of 32), between neighbouring groups
+    and between seeds (2 x 2 chi-square)."""
+    from scipy import stats
+    rng = np.random.default_rng(4)
+    R, C = 4096, 512
+    m = 4
+    # magnitudes k + 1/2 for k in 0..14 with one value of each group at 14.5,
+    # which fixes the shared exponent at 130 (LSB = 1)
+    k = rng.integers(0, 15, (R, C)).astype(np.float64)
+    k[:, ::32] = 14
+    x = ((k + 0.5) * rng.choice([-1.0, 1.0], (R, C))).astype(np.float32)
+    bits = {}
+    for seed in (1234, 1235):
+        announce("SR noise top bits on the GPU, seed %d" % seed)
+        t = fb.quantize(torch.from_numpy(x).cuda(), g=32, m=m, rounding="stochastic", seed=seed)
+        assert np.all(t.exp.cpu().numpy() == 130)
+        y = np.abs(fb.dequantize(t).cpu().numpy().astype(np.float64))
+        bits[seed] = (y - np.floor(np.abs(x.astype(np.float64)))).astype(np.int64).reshape(-1, 32)
+    u = bits[1234]
+    assert set(np.unique(u)) <= {0, 1}
+    n = u.size
+    assert abs(int(u.sum()) - n / 2) < 6 * np.sqrt(n / 4)
+
+    def indep(a, b):
+        tab = np.bincount(2 * a + b, minlength=4).reshape(2, 2)
+        return stats.chi2_contingency(tab, correction=False)[1]
+
+    for p, q in [(0, 1), (0, 4), (2, 6), (3, 4), (0, 16), (5, 21), (15, 16)]:
+        assert indep(u[:, p], u[:, q]) > 1e-7, (p, q)
+    assert indep(u[:-1, 7].ravel(), u[1:, 7].ravel()) > 1e-7
+    assert indep(u.ravel(), bits[1235].ravel()) > 1e-7
