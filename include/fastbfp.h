@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define FASTBFP_ABI_VERSION 4
+#define FASTBFP_ABI_VERSION 5
 
 typedef enum {
   BFP_ROUND_NEAREST = 0,    /* add half an LSB, then truncate (ties away from zero) */
@@ -283,6 +283,35 @@ int bfp_weight_update(const float* w, const float* dw, float alpha, float* w_out
 int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode, uint64_t seed,
                           uint8_t* mant4, uint8_t* mant2, uint8_t* exp, double* sums, uint32_t* status_word,
                           void* stream);
+
+/*
+ * bfp_quantize_adaptive_noalloc -- bfp_quantize_adaptive for callers that
+ * cannot allocate device memory or pass a workspace (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * outputs, computed by the same kernels, but the per-workgroup partial sums
+ * live in a device array inside the library (2 MiB per GPU, reserved when the
+ * library is loaded and held until the process ends) instead of in sums[2..].
+ * The call allocates nothing.
+ *   sums        : device doubles, at least 2 (8-byte aligned): sums[0] and
+ *                 sums[1] as bfp_quantize_adaptive.
+ *   The rest    : as bfp_quantize_adaptive.
+ * Limit: bfp_adaptive_parts(R, C, group_axis, g) <=
+ * bfp_adaptive_noalloc_max_parts() (131072: 2^26 groups along rows, e.g.
+ * 2^30 values at g = 16); larger shapes return BFP_E_UNSUPPORTED.
+ * Every call on one GPU uses that GPU's one array: calls that overlap on the
+ * same GPU (different streams, or threads) race and give wrong sums; the
+ * caller must order them.  Each call writes every partial it reads, so no
+ * state carries over between calls.
+ */
+int bfp_quantize_adaptive_noalloc(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode,
+                                  uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exp, double* sums,
+                                  uint32_t* status_word, void* stream);
+
+/* The number of per-workgroup partial pairs the adaptive converter produces
+ * for this shape (-1 if group_axis or g is invalid), and the most that
+ * bfp_quantize_adaptive_noalloc can hold. */
+int64_t bfp_adaptive_parts(int64_t R, int64_t C, int group_axis, int g);
+int64_t bfp_adaptive_noalloc_max_parts(void);
 
 /*
  * bfp_adaptive_sums_len -- the number of doubles bfp_quantize_adaptive needs

@@ -22,7 +22,7 @@ import torch
 from ._lib import BFPError, check, load
 
 __all__ = ["BFPTensor", "BFPError", "quantize", "quantize_dual", "weight_update", "dequantize", "gemm", "gemm_bfp",
-           "gemm_group_partials", "quantize_adaptive", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING"]
+           "gemm_group_partials", "quantize_adaptive", "quantize_adaptive_noalloc", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING"]
 
 ROUNDING = {"nearest": 0, "stochastic": 1, "truncate": 2}
 
@@ -234,6 +234,40 @@ def quantize_adaptive(x: torch.Tensor, group_axis: int = -1, g: int = 16, roundi
                                     ctypes.c_void_p(t4.exp.data_ptr()), ctypes.c_void_p(work.data_ptr()), st_ptr,
                                     _stream(x.device)), "bfp_quantize_adaptive")
     return t4, t2, sums
+
+
+def quantize_adaptive_noalloc(x: torch.Tensor, t4: BFPTensor, sums: torch.Tensor, group_axis: int = -1,
+                              rounding: str = "nearest", seed: int = 0, t2: BFPTensor | None = None,
+                              status: torch.Tensor | None = None):
+    """quantize_adaptive into caller-provided outputs, with no allocation
+    anywhere (bfp_quantize_adaptive_noalloc: the library's device scratch
+    array holds the partial sums): t4 = BFP(X, 4), optional t2 (mantissas of
+    BFP(X, 2), sharing t4.exp), sums a float64 CUDA tensor of at least 2."""
+    _need_cuda(x, "x", torch.float32)
+    _need_cuda(sums, "sums", torch.float64)
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    nd = x.dim()
+    ax = group_axis % nd
+    if ax == nd - 1:
+        C = x.shape[-1]
+        R = math.prod(x.shape[:-1])
+        axis_flag, rows, length = 1, R, C
+    elif nd == 2 and ax == 0:
+        R, C = x.shape
+        axis_flag, rows, length = 0, C, R
+    else:
+        raise ValueError("group_axis must be the last axis, or 0 of a 2-D tensor")
+    if (t4.rows, t4.len, t4.m) != (rows, length, 4) or (t2 is not None and (t2.rows, t2.len, t2.m) != (rows, length, 2)):
+        raise ValueError("t4 / t2 have the wrong shape or format")
+    if sums.numel() < 2:
+        raise ValueError("sums needs 2 doubles")
+    check(load().bfp_quantize_adaptive_noalloc(ctypes.c_void_p(x.data_ptr()), R, C, axis_flag, t4.g, ROUNDING[rounding],
+                                               ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF),
+                                               ctypes.c_void_p(t4.mant.data_ptr()),
+                                               ctypes.c_void_p(t2.mant.data_ptr()) if t2 is not None else None,
+                                               ctypes.c_void_p(t4.exp.data_ptr()), ctypes.c_void_p(sums.data_ptr()),
+                                               _status_ptr(status), _stream(x.device)), "bfp_quantize_adaptive_noalloc")
 
 
 def adaptive_threshold(alpha: float, beta: float, i: int, I: int, l: int, L: int) -> float:

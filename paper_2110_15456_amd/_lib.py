@@ -34,10 +34,13 @@ SIGNATURES = {
                                _P]),
     "bfp_quantize_adaptive": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _P, _P, _P, _P, _P, _P]),
     "bfp_adaptive_sums_len": (_I64, [_I64, _I64, _I, _I]),
+    "bfp_quantize_adaptive_noalloc": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _P, _P, _P, _P, _P, _P]),
+    "bfp_adaptive_parts": (_I64, [_I64, _I64, _I, _I]),
+    "bfp_adaptive_noalloc_max_parts": (_I64, []),
     "bfp_adaptive_threshold": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, _I64, _I64, _I64, _I64]),
     "bfp_adaptive_mantissa": (_I, [ctypes.c_double, ctypes.c_double, ctypes.c_double]),
 }
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 _lock = threading.Lock()
 _lib = None

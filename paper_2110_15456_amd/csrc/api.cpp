@@ -218,6 +218,35 @@ int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, 
                                                      status_word, static_cast<hipStream_t>(stream)));
 }
 
+int bfp_quantize_adaptive_noalloc(const float* x, int64_t R, int64_t C, int group_axis, int g, int round_mode,
+                                  uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exp, double* sums,
+                                  uint32_t* status_word, void* stream) {
+  if (group_axis != 0 && group_axis != 1) return BFP_E_ARG;
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  const int64_t rows = group_axis == 1 ? R : C, len = group_axis == 1 ? C : R;
+  const int st = check_tensor(rows, len, g, 4);
+  if (st != BFP_OK) return st;
+  if (!sums || !aligned(sums, 8)) return BFP_E_ARG;
+  if (2 * fastbfp::adaptive_parts(R, C, group_axis, g) > fastbfp::kAdaptiveScratchDoubles) return BFP_E_UNSUPPORTED;
+  if (R != 0 && C != 0) {
+    if (!x || !mant4 || !exp) return BFP_E_ARG;
+    if (!aligned(x, group_axis == 1 ? 16 : 4) || !aligned(mant4, 4) || !aligned(mant2, 4) ||
+        !aligned(status_word, 4))
+      return BFP_E_ARG;
+  }
+  return status_of(fastbfp::launch_quantize_adaptive_static(x, R, C, group_axis, g, round_mode, seed, mant4, mant2,
+                                                            exp, sums, status_word,
+                                                            static_cast<hipStream_t>(stream)));
+}
+
+int64_t bfp_adaptive_noalloc_max_parts(void) { return fastbfp::kAdaptiveScratchDoubles / 2; }
+
+int64_t bfp_adaptive_parts(int64_t R, int64_t C, int group_axis, int g) {
+  if ((group_axis != 0 && group_axis != 1) || (g != 16 && g != 32) || R < 0 || C < 0) return -1;
+  if ((group_axis == 1 ? C : R) % g != 0) return -1;
+  return fastbfp::adaptive_parts(R, C, group_axis, g);
+}
+
 int64_t bfp_adaptive_sums_len(int64_t R, int64_t C, int group_axis, int g) {
   if ((group_axis != 0 && group_axis != 1) || (g != 16 && g != 32) || R < 0 || C < 0) return -1;
   if ((group_axis == 1 ? C : R) % g != 0) return -1;

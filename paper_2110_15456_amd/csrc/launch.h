@@ -32,6 +32,16 @@ int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g);
 hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
                                     uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
                                     uint32_t* status, hipStream_t s);
+// Capacity, in doubles, of the device scratch array that holds the partial
+// pairs of the allocation-free adaptive converter (2 MiB per GPU).
+constexpr int64_t kAdaptiveScratchDoubles = int64_t(1) << 18;
+// launch_quantize_adaptive without a caller workspace: sums holds the two
+// result doubles only; the partials use the library's device scratch array
+// (the caller checks 2 * adaptive_parts(...) <= kAdaptiveScratchDoubles).
+// Calls that overlap on one GPU share that array and race.
+hipError_t launch_quantize_adaptive_static(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
+                                           uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps,
+                                           double* sums, uint32_t* status, hipStream_t s);
 // Both groupings (g = 16) of x[R][C] from one read: mr/er along rows (seed_r),
 // mc/ec along columns (seed_c), in the layout of quantize.
 hipError_t launch_quantize_dual(const float* x, int64_t R, int64_t C, int m, int mode, uint64_t seed_r,

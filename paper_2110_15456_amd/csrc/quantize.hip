@@ -10,6 +10,8 @@
 // otherwise, 3G/4 bytes) plus one exponent byte.  Owning a whole
 // group per lane makes one Philox call serve 16 values, which keeps stochastic
 // rounding within the HBM-bound budget.
+#include <mutex>
+
 #include "bfp_quant.h"
 
 namespace fastbfp {
@@ -45,14 +47,14 @@ __device__ __forceinline__ void block_improvement(double num, double den, double
   }
 }
 
-// sums[0..1] = the sums of the nparts partial pairs at sums + 2, in a fixed
-// order (one block): the result does not depend on scheduling.
-__global__ __launch_bounds__(256) void k_improvement_finalize(double* sums, int64_t nparts) {
+// out[0..1] = the sums of the nparts partial pairs at part, in a fixed order
+// (one block): the result does not depend on scheduling.
+__global__ __launch_bounds__(256) void k_improvement_finalize(double* out, const double* part, int64_t nparts) {
   __shared__ double red[2][256];
   double num = 0.0, den = 0.0;
   for (int64_t i = threadIdx.x; i < nparts; i += 256) {
-    num += sums[2 + 2 * i];
-    den += sums[3 + 2 * i];
+    num += part[2 * i];
+    den += part[2 * i + 1];
   }
   red[0][threadIdx.x] = num;
   red[1][threadIdx.x] = den;
@@ -65,8 +67,8 @@ __global__ __launch_bounds__(256) void k_improvement_finalize(double* sums, int6
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    sums[0] = red[0][0];
-    sums[1] = red[1][0];
+    out[0] = red[0][0];
+    out[1] = red[1][0];
   }
 }
 
@@ -85,7 +87,7 @@ template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1>
 __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__ x, int64_t ngroups, uint32_t m,
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
                                                        uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
-                                                       uint32_t* status, double* sums) {
+                                                       uint32_t* status, double* part) {
   constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane
   constexpr int CPG = G / 4;                         // 16-byte chunks per group
   constexpr int CPL = GPL * CPG;                     // 16-byte chunks per lane
@@ -149,7 +151,7 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
         num += ldexp((double)s_lo[gi], (int)E[gi] - 130);
         den += ldexp((double)s_hi[gi], (int)E[gi] - 128);
       }
-    block_improvement(num, den, sums + 2);
+    block_improvement(num, den, part);
   }
 }
 
@@ -164,7 +166,7 @@ template <int G, int MODE, int NCH, int NGT, bool ADAPT, bool F0, bool F1>
 __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__ x, int64_t R, int64_t C,
                                                        int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
                                                        uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1,
-                                                       uint8_t* __restrict__ exps, uint32_t* status, double* sums) {
+                                                       uint8_t* __restrict__ exps, uint32_t* status, double* part) {
   constexpr int JB = 4 * NGT;             // group rows per block
   constexpr int WPG = G * 6 / 32;         // code dwords per group of an FP6 plane (an FP4 plane: G / 8)
   constexpr int WP[2] = {F0 ? G / 8 : WPG, F1 ? G / 8 : WPG};  // code dwords per group of each plane
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       any_bad |= nonfinite;
     }
   }
-  if (ADAPT) block_improvement(num, den, sums + 2);
+  if (ADAPT) block_improvement(num, den, part);
   __syncthreads();
   // Write-out: output row c0 + r gets jn groups starting at group jb.
   const int ncols = (int)min((int64_t)64, C - c0);
@@ -268,22 +270,22 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
 
 template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
 static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
-                                uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
+                                uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
   constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane (as in the kernel)
   const int64_t blocks = (ngroups + 256 * GPL - 1) / (256 * GPL);
   hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, F0, F1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
-                     (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
+                     (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
   return hipGetLastError();
 }
 
 template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
 static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant0,
-                                uint8_t* mant1, uint8_t* exps, uint32_t* status, double* sums, hipStream_t s) {
+                                uint8_t* mant1, uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
   constexpr int NGT = 8;
   const int64_t gpr = R / G;
   const int64_t nbx = (C + 63) / 64, nby = (gpr + 4 * NGT - 1) / (4 * NGT);
   hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, F0, F1>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
-                     C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, sums);
+                     C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
   return hipGetLastError();
 }
 
@@ -354,27 +356,69 @@ int64_t adaptive_parts(int64_t R, int64_t C, int group_axis, int g) {
 }
 
 static hipError_t launch_adaptive_kernel(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
-                                         uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
+                                         uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* part,
                                          uint32_t* status, hipStream_t s) {
   const int m = 4;
   const bool two = mant2 != nullptr;  // second output plane: the 2-bit mantissas
   if (group_axis == 1) {
     const int64_t ngroups = R * (C / g);
-    FASTBFP_DISPATCH_ADAPT(launch_rows_t, x, ngroups, m, seed, mant4, mant2, exps, status, sums, s);
+    FASTBFP_DISPATCH_ADAPT(launch_rows_t, x, ngroups, m, seed, mant4, mant2, exps, status, part, s);
   }
-  FASTBFP_DISPATCH_ADAPT(launch_cols_t, x, R, C, m, seed, mant4, mant2, exps, status, sums, s);
+  FASTBFP_DISPATCH_ADAPT(launch_cols_t, x, R, C, m, seed, mant4, mant2, exps, status, part, s);
+}
+
+// part: the per-workgroup partial pairs (2 * adaptive_parts doubles); out:
+// the two sums.
+static hipError_t launch_adaptive_parts(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
+                                        uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* out,
+                                        double* part, uint32_t* status, hipStream_t s) {
+  const int64_t nparts = adaptive_parts(R, C, group_axis, g);
+  if (nparts > 0) {
+    const hipError_t e = launch_adaptive_kernel(x, R, C, group_axis, g, mode, seed, mant4, mant2, exps, part, status, s);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_improvement_finalize, dim3(1), dim3(256), 0, s, out, part, nparts);
+  return hipGetLastError();
 }
 
 hipError_t launch_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
                                     uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps, double* sums,
                                     uint32_t* status, hipStream_t s) {
-  const int64_t nparts = adaptive_parts(R, C, group_axis, g);
-  if (nparts > 0) {
-    const hipError_t e = launch_adaptive_kernel(x, R, C, group_axis, g, mode, seed, mant4, mant2, exps, sums, status, s);
+  return launch_adaptive_parts(x, R, C, group_axis, g, mode, seed, mant4, mant2, exps, sums, sums + 2, status, s);
+}
+
+// The allocation-free variant: the partial pairs go to a file-scope device
+// array (one copy per GPU, kept until the process ends) instead of a caller
+// workspace.  Its address is looked up once per device, with that device
+// current; host code uses only that address, never the array's name.
+static __device__ __align__(256) double scratch[kAdaptiveScratchDoubles];
+
+static hipError_t scratch_address(double** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static double* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
     if (e != hipSuccess) return e;
+    addr[dev] = static_cast<double*>(p);
   }
-  hipLaunchKernelGGL(k_improvement_finalize, dim3(1), dim3(256), 0, s, sums, nparts);
-  return hipGetLastError();
+  *ptr = addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_quantize_adaptive_static(const float* x, int64_t R, int64_t C, int group_axis, int g, int mode,
+                                           uint64_t seed, uint8_t* mant4, uint8_t* mant2, uint8_t* exps,
+                                           double* sums, uint32_t* status, hipStream_t s) {
+  double* part = nullptr;
+  const hipError_t e = scratch_address(&part);
+  if (e != hipSuccess) return e;
+  return launch_adaptive_parts(x, R, C, group_axis, g, mode, seed, mant4, mant2, exps, sums, part, status, s);
 }
 
 // Both groupings of a matrix from one read (and, with UPD, the weight update
