@@ -25,10 +25,11 @@ int check_tensor(int64_t rows, int64_t len, int g, int m) {
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 // Planes the GEMM reads for an operand stored at m_stored and used at m_use:
-// every stored plane, or only the high plane when the low chunk is dropped.
+// every stored plane, or only the high plane when the low chunk (2 bits for
+// m = 5, 6; 4 for m = 7, 8) is dropped.
 int planes_used(int m_stored, int m_use) {
   if (m_use == m_stored) return m_stored > 4 ? 2 : 1;
-  if (m_stored > 4 && m_use == m_stored - 4) return 1;
+  if (m_stored > 4 && m_use == m_stored - fastbfp::low_chunk_bits(m_stored)) return 1;
   return 0;
 }
 

@@ -46,6 +46,29 @@ __device__ __forceinline__ int e2m3_half_decode(uint32_t code) {
   return (code & 0x20u) ? -(int)c : (int)c;
 }
 
+// A Lo2 chunk plane (a 2-bit chunk c with its sign, per value) holds, per 16
+// values, the three dwords T0, T1, T2 of their packed FP6 E2M3 codes of
+// +-c/8.  Such a code is subnormal: of its 6 bits only the two mantissa bits
+// of the value (field bits 0, 1) and the sign (bit 5) can be set.  Across the
+// 96 bits, T1's possible bits moved down by one fall exactly on T0's
+// always-zero bits, so the 16 codes fit in two dwords:
+//   D0 = T0 | (T1 >> 1),  D1 = T2
+// and come back with three instructions.  kLo2M0 / kLo2M1 are the bits T0 /
+// T1 can have set (T2's are D1 as stored).
+constexpr uint32_t kLo2M0 = 0xE38E38E3u, kLo2M1 = 0x38E38E38u;
+__device__ __forceinline__ uint2 lo2_pack(uint32_t t0, uint32_t t1, uint32_t t2) {
+  return make_uint2(t0 | (t1 >> 1), t2);
+}
+__device__ __forceinline__ void lo2_unpack(uint32_t d0, uint32_t d1, uint32_t& t0, uint32_t& t1, uint32_t& t2) {
+  t0 = d0 & kLo2M0;
+  t1 = (d0 << 1) & kLo2M1;
+  t2 = d1;
+}
+// +-c for a 6-bit FP6 E2M3 code of +-c/8 (c <= 7: a subnormal code).
+__device__ __forceinline__ int e2m3_eighth_decode(uint32_t code) {
+  return (code & 0x20u) ? -(int)(code & 7u) : (int)(code & 7u);
+}
+
 // 6-bit field t of a packed little-endian FP6 group held in dwords w[].
 __device__ __forceinline__ uint32_t fp6_field(const uint32_t* w, int t) {
   const int bit = 6 * t, wi = bit >> 5, sh = bit & 31;

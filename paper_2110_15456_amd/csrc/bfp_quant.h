@@ -63,24 +63,27 @@ __device__ __forceinline__ v6u_t cvt_fp6_x32(v16f_t a, v16f_t b) {
 // Subnormal inputs are read as zero: explicitly, or (FTZ true, only for
 // files built with FP32 denormals flushed) by the ldexp's own input flush.
 //
-// Plane formats: F0 / F1 true makes plane 0 / 1 an FP4 E2M1 plane (chunks of
-// at most 2 bits: the code is the sign bit above the chunk itself, 4 bits per
-// value, G/8 words); otherwise an FP6 E2M3 plane (3G/16 words), whose codes
-// come from the gfx950 FP6 converter.  That converter interleaves its two
-// 16-value inputs: output value 2i is a[i] / scale and 2i+1 is b[i] / scale.
+// Plane formats P0 / P1 (launch.h): kPlaneFP4 (chunks of at most 2 bits: the
+// code is the sign bit above the chunk itself, 4 bits per value, G/8 words);
+// kPlaneFP6 (3G/16 words) and kPlaneLo2 (G/8 words: the FP6 codes of
+// +-chunk/8, squeezed by lo2_pack), whose codes come from the gfx950 FP6
+// converter.  That converter interleaves its two 16-value inputs: output
+// value 2i is a[i] / scale and 2i+1 is b[i] / scale.  Two chunk planes split
+// q at 2 bits when plane 1 is a Lo2 plane (q >> 2, q & 3: m = 5, 6) and at 4
+// otherwise (q >> 4, q & 15: m = 7, 8).
 //
 // ADAPT (m = 4 only; section V-D and Eq. 2): plane 0 gets the 4-bit magnitude
 // q as one code, plane 1 (if NCH = 2) the 2-bit mantissa left when the low
 // chunk is discarded, q >> 2; s_lo and s_hi return the group's sums of q & 3
 // and q >> 2 (the magnitudes BFP(X,4) - BFP(X,2) and BFP(X,2) in units of
 // 2^(E-130) and 2^(E-128)).
-template <int G, int NG, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ>
+template <int G, int NG, int MODE, int NCH, bool ADAPT, int P0, int P1, bool FTZ>
 __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uint32_t m, uint64_t gid, uint32_t key0,
                                                 uint32_t key1, uint32_t (&w)[NCH][NG * G * 6 / 32],
                                                 uint32_t (&E_out)[NG], bool& nonfinite, uint32_t (&s_lo)[NG],
                                                 uint32_t (&s_hi)[NG]) {
   static_assert(NG == 1 || G == 16, "several groups per call: 16-value groups");
-  constexpr bool FP4[2] = {F0, F1};
+  constexpr int PK[2] = {P0, P1};
   constexpr int LEN = NG * G;  // values converted together (one packing unit)
 #pragma unroll
   for (int gi = 0; gi < NG; ++gi) {
@@ -163,6 +166,9 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
     } else if (NCH == 1) {
       c[0] = q;
       c[1] = 0u;
+    } else if (P1 == kPlaneLo2) {
+      c[0] = q >> 2;
+      c[1] = q & 3u;
     } else {
       c[0] = q >> 4;
       c[1] = q & 15u;
@@ -172,10 +178,11 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
     const int h = t / 32, k = (t % 32) / 2;
 #pragma unroll
     for (int p = 0; p < NCH; ++p) {
-      if (FP4[p]) {
+      if (PK[p] == kPlaneFP4) {
         w[p][t >> 3] |= (c[p] ? (sgn | c[p]) : 0u) << (4 * (t & 7));
       } else {
-        const float f = signed_half(c[p], nh);
+        // +-c/2, or +-c/8 for a Lo2 plane (exact either way; zero as +0)
+        const float f = signed_half(c[p], PK[p] == kPlaneLo2 ? 0.25f * nh : nh);
         if (t % 2 == 0) ev[p][h][k] = f; else od[p][h][k] = f;
       }
     }
@@ -183,42 +190,53 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
   typedef uint32_t v6u __attribute__((ext_vector_type(6)));
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
-    if (FP4[p]) continue;
+    if (PK[p] == kPlaneFP4) continue;
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
       const v6u cv = cvt_fp6_x32(ev[p][h], od[p][h]);
 #pragma unroll
       for (int i = 0; i < 6 && 6 * h + i < LEN * 6 / 32; ++i) w[p][6 * h + i] = cv[i];
     }
+    if (PK[p] == kPlaneLo2) {
+      // squeeze each 16 values' three code dwords into two (in order: the
+      // dwords written never come after those still to be read)
+#pragma unroll
+      for (int u = 0; u < LEN / 16; ++u) {
+        const uint2 d = lo2_pack(w[p][3 * u], w[p][3 * u + 1], w[p][3 * u + 2]);
+        w[p][2 * u] = d.x;
+        w[p][2 * u + 1] = d.y;
+      }
+    }
   }
 }
 
 
 // One group (the common case).
-template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1, bool FTZ = false>
+template <int G, int MODE, int NCH, bool ADAPT, int P0, int P1, bool FTZ = false>
 __device__ __forceinline__ void quantize_group(const uint32_t (&b)[G], uint32_t m, uint64_t gid, uint32_t key0,
                                                uint32_t key1, uint32_t (&w)[NCH][G * 6 / 32], uint32_t& E_out,
                                                bool& nonfinite, uint32_t& s_lo, uint32_t& s_hi) {
   uint32_t E[1], lo[1], hi[1];
-  quantize_groups<G, 1, MODE, NCH, ADAPT, F0, F1, FTZ>(b, m, gid, key0, key1, w, E, nonfinite, lo, hi);
+  quantize_groups<G, 1, MODE, NCH, ADAPT, P0, P1, FTZ>(b, m, gid, key0, key1, w, E, nonfinite, lo, hi);
   E_out = E[0];
   s_lo = lo[0];
   s_hi = hi[0];
 }
 
 // Stores plane p's codes of group gid (from quantize_group) at
-// mant_p + gid * bytes-per-group: 8 or 12 bytes per 16 values.
+// mant_p + gid * bytes-per-group: 8 (FOUR: an FP4 or Lo2 plane) or 12 bytes
+// per 16 values.
 template <class T, bool STREAM>
 __device__ __forceinline__ void put(T* p, T v) {
   if constexpr (STREAM) stream_store(p, v);
   else *p = v;
 }
 // STREAM: nt stores (for a wave that writes whole contiguous lines).
-template <int G, bool FP4, bool STREAM = false>
+template <int G, bool FOUR, bool STREAM = false>
 __device__ __forceinline__ void store_plane(uint8_t* __restrict__ mant, int64_t gid, const uint32_t* w) {
   typedef uint32_t u2 __attribute__((ext_vector_type(2)));
   typedef uint32_t u3 __attribute__((ext_vector_type(3)));
-  if (FP4) {
+  if (FOUR) {
     u2* dst = reinterpret_cast<u2*>(mant + gid * (G / 2));
 #pragma unroll
     for (int i = 0; i < G / 16; ++i) put<u2, STREAM>(dst + i, u2{w[2 * i], w[2 * i + 1]});

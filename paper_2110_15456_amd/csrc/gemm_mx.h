@@ -2,10 +2,11 @@
 // (section III-B dot product; fMAC of section V-B): the kernel template and
 // its launcher, instantiated per operand format in gemm_mx_{11,12,21,22}.hip.
 //
-// C[M][N] = A[M][K] * B[N][K]^T, both operands BFP with groups of 16 along K,
-// stored as chunk planes (value +-chunk/2 as an FP6 E2M3 code, 12 bytes per
-// group, or as an FP4 E2M1 code for chunks of at most 2 bits, 8 bytes per
-// group) and one exponent byte per group.
+// C[M][N] = A[M][K] * B[N][K]^T, both operands BFP with groups of 16 (or 32)
+// along K, stored as chunk planes (layout of include/fastbfp.h: FP4 or FP6
+// codes of +-q/2 for m <= 4; for m = 5, 6 an FP6 plane of q >> 2 and a Lo2
+// plane of q & 3; for m = 7, 8 FP6 planes of q >> 4 and q & 15) and one
+// exponent byte per group.
 //
 // What the fMAC does per group pair -- g integer products, an adder tree, one
 // exponent addition, conversion to FP and an FP32 accumulation -- is what one
@@ -13,42 +14,39 @@
 // products of chunks are exact, the block sum is scaled by 2^(sa-127) *
 // 2^(sb-127) with the shared exponents as the E8M0 block scales, and the
 // result is added to an FP32 accumulator.  The hardware block is 32 values
-// and a BFP group is 16, so each lane's block carries one active group per
-// operand, arranged so that it meets the other operand's active group and
-// everything else meets zeros (FP6 and FP4 have no NaN or Inf encodings).
-// One instruction thus covers 4 groups of K, one per lane block; the operand
-// formats of A and B are chosen per instruction.
+// and a BFP group 16: with one chunk plane per operand a lane's block carries
+// one active group per operand, arranged so that it meets the other
+// operand's active group and everything else meets zeros (FP6 and FP4 have
+// no NaN or Inf encodings).  One instruction thus covers 4 groups of K, one
+// per lane block; the operand formats of A and B are chosen per instruction.
 //
-// Variable precision (section V-B): an m-bit magnitude is one 4-bit chunk when
-// m <= 4 and two when m > 4; each chunk-plane pair (ca, cb) is one pass of
-// MFMAs over the group with the chunk's scale raised by 4 per chunk of
-// significance (the paper lowers the exponent of the lower chunk instead; both
-// give the same weights).  Passes per group pair = chunks(m_a) * chunks(m_b).
-// The one remaining constant factor, 2^(4 - m_a - m_b) (the halving of both
-// operands' codes and the (m-1) in the LSB), is applied exactly in the
-// epilogue.
+// Variable precision (section V-B): chunk planes are passes over the group
+// with the chunk's weight on the scale byte.  An operand split at 2 bits
+// (m = 5, 6) fills a whole block with one group: +-(q >> 2)/2 in one half and
+// +-(q & 3)/8 in the other, i.e. q/8, against the other operand's group
+// repeated in both halves -- one MFMA per chunk plane of the other operand
+// and no zero half.  The one remaining constant factor, 2^(4 - m_a - m_b)
+// (the halving of both operands' codes and the (m-1) in the LSB), is applied
+// exactly in the epilogue.
 //
 // Staging: a K slab is 8 groups.  In an FP6 plane each group occupies a
 // 16-byte LDS slot filled by a direct buffer->LDS 12-byte load, which leaves
-// the slot's last dword untouched (zeroed once); in an FP4 plane each slot
-// holds a group pair (2p, 2p + 1), filled by one 16-byte load.  Lane block lb
-// of K-step ks works on group 2 lb + ks, so an FP4 lane reads one slot for
-// both K-steps.  Slot order within a row is XOR-swizzled by the row so that
-// the 16-byte fragment reads of 16 rows hit all 64 banks, while each load
-// instruction still reads whole runs of consecutive rows.  With full slabs of
-// groups of 16, the exponents of two slabs come in one 16-byte load per row
-// into a buffer of their own.  Slabs are double
-// buffered in two LDS objects: the loads of slab s+1 are issued right after
-// the barrier that publishes slab s and have all of slab s's MFMAs to land.
-// Every load instruction costs the MFMA waves that issue it time (the load
-// path takes about 31 cycles per instruction per CU, whatever the width, and
-// the issuing wave stalls behind it), so the kernel issues no load it does not
-// need (an L2 prefetch of slab s+2 cost more than it saved), spreads a slab's
-// loads between blocks of MFMAs, and where the registers allow (256x128 tiles
-// of FP4 + FP6 operands) hands them to a fifth wave that only issues loads.  A
-// 256-thread workgroup (2x2 MFMA waves) computes a 256x256 tile (128 along an
-// operand with two chunk planes); tiles are ordered so that neighbours share
-// panels in L2 on the same XCD.
+// the slot's last dword untouched (zeroed once); in an FP4 or Lo2 plane each
+// slot holds a group pair (2p, 2p + 1), filled by one 16-byte load.  Lane
+// block lb of K-step ks works on group 2 lb + ks, so such a lane reads one
+// slot for both K-steps.  Slot order within a row is XOR-swizzled by the row
+// so that the 16-byte fragment reads of 16 rows hit all 64 banks, while each
+// load instruction still reads whole runs of consecutive rows.  With full
+// slabs of groups of 16, the exponents of two slabs come in one 16-byte load
+// per row into a buffer of their own.  Slabs are double buffered in two LDS
+// objects: the loads of slab s+1 are issued right after the barrier that
+// publishes slab s and have all of slab s's MFMAs to land.  Every load
+// instruction costs the MFMA waves that issue it time, so the kernel issues
+// no load it does not need (an L2 prefetch of slab s+2 cost more than it
+// saved) and spreads a slab's loads between blocks of MFMAs.  A 256-thread
+// workgroup (2x2 MFMA waves) computes a 256x256 tile (128 along an operand
+// with two chunk planes, except 256 along A when both are split at 2 bits);
+// tiles are ordered so that neighbours share panels in L2 on the same XCD.
 #pragma once
 #include "bfp_quant.h"
 
@@ -70,9 +68,6 @@ namespace mx {
 #ifndef FASTBFP_MX_X3
 #define FASTBFP_MX_X3 1  // one MFMA for both cross products of two-chunk operands
 #endif
-#ifndef FASTBFP_MX_PROD
-#define FASTBFP_MX_PROD 1  // a fifth wave issues the direct loads of the two-chunk kernels
-#endif
 #ifndef FASTBFP_MX_PIPE2
 #define FASTBFP_MX_PIPE2 1
 #endif
@@ -86,8 +81,11 @@ namespace mx {
 #define FASTBFP_MX11_BN FASTBFP_MX_BN
 #endif
 constexpr int KG = 8;            // groups per K slab (two MFMA K-steps)
-// NA / NB: chunk planes of A / B read; FA / FB: 1 if plane 0 of A / B holds
-// FP4 codes (plane 1 always holds FP6 codes).
+// NA / NB: chunk planes of A / B read.  FA / FB: with one plane read, 1 if it
+// holds FP4 codes (else FP6); with two, 1 if the operand is split at 2 bits
+// (m = 5, 6: plane 0 FP6 codes of q >> 2, plane 1 a Lo2 plane of q & 3), 0 if
+// at 4 (m = 7, 8: two FP6 planes).  FP4 and Lo2 planes take 8 bytes per
+// group of 16 and are staged alike (16-byte LDS slots of group pairs).
 // G: the operands' group size, 16 or 32.  A slab is 8 groups of 16 (KG) or
 // 4 of 32: the mantissa planes of a g = 32 tensor are laid out exactly like
 // those of a g = 16 tensor with twice the groups (each group is its two
@@ -106,12 +104,13 @@ struct Cfg {
   static constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
   static constexpr int TM = WM / 16, TN = WN / 16;    // 16x16 MFMA tiles per wave
   // LDS bytes per row of a slab: 8 slots of one group (FP6) or 4 slots of a
-  // group pair (FP4), 16 bytes each.
-  static constexpr int RA0 = FA ? 64 : 128, RB0 = FB ? 64 : 128;
+  // group pair (FP4, Lo2), 16 bytes each.
+  static constexpr int RA0 = (NA == 1 && FA) ? 64 : 128, RB0 = (NB == 1 && FB) ? 64 : 128;
+  static constexpr int RA1 = FA ? 64 : 128, RB1 = FB ? 64 : 128;  // plane 1 (two planes read)
   static constexpr int OFF_A1 = BM * RA0;                        // A's plane 1
-  static constexpr int OFF_B = OFF_A1 + (NA == 2 ? BM * 128 : 0);
+  static constexpr int OFF_B = OFF_A1 + (NA == 2 ? BM * RA1 : 0);
   static constexpr int OFF_B1 = OFF_B + BN * RB0;                // B's plane 1
-  static constexpr int OFF_EA = OFF_B1 + (NB == 2 ? BN * 128 : 0);
+  static constexpr int OFF_EA = OFF_B1 + (NB == 2 ? BN * RB1 : 0);
   static constexpr int OFF_EB = OFF_EA + BM * EK;
   static constexpr int SPARE = OFF_EB + BN * EK;  // EK bytes written by threads without an exponent row
   static constexpr int STAGE = SPARE + 16;
@@ -125,24 +124,32 @@ struct Cfg {
   static_assert((BN / 16) % NW == 0 && (BM / 16) % NW == 0, "plane loads split evenly over the waves");
   static_assert(2 * STAGE <= 160 * 1024, "two stages fit in LDS");
 };
-// LDS offset of plane p of A / B within a stage, and its format.
+// LDS offset of plane p of A / B within a stage, and its format: a_fp4 /
+// b_fp4 (FP4 codes, read by the MFMA as FP4), a_lo2 / b_lo2 (a Lo2 plane,
+// unpacked to FP6 codes), a_four / b_four (either: 8 bytes per group, staged
+// in group-pair slots).
 template <class CF> __device__ constexpr int a_plane(int p) { return p ? CF::OFF_A1 : 0; }
 template <class CF> __device__ constexpr int b_plane(int p) { return p ? CF::OFF_B1 : CF::OFF_B; }
-template <class CF> __device__ constexpr int a_fp4(int p) { return p == 0 && CF::FA; }
-template <class CF> __device__ constexpr int b_fp4(int p) { return p == 0 && CF::FB; }
-// Load-issuing wave: with both operands in an FP4 and an FP6 chunk plane
-// (256x128 tiles, at most 256 registers per wave, so a fifth wave fits beside
-// the four MFMA waves), full slabs of groups of 16 and FP32 output, one extra
-// wave issues every direct load and the four MFMA waves issue none.  (The
-// kernels with fewer MFMAs per load -- one chunk plane on a side, or FP6
-// upper planes with 128x128 tiles -- were 5-12% slower this way: one wave
-// issuing all of a slab's loads then sets the pace.)
-template <class CF, bool EXP_FULL, int QNCH>
-constexpr bool producer() {
-  return FASTBFP_MX_PROD && EXP_FULL && CF::G == 16 && QNCH == 0 && CF::NA == 2 && CF::NB == 2 && CF::FA && CF::FB;
+template <class CF> __device__ constexpr int a_fp4(int p) { return p == 0 && CF::NA == 1 && CF::FA; }
+template <class CF> __device__ constexpr int b_fp4(int p) { return p == 0 && CF::NB == 1 && CF::FB; }
+template <class CF> __device__ constexpr int a_lo2(int p) { return p == 1 && CF::NA == 2 && CF::FA; }
+template <class CF> __device__ constexpr int b_lo2(int p) { return p == 1 && CF::NB == 2 && CF::FB; }
+template <class CF> __device__ constexpr int a_four(int p) { return a_fp4<CF>(p) || a_lo2<CF>(p); }
+template <class CF> __device__ constexpr int b_four(int p) { return b_fp4<CF>(p) || b_lo2<CF>(p); }
+template <class CF> __device__ constexpr int a_kind(int p) {
+  return a_fp4<CF>(p) ? kPlaneFP4 : a_lo2<CF>(p) ? kPlaneLo2 : kPlaneFP6;
 }
-template <class CF, bool EXP_FULL, int QNCH>
-constexpr int threads() { return producer<CF, EXP_FULL, QNCH>() ? CF::NT + 64 : CF::NT; }
+template <class CF> __device__ constexpr int b_kind(int p) {
+  return b_fp4<CF>(p) ? kPlaneFP4 : b_lo2<CF>(p) ? kPlaneLo2 : kPlaneFP6;
+}
+// Scale-byte offset of chunk plane p of an operand, relative to one FP6 or
+// FP4 plane of codes of +-q/2 (the unit the epilogue's 2^(4 - m_a - m_b)
+// assumes): split at 4 bits, the upper plane +-(q >> 4)/2 weighs 2^4 and the
+// lower one 2^0; split at 2 bits, the upper plane +-(q >> 2)/2 weighs 2^2 and
+// the lower one, unpacked to +-(q & 3)/8, 2^2 as well.
+template <int NP, int SPLIT2> __device__ constexpr int plane_weight(int p) {
+  return NP == 1 ? 0 : SPLIT2 ? 2 : (p == 0 ? 4 : 0);
+}
 }  // namespace mx
 
 // Calls f(ic<0>{}), ..., f(ic<N-1>{}): a loop whose index is a constant
@@ -401,12 +408,12 @@ struct OutBFP {
   uint8_t* exps;
   uint32_t* status;
   int m, mode;
-  int hi4;  // plane 0 holds FP4 codes
+  int four;  // one plane: it holds FP4 codes (m <= 2); two planes: plane 1 is a Lo2 plane (m = 5, 6)
   uint32_t key0, key1;
 };
 
 template <class CF, bool EXP_FULL, int QNCH>
-__global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
+__global__ __launch_bounds__(CF::NT) void k_gemm_mx(const uint8_t* __restrict__ a_mant, const uint8_t* __restrict__ a_exp,
                                                  int64_t a_plane_stride, const uint8_t* __restrict__ b_mant,
                                                  const uint8_t* __restrict__ b_exp, int64_t b_plane_stride, int M,
                                                  int N, int ng, float scale, float* __restrict__ C, int64_t ldc,
@@ -419,10 +426,11 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   // strips).  Otherwise each stage holds its slab's exponents.
   constexpr bool XP = EXP_FULL && CF::G == 16;
   constexpr bool X3 = FASTBFP_MX_X3 && NA == 2 && NB == 2 && CF::G == 16 && !CF::PIPE && !FA && !FB;
-  constexpr bool PROD = mx::producer<CF, EXP_FULL, QNCH>();
-  // explicit pipeline of the two-chunk loop
-  constexpr bool PIPE2 = FASTBFP_MX_PIPE2 && (NA == 2 || NB == 2) && CF::G == 16 && !X3;
-  constexpr int NTHR = mx::threads<CF, EXP_FULL, QNCH>();
+  // an operand split at 2 bits fills whole MFMA blocks (groups of 16)
+  constexpr bool COMB = CF::G == 16 && ((NA == 2 && FA) || (NB == 2 && FB));
+  // explicit pipeline of the two-chunk loop (operands split at 4 bits)
+  constexpr bool PIPE2 = FASTBFP_MX_PIPE2 && (NA == 2 || NB == 2) && CF::G == 16 && !X3 && !COMB;
+  constexpr int NTHR = CF::NT;
   constexpr int STRIP_BYTES = QNCH ? CF::NW * 16 * (CF::WN + 4) * 4 : 0;
   constexpr int SB = XP ? (CF::OFF_EA > STRIP_BYTES ? CF::OFF_EA : STRIP_BYTES) : CF::STAGE;
   constexpr int XEB = XP ? (CF::BM + CF::BN) * 16 : 16;
@@ -475,12 +483,12 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   rsrc_t ra[NA], rb[NB];
 #pragma unroll
   for (int p = 0; p < NA; ++p) {
-    const uint32_t r = rbytes(mx::a_fp4<CF>(p));
+    const uint32_t r = rbytes(mx::a_four<CF>(p));
     ra[p] = make_rsrc(a_mant + p * a_plane_stride + (int64_t)row0 * r, (uint32_t)a_rows * r);
   }
 #pragma unroll
   for (int p = 0; p < NB; ++p) {
-    const uint32_t r = rbytes(mx::b_fp4<CF>(p));
+    const uint32_t r = rbytes(mx::b_four<CF>(p));
     rb[p] = make_rsrc(b_mant + p * b_plane_stride + (int64_t)col0 * r, (uint32_t)b_rows * r);
   }
   // FP6: lane -> (row lane / 8 of the instruction's 8, slot lane % 8), loading
@@ -515,17 +523,17 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   // order (the register exponent loads of the ragged path go with part 0).
   // XP: the exponent loads are those of a slab pair, issued only where xe
   // (their destination) is given.
-  constexpr int LA0 = plane_loads<CF::NW, CF::BM>(mx::a_fp4<CF>(0)), LA1 = NA == 2 ? plane_loads<CF::NW, CF::BM>(false) : 0;
-  constexpr int LB0 = plane_loads<CF::NW, CF::BN>(mx::b_fp4<CF>(0)), LB1 = NB == 2 ? plane_loads<CF::NW, CF::BN>(false) : 0;
+  constexpr int LA0 = plane_loads<CF::NW, CF::BM>(mx::a_four<CF>(0));
+  constexpr int LA1 = NA == 2 ? plane_loads<CF::NW, CF::BM>(mx::a_four<CF>(1)) : 0;
+  constexpr int LB0 = plane_loads<CF::NW, CF::BN>(mx::b_four<CF>(0));
+  constexpr int LB1 = NB == 2 ? plane_loads<CF::NW, CF::BN>(mx::b_four<CF>(1)) : 0;
   constexpr int LEA = XP ? pair_loads<CF::NW, CF::BM>() : EXP_FULL ? exps_loads<CF::NW, CF::BM, CF::EK>() : 0;
   constexpr int LEB = XP ? pair_loads<CF::NW, CF::BN>() : EXP_FULL ? exps_loads<CF::NW, CF::BN, CF::EK>() : 0;
   constexpr int OFS[6] = {0, LA0, LA0 + LA1, LA0 + LA1 + LB0, LA0 + LA1 + LB0 + LB1, LA0 + LA1 + LB0 + LB1 + LEA};
   constexpr int NLOAD = OFS[5] + LEB;
-  // vw: the wave whose share of the instructions is issued (the calling wave,
-  // or each of the four in turn for the load-issuing wave).
   auto issue = [&](uint8_t* stage, int slab, bool live, uint2 (&e)[CF::EXP_ROWS_PER_T], uint8_t* xe, int part = 0,
-                   int nparts = 1, int vw = -1) {
-    if (vw < 0) vw = wave;
+                   int nparts = 1) {
+    const int vw = wave;
     const int g_lane = (lane & 7) ^ ((4 * (vw & 1) + (lane >> 4)) & 7);
     const uint32_t m_lane_off = (uint32_t)(lane >> 3) * rb6 + (uint32_t)g_lane * 12u;
     const int lo = part * NLOAD / nparts, hi = (part + 1) * NLOAD / nparts;
@@ -547,7 +555,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     const bool p_ok = slab * mx::KG + 2 * p_lane < ng;
 #pragma unroll
     for (int p = 0; p < NA; ++p) {
-      if (mx::a_fp4<CF>(p))
+      if (mx::a_four<CF>(p))
         load_plane4<CF::NW, CF::BM, !EXP_FULL>(stage + mx::a_plane<CF>(p), live ? ra[p] : rnull, m4_lane_off, rb4, slab, p_ok,
                                        vw, u0(p), u1(p));
       else
@@ -556,7 +564,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     }
 #pragma unroll
     for (int p = 0; p < NB; ++p) {
-      if (mx::b_fp4<CF>(p))
+      if (mx::b_four<CF>(p))
         load_plane4<CF::NW, CF::BN, !EXP_FULL>(stage + mx::b_plane<CF>(p), live ? rb[p] : rnull, m4_lane_off, rb4, slab, p_ok,
                                        vw, u0(2 + p), u1(2 + p));
       else
@@ -592,30 +600,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
   };
 
   uint2 e_regs[CF::EXP_ROWS_PER_T];
-  if constexpr (PROD) {
-    if (wave == CF::NW) {
-      // The load-issuing wave: slab 0, then after the barrier that publishes
-      // slab s the loads of slab s + 1 into the other stage (every MFMA wave
-      // has passed that barrier, so is done with slab s - 1 there), and the
-      // exponents of a slab pair with its even slab into xe[pair % 2] (which
-      // held pair - 2).  It passes the same barriers as the MFMA waves (one
-      // per slab), each after waiting for all of its loads.
-      auto issue_all = [&](uint8_t* stage, int slab, uint8_t* xe) {
-#pragma unroll
-        for (int v = 0; v < CF::NW; ++v) issue(stage, slab, true, e_regs, xe, 0, 1, v);
-      };
-      if (nslabs > 0) issue_all(stage0, 0, xe0);
-      for (int s = 0; s < nslabs; ++s) {
-        __builtin_amdgcn_s_waitcnt(0);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        const int t = s + 1;
-        if (t < nslabs) issue_all((t & 1) ? stage1 : stage0, t, (t & 1) ? nullptr : ((t >> 1) & 1) ? xe1 : xe0);
-      }
-      return;
-    }
-  } else if (nslabs > 0) {
+  if (nslabs > 0) {
     issue(stage0, 0, true, e_regs, XP ? xe0 : nullptr);
     put_exps(stage0, e_regs);
   }
@@ -656,12 +641,12 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     auto issue_after = [&](int b, int nblk) {
 #pragma unroll
       for (int k = 0; k < NPART; ++k)
-        if (!PROD && NPART > 1 && k * (nblk / 2) / NPART == b) {
+        if (NPART > 1 && k * (nblk / 2) / NPART == b) {
           issue(nxt, nslab, more, e_regs, xnext, k, NPART);
           __builtin_amdgcn_sched_barrier(0);
         }
     };
-    if constexpr (NPART == 1 && !PROD) issue(nxt, nslab, more, e_regs, xnext);
+    if constexpr (NPART == 1) issue(nxt, nslab, more, e_regs, xnext);
     __builtin_amdgcn_sched_barrier(0);
     // Fragment addresses.  Row rl = wr*WM + 16*i + lr has the FP6 swizzle
     // ((rl >> 1) & 7) = ((lr >> 1) & 7) and the FP4 swizzle ((rl >> 2) & 3) =
@@ -688,10 +673,17 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     };
     auto rd = [&](int off) { return *reinterpret_cast<const u32x4*>(cur + off); };
     // G = 32: the operand is the whole group, with no padding -- the FP4 slot
-    // as read, or the 12 bytes of each of the two FP6 half-group slots.
-    auto op32 = [&](int fp4, int plane_off, int r, int t) -> v8i {
-      const u32x4 x = rd(slot_addr(plane_off, fp4, r, t, 0));
-      if (fp4) return v8i{(int)x[0], (int)x[1], (int)x[2], (int)x[3], 0, 0, 0, 0};
+    // as read, the 12 bytes of each of the two FP6 half-group slots, or a Lo2
+    // slot's two halves unpacked to FP6 codes.  kind: kPlaneFP6 / FP4 / Lo2.
+    auto op32 = [&](int kind, int plane_off, int r, int t) -> v8i {
+      const u32x4 x = rd(slot_addr(plane_off, kind != kPlaneFP6, r, t, 0));
+      if (kind == kPlaneFP4) return v8i{(int)x[0], (int)x[1], (int)x[2], (int)x[3], 0, 0, 0, 0};
+      if (kind == kPlaneLo2) {
+        uint32_t t0, t1, t2, u0, u1, u2;
+        lo2_unpack(x[0], x[1], t0, t1, t2);
+        lo2_unpack(x[2], x[3], u0, u1, u2);
+        return v8i{(int)t0, (int)t1, (int)t2, (int)u0, (int)u1, (int)u2, 0, 0};
+      }
       const u32x4 y = rd(slot_addr(plane_off, 0, r, t, 1));
       return v8i{(int)x[0], (int)x[1], (int)x[2], (int)y[0], (int)y[1], (int)y[2], 0, 0};
     };
@@ -747,21 +739,118 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
         int eb[TN];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          bv[j] = op32(fb, mx::b_plane<CF>(cb), b_r, j);
-          eb[j] = (int)xcur[eb_lane + j * 16 * ER] + 4 * (NB - 1 - cb);  // +4 per chunk of significance
+          bv[j] = op32(mx::b_kind<CF>(cb), mx::b_plane<CF>(cb), b_r, j);
+          eb[j] = (int)xcur[eb_lane + j * 16 * ER] + mx::plane_weight<NB, FB>(cb);  // the chunk's weight
         }
         static_for<NA>([&](auto cac) {
           constexpr int ca = decltype(cac)::value, fa = mx::a_fp4<CF>(ca);
 #pragma unroll
           for (int i = 0; i < TM; ++i) {
-            const v8i av = op32(fa, mx::a_plane<CF>(ca), a_r, i);
-            const int ea = (int)xcur[ea_lane + i * 16 * ER] + 4 * (NA - 1 - ca);
+            const v8i av = op32(mx::a_kind<CF>(ca), mx::a_plane<CF>(ca), a_r, i);
+            const int ea = (int)xcur[ea_lane + i * 16 * ER] + mx::plane_weight<NA, FA>(ca);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
               mma<fa, fb>(acc[i][j], av, bv[j], ea, eb[j]);
             issue_after((cb * NA + ca) * TM + i, NB * NA * TM);
           }
         });
+      });
+    } else if constexpr (COMB) {
+      // An operand split at 2 bits (q = 4 (q >> 2) + (q & 3)) fills a whole
+      // 32-value MFMA block with one group of 16: the codes of +-(q >> 2)/2
+      // (its FP6 plane) in half 0 and those of +-(q & 3)/8 (its Lo2 plane,
+      // unpacked) in half 1, i.e. q/8 per value.  The other operand's group
+      // is repeated in both halves, one block per chunk plane of it.  So a
+      // fragment pair takes one MFMA per chunk plane of the repeated operand
+      // and no block holds zeros: (6,6) 2 MFMAs per group of 16 where
+      // separate chunk passes over half-empty blocks take 4, (6, m <= 4) 1
+      // where they take 2.  The combined operand C is A when A is split at 2
+      // bits, else B; D is the other.  The scale bytes carry the chunk
+      // weights: 2 for the combined block (q/8 against the unit q/2) plus the
+      // repeated plane's.
+      //
+      // Software pipeline: a block is one C fragment (K-step ks, fragment c)
+      // against every D fragment and plane (TD * ND MFMAs).  Each block first
+      // reads the next block's C slots (a Lo2 slot holds both K-steps' groups
+      // and is read once), and the blocks of K-step 0 read a share of K-step
+      // 1's D slots; D's repeated operands are built from the raw slots at
+      // the start of each K-step; a scheduling barrier closes each block.
+      constexpr bool CA = NA == 2 && FA;
+      constexpr int TC = CA ? TM : TN, TD = CA ? TN : TM, ND = CA ? NB : NA;
+      constexpr int C0 = CA ? mx::a_plane<CF>(0) : mx::b_plane<CF>(0);  // FP6 plane of q >> 2
+      constexpr int C1 = CA ? mx::a_plane<CF>(1) : mx::b_plane<CF>(1);  // Lo2 plane of q & 3
+      constexpr int DP0 = CA ? mx::b_plane<CF>(0) : mx::a_plane<CF>(0);
+      constexpr int DP1 = CA ? mx::b_plane<CF>(1) : mx::a_plane<CF>(1);
+      constexpr int DK0 = CA ? mx::b_kind<CF>(0) : mx::a_kind<CF>(0);
+      constexpr int DK1 = CA ? mx::b_kind<CF>(1) : mx::a_kind<CF>(1);
+      constexpr int FD = CA ? FB : FA;
+      const int c_r = CA ? a_r : b_r, d_r = CA ? b_r : a_r;
+      const int c_e = CA ? ea_lane : eb_lane, d_e = CA ? eb_lane : ea_lane;
+      u32x4 dr[2][ND][TD];  // D's raw slots per K-step (an FP4 / Lo2 slot only in [0])
+      int de[2][TD];
+      v8i dd[ND][TD];       // D's repeated operands of the current K-step
+      u32x4 ch[2], cl[TC];  // C's FP6 slots (per block) and Lo2 slots (per fragment)
+      int ce[2];
+      auto read_d = [&](int ks, int t) {
+        static_for<ND>([&](auto pc) {
+          constexpr int p = decltype(pc)::value, k = p == 0 ? DK0 : DK1, off = p == 0 ? DP0 : DP1;
+          if (k == kPlaneFP6 || ks == 0) dr[k == kPlaneFP6 ? ks : 0][p][t] = rd(slot_addr(off, k != kPlaneFP6, d_r, t, ks));
+        });
+        de[ks][t] = (int)xcur[d_e + t * 16 * ER + ks];
+      };
+      auto read_c = [&](int blk) {
+        const int ks = blk / TC, c = blk % TC;
+        ch[blk & 1] = rd(slot_addr(C0, 0, c_r, c, ks));
+        if (ks == 0) cl[c] = rd(slot_addr(C1, 1, c_r, c, 0));
+        ce[blk & 1] = (int)xcur[c_e + c * 16 * ER + ks];
+      };
+      // the group repeated in both halves, from a raw slot of a plane of kind k
+      auto make_dup = [&](int k, const u32x4& x, int ks) -> v8i {
+        if (k == kPlaneFP6) return v8i{(int)x[0], (int)x[1], (int)x[2], (int)x[0], (int)x[1], (int)x[2], 0, 0};
+        if (k == kPlaneFP4)
+          return v8i{(int)x[2 * ks], (int)x[2 * ks + 1], (int)x[2 * ks], (int)x[2 * ks + 1], 0, 0, 0, 0};
+        uint32_t t0, t1, t2;
+        lo2_unpack(x[2 * ks], x[2 * ks + 1], t0, t1, t2);
+        return v8i{(int)t0, (int)t1, (int)t2, (int)t0, (int)t1, (int)t2, 0, 0};
+      };
+#pragma unroll
+      for (int t = 0; t < TD; ++t) read_d(0, t);
+      read_c(0);
+      static_for<2 * TC>([&](auto bc) {
+        constexpr int blk = decltype(bc)::value, ks = blk / TC, c = blk % TC;
+        if constexpr (c == 0) {
+#pragma unroll
+          for (int t = 0; t < TD; ++t)
+            static_for<ND>([&](auto pc) {
+              constexpr int p = decltype(pc)::value, k = p == 0 ? DK0 : DK1;
+              dd[p][t] = make_dup(k, dr[k == kPlaneFP6 ? ks : 0][p][t], ks);
+            });
+        }
+        if constexpr (blk + 1 < 2 * TC) read_c(blk + 1);
+        if constexpr (ks == 0) {
+#pragma unroll
+          for (int t = c * TD / TC; t < (c + 1) * TD / TC; ++t) read_d(1, t);
+        }
+        uint32_t t0, t1, t2;
+        lo2_unpack(cl[c][2 * ks], cl[c][2 * ks + 1], t0, t1, t2);
+        const u32x4& h = ch[blk & 1];
+        const v8i cv = v8i{(int)h[0], (int)h[1], (int)h[2], (int)t0, (int)t1, (int)t2, 0, 0};
+        const int e_c = ce[blk & 1];
+        // plane-major: consecutive MFMAs accumulate into different tiles
+        static_for<ND>([&](auto pc) {
+          constexpr int p = decltype(pc)::value;
+          constexpr int W = 2 + mx::plane_weight<ND, FD>(p);
+          constexpr int dfp4 = (p == 0 ? DK0 : DK1) == kPlaneFP4;
+#pragma unroll
+          for (int t = 0; t < TD; ++t) {
+            if constexpr (CA)
+              mma<0, dfp4>(acc[c][t], cv, dd[p][t], e_c + (W + 1) / 2, de[ks][t] + W / 2);
+            else
+              mma<dfp4, 0>(acc[t][c], dd[p][t], cv, de[ks][t] + (W + 1) / 2, e_c + W / 2);
+          }
+        });
+        issue_after(blk, 2 * TC);
+        __builtin_amdgcn_sched_barrier(0);
       });
     } else if constexpr (PIPE2) {
       // Software pipeline of the two-chunk kernels (an operand in two chunk
@@ -772,7 +861,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
       // exponent byte, which serves every plane), and the blocks of K-step 0
       // also read a share of K-step 1's B fragments, so that every LDS read
       // has a block of MFMAs to land in; the next slab's load parts go
-      // between blocks (none with the load-issuing wave), and a scheduling
+      // between blocks, and a scheduling
       // barrier closes each block.  A B plane of FP4 slots holds the group
       // pairs of both K-steps and is read once.
       constexpr int BPK = NA * TM;   // blocks per K-step
@@ -951,25 +1040,27 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
     float* strip = reinterpret_cast<float*>(stage0) + wave * (16 * SROW);
     const int ngN = N / 16;
     bool bad = false;
-    // Convert and store one group: F0 = plane 0 holds FP4 codes.
+    // Convert and store one group: FOUR as OutBFP::four.
     auto convert = [&](auto f0c, const uint32_t (&b)[16], int64_t gid) {
-      constexpr bool F0 = decltype(f0c)::value;
+      constexpr bool FOUR = decltype(f0c)::value;
+      constexpr int P0 = (QNCH == 1 && FOUR) ? kPlaneFP4 : kPlaneFP6;
+      constexpr int P1 = (QNCH == 2 && FOUR) ? kPlaneLo2 : kPlaneFP6;
       uint32_t w[QNCH][16 * 6 / 32];
       uint32_t E, s_lo, s_hi;
       bool nonfinite;
       const uint32_t m = (uint32_t)qo.m;
       if (qo.mode == kStochastic)
-        quantize_group<16, kStochastic, QNCH, false, F0, false>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+        quantize_group<16, kStochastic, QNCH, false, P0, P1>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
                                                                 s_lo, s_hi);
       else if (qo.mode == kNearest)
-        quantize_group<16, kNearest, QNCH, false, F0, false>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+        quantize_group<16, kNearest, QNCH, false, P0, P1>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
                                                              s_lo, s_hi);
       else
-        quantize_group<16, kTruncate, QNCH, false, F0, false>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
+        quantize_group<16, kTruncate, QNCH, false, P0, P1>(b, m, (uint64_t)gid, qo.key0, qo.key1, w, E, nonfinite,
                                                               s_lo, s_hi);
       qo.exps[gid] = (uint8_t)E;
-      store_plane<16, F0>(qo.mant0, gid, w[0]);
-      if (QNCH == 2) store_plane<16, false>(qo.mant1, gid, w[QNCH - 1]);
+      store_plane<16, P0 != kPlaneFP6>(qo.mant0, gid, w[0]);
+      if (QNCH == 2) store_plane<16, P1 != kPlaneFP6>(qo.mant1, gid, w[QNCH - 1]);
       bad |= nonfinite;
     };
     // The strips, with the output format fixed outside the loop (one copy of
@@ -1002,7 +1093,7 @@ __global__ __launch_bounds__((mx::threads<CF, EXP_FULL, QNCH>())) void k_gemm_mx
       __builtin_amdgcn_wave_barrier();
     }
     };
-    if (qo.hi4) strips(ic<1>{});
+    if (qo.four) strips(ic<1>{});
     else strips(ic<0>{});
     if (qo.status && bad) atomicOr(qo.status, 1u);
   }
@@ -1015,7 +1106,7 @@ static hipError_t launch_mx_v(const uint8_t* a_mant, const uint8_t* a_exp, int64
   const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
   const dim3 grid((unsigned)(tiles_m * tiles_n)), block(CF::NT);
   if (!qo)
-    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, dim3(mx::threads<CF, EXP_FULL, 0>()), 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
+    hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 0>), grid, dim3(CF::NT), 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
                        ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
   else if (qo->m > 4)
     hipLaunchKernelGGL((k_gemm_mx<CF, EXP_FULL, 2>), grid, block, 0, s, a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N,
@@ -1061,10 +1152,10 @@ hipError_t launch_mx_11_tile(const uint8_t* a_mant, const uint8_t* a_exp, const 
   const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
   const dim3 grid((unsigned)(tiles_m * tiles_n));
   if (ef)
-    hipLaunchKernelGGL((k_gemm_mx<CF, true, 0>), grid, dim3(mx::threads<CF, true, 0>()), 0, s, a_mant, a_exp,
+    hipLaunchKernelGGL((k_gemm_mx<CF, true, 0>), grid, dim3(CF::NT), 0, s, a_mant, a_exp,
                        (int64_t)0, b_mant, b_exp, (int64_t)0, M, N, ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
   else
-    hipLaunchKernelGGL((k_gemm_mx<CF, false, 0>), grid, dim3(mx::threads<CF, false, 0>()), 0, s, a_mant, a_exp,
+    hipLaunchKernelGGL((k_gemm_mx<CF, false, 0>), grid, dim3(CF::NT), 0, s, a_mant, a_exp,
                        (int64_t)0, b_mant, b_exp, (int64_t)0, M, N, ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
   return hipGetLastError();
 }

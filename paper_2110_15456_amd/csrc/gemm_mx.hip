@@ -100,7 +100,8 @@ static hipError_t launch_gemm_g(const uint8_t* a_mant, const uint8_t* a_exp, int
   if (M == 0 || N == 0) return hipSuccess;
   const int ng = (int)(K / 16);  // 16-value halves per row (the plane layout's unit)
   const int64_t a_ps = M * (K / G) * plane_group_bytes(G, a_m, 0), b_ps = N * (K / G) * plane_group_bytes(G, b_m, 0);
-  const int fa = plane0_fp4(a_m), fb = plane0_fp4(b_m);
+  // the kernels' FA / FB: one plane read, FP4 codes; two, split at 2 bits
+  const int fa = na == 1 ? plane0_fp4(a_m) : a_m <= 6, fb = nb == 1 ? plane0_fp4(b_m) : b_m <= 6;
   const float scale = ldexpf(1.0f, scale_log2);
   const int m = (int)M, n = (int)N;
   if (G == 16 && na == 1 && nb == 1 && !qo) {
@@ -141,8 +142,8 @@ hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a
                               const uint8_t* b_exp, int b_m, int nb, int64_t M, int64_t N, int64_t K, int g,
                               int scale_log2, int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp,
                               uint32_t* status, hipStream_t s) {
-  const OutBFP qo{c_mant,     c_mant + M * (N / 16) * plane_group_bytes(16, c_m, 0), c_exp, status, c_m, mode,
-                  plane0_fp4(c_m), (uint32_t)seed, (uint32_t)(seed >> 32)};
+  const OutBFP qo{c_mant, c_mant + M * (N / 16) * plane_group_bytes(16, c_m, 0), c_exp, status, c_m, mode,
+                  c_m <= 4 ? plane0_fp4(c_m) : c_m <= 6, (uint32_t)seed, (uint32_t)(seed >> 32)};
   return launch_gemm_any(a_mant, a_exp, a_m, na, b_mant, b_exp, b_m, nb, M, N, K, g, scale_log2, nullptr, N, &qo, 0, s);
 }
 

@@ -10,13 +10,29 @@ namespace fastbfp {
 // Rounding modes, numerically equal to bfp_round_t.
 enum { kNearest = 0, kStochastic = 1, kTruncate = 2 };
 
-// Chunk-plane formats of an m-bit tensor (the layout of include/fastbfp.h):
-// plane 0 holds FP4 E2M1 codes when its chunk has at most 2 bits (m = 1, 2, 5,
-// 6) and FP6 E2M3 codes otherwise; plane 1 (m >= 5) always holds FP6 codes.
-__host__ __device__ constexpr bool plane0_fp4(int m) { return m <= 2 || m == 5 || m == 6; }
+// Chunk-plane formats of an m-bit tensor (the layout of include/fastbfp.h).
+// A plane holds one chunk of every value, with the value's sign, in one of
+// three encodings:
+//   kPlaneFP6: FP6 E2M3 codes of +-chunk/2 (chunks up to 15; 12 bytes per 16
+//              values);
+//   kPlaneFP4: FP4 E2M1 codes of +-chunk/2 (chunks up to 3; 8 bytes);
+//   kPlaneLo2: a 2-bit chunk as the FP6 E2M3 codes of +-chunk/8 (subnormal
+//              codes: only the sign and the two low bits of a field can be
+//              set), with the zero bits squeezed out (8 bytes, see lo2_pack).
+// m = 1, 2: one FP4 plane (q).  m = 3, 4: one FP6 plane (q).  m = 5, 6: an FP6
+// plane of q >> 2 and a Lo2 plane of q & 3.  m = 7, 8: FP6 planes of q >> 4 and
+// q & 15.
+enum { kPlaneFP6 = 0, kPlaneFP4 = 1, kPlaneLo2 = 2 };
+__host__ __device__ constexpr int plane_kind(int m, int p) {
+  return p == 0 ? (m <= 2 ? kPlaneFP4 : kPlaneFP6) : (m <= 6 ? kPlaneLo2 : kPlaneFP6);
+}
+__host__ __device__ constexpr bool plane0_fp4(int m) { return m <= 2; }
+// Bits of the lower chunk of a two-chunk magnitude (the upper chunk's weight
+// is 2^low_chunk_bits): 2 for m = 5, 6; 4 for m = 7, 8.
+__host__ __device__ constexpr int low_chunk_bits(int m) { return m <= 6 ? 2 : 4; }
 // Bytes per group of g values in plane p.
 __host__ __device__ constexpr int plane_group_bytes(int g, int m, int p) {
-  return (p == 0 && plane0_fp4(m)) ? g / 2 : 3 * g / 4;
+  return plane_kind(m, p) == kPlaneFP6 ? 3 * g / 4 : g / 2;
 }
 
 hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,

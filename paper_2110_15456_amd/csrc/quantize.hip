@@ -18,11 +18,11 @@ namespace fastbfp {
 
 // Plane p of the group goes to mant_p (plane 1 of a two-chunk tensor, or the
 // separate 2-bit tensor of the adaptive path).
-template <int G, int NCH, bool F0, bool F1, bool STREAM = false>
+template <int G, int NCH, int P0, int P1, bool STREAM = false>
 __device__ __forceinline__ void store_group(uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1, int64_t gid,
                                             const uint32_t (&w)[NCH][G * 6 / 32]) {
-  store_plane<G, F0, STREAM>(mant0, gid, w[0]);
-  if (NCH == 2) store_plane<G, F1, STREAM>(mant1, gid, w[NCH - 1]);
+  store_plane<G, P0 != kPlaneFP6, STREAM>(mant0, gid, w[0]);
+  if (NCH == 2) store_plane<G, P1 != kPlaneFP6, STREAM>(mant1, gid, w[NCH - 1]);
 }
 
 // Writes the block's Eq. 2 partial sums to part[2 * blockIdx.x + {0, 1}]:
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void k_improvement_finalize(double* out, const
 // all 64 banks on the read-back.  (Reading 64 contiguous bytes per lane
 // straight from global memory instead leaves each load instruction touching
 // 64 scattered 16-byte pieces, which costs about a third of HBM bandwidth.)
-template <int G, int MODE, int NCH, bool ADAPT, bool F0, bool F1>
+template <int G, int MODE, int NCH, bool ADAPT, int P0, int P1>
 __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__ x, int64_t ngroups, uint32_t m,
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
                                                        uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
@@ -128,19 +128,19 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   uint32_t w[NCH][GPL * G * 6 / 32];
   uint32_t E[GPL], s_lo[GPL], s_hi[GPL];
   bool nonfinite;
-  quantize_groups<G, GPL, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo,
+  quantize_groups<G, GPL, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo,
                                                           s_hi);
   if (GPL == 2 && nmine == 2) {
     // both groups: one packing unit of 32 values (its bytes are the two
     // groups' bytes side by side) and two exponent bytes
     stream_store(reinterpret_cast<uint16_t*>(exps + gid), (uint16_t)(E[0] | (E[GPL - 1] << 8)));
-    store_group<GPL * G, NCH, F0, F1, true>(mant0, mant1, gid / GPL, w);
+    store_group<GPL * G, NCH, P0, P1, true>(mant0, mant1, gid / GPL, w);
     if (status && nonfinite) atomicOr(status, 1u);
   } else if (nmine > 0) {
     // one group (GPL = 1, or the last group of an odd count): its own bytes
     exps[gid] = (uint8_t)E[0];
-    store_plane<G, F0, true>(mant0, gid, w[0]);
-    if (NCH == 2) store_plane<G, F1, true>(mant1, gid, w[NCH - 1]);
+    store_plane<G, P0 != kPlaneFP6, true>(mant0, gid, w[0]);
+    if (NCH == 2) store_plane<G, P1 != kPlaneFP6, true>(mant1, gid, w[NCH - 1]);
     if (status && nonfinite) atomicOr(status, 1u);
   }
   if (ADAPT) {
@@ -162,14 +162,14 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
 // consecutive group rows (NGT per wave).  The packed codes and exponents of
 // the 64 x JB groups are gathered in LDS and then written row by row, so that
 // every store instruction writes contiguous bytes of one output row.
-template <int G, int MODE, int NCH, int NGT, bool ADAPT, bool F0, bool F1>
+template <int G, int MODE, int NCH, int NGT, bool ADAPT, int P0, int P1>
 __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__ x, int64_t R, int64_t C,
                                                        int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
                                                        uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1,
                                                        uint8_t* __restrict__ exps, uint32_t* status, double* part) {
   constexpr int JB = 4 * NGT;             // group rows per block
   constexpr int WPG = G * 6 / 32;         // code dwords per group of an FP6 plane (an FP4 plane: G / 8)
-  constexpr int WP[2] = {F0 ? G / 8 : WPG, F1 ? G / 8 : WPG};  // code dwords per group of each plane
+  constexpr int WP[2] = {P0 != kPlaneFP6 ? G / 8 : WPG, P1 != kPlaneFP6 ? G / 8 : WPG};  // code dwords per group
   constexpr int ROWW = JB * WPG;          // LDS row stride, code dwords per output row
   __shared__ uint32_t sc[NCH][64][ROWW];
   __shared__ uint8_t se[64][JB];
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       uint32_t w[NCH][WPG];
       uint32_t E, s_lo, s_hi;
       bool nonfinite;
-      quantize_group<G, MODE, NCH, ADAPT, F0, F1, true>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo,
+      quantize_group<G, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo,
                                                   s_hi);
       if (ADAPT) {
         num += ldexp((double)s_lo, (int)E - 130);
@@ -229,28 +229,42 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
   if (status && any_bad) atomicOr(status, 1u);
 }
 
-// BFP -> FP32: y = +-q * 2^(E-127-(m-1)).  One lane per group.  F0: plane 0
-// holds FP4 codes.
-template <int G, int NCH, bool F0>
+// BFP -> FP32: y = +-q * 2^(E-127-(m-1)).  One lane per group.  P0 / P1:
+// the plane formats (launch.h); with two planes q = c0 * 2^s + c1, s = 2 when
+// plane 1 is a Lo2 plane and 4 otherwise (both chunks carry the sign).
+template <int G, int NCH, int P0, int P1>
 __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ mant, const uint8_t* __restrict__ exps,
                                                     int64_t ngroups, int m, float* __restrict__ y) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= ngroups) return;
-  constexpr int B0 = F0 ? G / 2 : G * 3 / 4;  // bytes per group in plane 0
+  constexpr int PK[2] = {P0, P1};
+  constexpr int B0 = P0 != kPlaneFP6 ? G / 2 : G * 3 / 4;  // bytes per group in plane 0
   uint32_t w[NCH][G * 6 / 32];
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
-    const int gb = (p == 0 && F0) ? G / 2 : G * 3 / 4;
+    const int gb = PK[p] != kPlaneFP6 ? G / 2 : G * 3 / 4;
     const uint32_t* src = reinterpret_cast<const uint32_t*>(mant + p * ngroups * B0 + gid * gb);
 #pragma unroll
     for (int i = 0; i < G * 6 / 32; ++i) w[p][i] = i < gb / 4 ? src[i] : 0u;
+    if (PK[p] == kPlaneLo2) {
+      // back to three FP6 code dwords per 16 values (last half first: in place)
+#pragma unroll
+      for (int u = G / 16 - 1; u >= 0; --u) {
+        uint32_t t0, t1, t2;
+        lo2_unpack(w[p][2 * u], w[p][2 * u + 1], t0, t1, t2);
+        w[p][3 * u] = t0;
+        w[p][3 * u + 1] = t1;
+        w[p][3 * u + 2] = t2;
+      }
+    }
   }
   const int e = (int)exps[gid] - 127 - (m - 1);
   auto chunk = [&](int p, int t) {
-    if (p == 0 && F0) {
-      const uint32_t nib = (w[0][t >> 3] >> (4 * (t & 7))) & 0xFu;
+    if (PK[p] == kPlaneFP4) {
+      const uint32_t nib = (w[p][t >> 3] >> (4 * (t & 7))) & 0xFu;
       return (nib & 8u) ? -(int)(nib & 7u) : (int)(nib & 7u);
     }
+    if (PK[p] == kPlaneLo2) return e2m3_eighth_decode(fp6_field(w[p], t));
     return e2m3_half_decode(fp6_field(w[p], t));
   };
   float4* dst = reinterpret_cast<float4*>(y + gid * G);
@@ -261,41 +275,41 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
     for (int k = 0; k < 4; ++k) {
       const int t = 4 * i + k;
       int q = chunk(0, t);
-      if (NCH == 2) q = q * 16 + chunk(NCH - 1, t);  // both chunks carry the value's sign
+      if (NCH == 2) q = q * (P1 == kPlaneLo2 ? 4 : 16) + chunk(NCH - 1, t);
       v[k] = ldexpf((float)q, e);
     }
     dst[i] = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
-template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
+template <int G, int MODE, int NCH, int P0, bool ADAPT = false, int P1 = kPlaneFP6>
 static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
                                 uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
   constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane (as in the kernel)
   const int64_t blocks = (ngroups + 256 * GPL - 1) / (256 * GPL);
-  hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, F0, F1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
+  hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, P0, P1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
                      (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
   return hipGetLastError();
 }
 
-template <int G, int MODE, int NCH, bool F0, bool ADAPT = false, bool F1 = false>
+template <int G, int MODE, int NCH, int P0, bool ADAPT = false, int P1 = kPlaneFP6>
 static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant0,
                                 uint8_t* mant1, uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
   constexpr int NGT = 8;
   const int64_t gpr = R / G;
   const int64_t nbx = (C + 63) / 64, nby = (gpr + 4 * NGT - 1) / (4 * NGT);
-  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, F0, F1>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
+  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, P0, P1>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
                      C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
   return hipGetLastError();
 }
 
-// Specialisation for (g, rounding mode, m): planes and plane-0 format.
+// Specialisation for (g, rounding mode, m): planes and plane formats.
 #define FASTBFP_QUANT_M(FN, G, MODE, ...)                                         \
   do {                                                                            \
-    if (m <= 2) return FN<G, MODE, 1, true>(__VA_ARGS__);                         \
-    if (m <= 4) return FN<G, MODE, 1, false>(__VA_ARGS__);                        \
-    if (m <= 6) return FN<G, MODE, 2, true>(__VA_ARGS__);                         \
-    return FN<G, MODE, 2, false>(__VA_ARGS__);                                    \
+    if (m <= 2) return FN<G, MODE, 1, kPlaneFP4>(__VA_ARGS__);                    \
+    if (m <= 4) return FN<G, MODE, 1, kPlaneFP6>(__VA_ARGS__);                    \
+    if (m <= 6) return FN<G, MODE, 2, kPlaneFP6, false, kPlaneLo2>(__VA_ARGS__);  \
+    return FN<G, MODE, 2, kPlaneFP6>(__VA_ARGS__);                                \
   } while (0)
 #define FASTBFP_DISPATCH_QUANT(FN, ...)                                           \
   do {                                                                            \
@@ -329,8 +343,8 @@ hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int
 // two) the 2-bit tensor (FP4).
 #define FASTBFP_ADAPT_M(FN, G, MODE, ...)                                         \
   do {                                                                            \
-    if (two) return FN<G, MODE, 2, false, true, true>(__VA_ARGS__);               \
-    return FN<G, MODE, 1, false, true, true>(__VA_ARGS__);                        \
+    if (two) return FN<G, MODE, 2, kPlaneFP6, true, kPlaneFP4>(__VA_ARGS__);      \
+    return FN<G, MODE, 1, kPlaneFP6, true, kPlaneFP4>(__VA_ARGS__);               \
   } while (0)
 #define FASTBFP_DISPATCH_ADAPT(FN, ...)                                           \
   do {                                                                            \
@@ -440,7 +454,7 @@ hipError_t launch_quantize_adaptive_static(const float* x, int64_t R, int64_t C,
 // rows past R read zero (the buffer resource ends at the last row); columns
 // past C read whatever follows in memory, and only whole groups past C are
 // affected, which are never stored.
-template <int MODE, int NCH, bool F0, bool UPD>
+template <int MODE, int NCH, int P0, int P1, bool UPD>
 __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const float* dx, float alpha, float* x_out,
                                                        int64_t R, int64_t C, int tiles_c, uint32_t m, uint32_t kr0,
                                                        uint32_t kr1, uint32_t kc0, uint32_t kc1,
@@ -515,10 +529,10 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
     }
     if (r0 + row < R && c0 + 16 * cg < C) {
       const int64_t gid = (r0 + row) * (C / 16) + c0 / 16 + cg;
-      quantize_group<16, MODE, NCH, false, F0, false, true>(b, m, (uint64_t)gid, kr0, kr1, w, E, nonfinite, s_lo,
+      quantize_group<16, MODE, NCH, false, P0, P1, true>(b, m, (uint64_t)gid, kr0, kr1, w, E, nonfinite, s_lo,
                                                             s_hi);
       er[gid] = (uint8_t)E;
-      store_group<16, NCH, F0, false>(mr0, mr1, gid, w);
+      store_group<16, NCH, P0, P1>(mr0, mr1, gid, w);
       bad |= nonfinite;
     }
   }
@@ -531,24 +545,24 @@ __global__ __launch_bounds__(256) void k_quantize_dual(const float* x, const flo
       b[u] = __float_as_uint(tile[(16 * rg + u) * T + 4 * ((col >> 2) ^ swz(16 * rg + u)) + (col & 3)]);
     if (c0 + col < C && r0 + 16 * rg < R) {
       const int64_t gid = (c0 + col) * (R / 16) + r0 / 16 + rg;
-      quantize_group<16, MODE, NCH, false, F0, false, true>(b, m, (uint64_t)gid, kc0, kc1, w, E, nonfinite, s_lo,
+      quantize_group<16, MODE, NCH, false, P0, P1, true>(b, m, (uint64_t)gid, kc0, kc1, w, E, nonfinite, s_lo,
                                                             s_hi);
       ec[gid] = (uint8_t)E;
-      store_group<16, NCH, F0, false>(mc0, mc1, gid, w);
+      store_group<16, NCH, P0, P1>(mc0, mc1, gid, w);
       bad |= nonfinite;
     }
   }
   if (status && bad) atomicOr(status, 1u);
 }
 
-template <int MODE, int NCH, bool F0, bool UPD>
+template <int MODE, int NCH, int P0, int P1, bool UPD>
 static hipError_t launch_dual_t(const float* x, const float* dx, float alpha, float* x_out, int64_t R, int64_t C, int m,
                                 uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er, uint8_t* mc, uint8_t* ec,
                                 uint32_t* status, hipStream_t s) {
   const int64_t tiles_r = (R + 63) / 64, tiles_c = (C + 63) / 64;
   const int64_t ng = R * (C / 16);  // groups per output (either grouping)
   const int64_t b0 = plane_group_bytes(16, m, 0);
-  hipLaunchKernelGGL((k_quantize_dual<MODE, NCH, F0, UPD>), dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0, s, x,
+  hipLaunchKernelGGL((k_quantize_dual<MODE, NCH, P0, P1, UPD>), dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0, s, x,
                      dx, alpha, x_out, R, C, (int)tiles_c, (uint32_t)m, (uint32_t)seed_r, (uint32_t)(seed_r >> 32),
                      (uint32_t)seed_c, (uint32_t)(seed_c >> 32), mr, mr + ng * b0, er, mc, mc + ng * b0, ec, status);
   return hipGetLastError();
@@ -559,16 +573,16 @@ static hipError_t launch_dual_any(const float* x, const float* dx, float alpha, 
                                   int m, int mode, uint64_t seed_r, uint64_t seed_c, uint8_t* mr, uint8_t* er,
                                   uint8_t* mc, uint8_t* ec, uint32_t* status, hipStream_t s) {
   if (R == 0 || C == 0) return hipSuccess;
-#define FASTBFP_DUAL(MODE)                                                                                         \
-  do {                                                                                                             \
-    if (m <= 2) return launch_dual_t<MODE, 1, true, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, \
-                                                         ec, status, s);                                           \
-    if (m <= 4) return launch_dual_t<MODE, 1, false, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, \
-                                                          ec, status, s);                                          \
-    if (m <= 6) return launch_dual_t<MODE, 2, true, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, \
-                                                         ec, status, s);                                           \
-    return launch_dual_t<MODE, 2, false, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, mc, ec, status, \
-                                              s);                                                                  \
+#define FASTBFP_DUAL(MODE)                                                                                        \
+  do {                                                                                                            \
+    if (m <= 2) return launch_dual_t<MODE, 1, kPlaneFP4, kPlaneFP6, UPD>(x, dx, alpha, x_out, R, C, m, seed_r,    \
+                                                                         seed_c, mr, er, mc, ec, status, s);      \
+    if (m <= 4) return launch_dual_t<MODE, 1, kPlaneFP6, kPlaneFP6, UPD>(x, dx, alpha, x_out, R, C, m, seed_r,    \
+                                                                         seed_c, mr, er, mc, ec, status, s);      \
+    if (m <= 6) return launch_dual_t<MODE, 2, kPlaneFP6, kPlaneLo2, UPD>(x, dx, alpha, x_out, R, C, m, seed_r,    \
+                                                                         seed_c, mr, er, mc, ec, status, s);      \
+    return launch_dual_t<MODE, 2, kPlaneFP6, kPlaneFP6, UPD>(x, dx, alpha, x_out, R, C, m, seed_r, seed_c, mr, er, \
+                                                             mc, ec, status, s);                                  \
   } while (0)
   if (mode == kNearest) FASTBFP_DUAL(kNearest);
   if (mode == kStochastic) FASTBFP_DUAL(kStochastic);
@@ -588,29 +602,28 @@ hipError_t launch_weight_update(const float* w, const float* dw, float alpha, fl
   return launch_dual_any<true>(w, dw, alpha, w_out, R, C, m, mode, seed_r, seed_c, mr, er, mc, ec, status, s);
 }
 
-template <int G, int NCH, bool F0>
+template <int G, int NCH, int P0, int P1 = kPlaneFP6>
 static hipError_t launch_deq_t(const uint8_t* mant, const uint8_t* exps, int64_t ngroups, int m, float* y,
                                hipStream_t s) {
   const unsigned blocks = (unsigned)((ngroups + 255) / 256);
-  hipLaunchKernelGGL((k_dequantize<G, NCH, F0>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
+  hipLaunchKernelGGL((k_dequantize<G, NCH, P0, P1>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
   return hipGetLastError();
+}
+
+template <int G>
+static hipError_t launch_deq_g(const uint8_t* mant, const uint8_t* exps, int64_t ngroups, int m, float* y,
+                               hipStream_t s) {
+  if (m <= 2) return launch_deq_t<G, 1, kPlaneFP4>(mant, exps, ngroups, m, y, s);
+  if (m <= 4) return launch_deq_t<G, 1, kPlaneFP6>(mant, exps, ngroups, m, y, s);
+  if (m <= 6) return launch_deq_t<G, 2, kPlaneFP6, kPlaneLo2>(mant, exps, ngroups, m, y, s);
+  return launch_deq_t<G, 2, kPlaneFP6, kPlaneFP6>(mant, exps, ngroups, m, y, s);
 }
 
 hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m,
                              float* y, hipStream_t s) {
   const int64_t ngroups = rows * (len / g);
   if (ngroups == 0) return hipSuccess;
-  const bool two = m > 4, f4 = plane0_fp4(m);
-  if (g == 16) {
-    if (two) return f4 ? launch_deq_t<16, 2, true>(mant, exps, ngroups, m, y, s)
-                       : launch_deq_t<16, 2, false>(mant, exps, ngroups, m, y, s);
-    return f4 ? launch_deq_t<16, 1, true>(mant, exps, ngroups, m, y, s)
-              : launch_deq_t<16, 1, false>(mant, exps, ngroups, m, y, s);
-  }
-  if (two) return f4 ? launch_deq_t<32, 2, true>(mant, exps, ngroups, m, y, s)
-                     : launch_deq_t<32, 2, false>(mant, exps, ngroups, m, y, s);
-  return f4 ? launch_deq_t<32, 1, true>(mant, exps, ngroups, m, y, s)
-            : launch_deq_t<32, 1, false>(mant, exps, ngroups, m, y, s);
+  return g == 16 ? launch_deq_g<16>(mant, exps, ngroups, m, y, s) : launch_deq_g<32>(mant, exps, ngroups, m, y, s);
 }
 
 }  // namespace fastbfp

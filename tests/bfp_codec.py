@@ -5,8 +5,15 @@ with bias 1, 3 mantissa bits) and FP4 E2M1 (1 sign bit, 2 exponent bits with
 bias 1, 1 mantissa bit); exponent field 0 is subnormal in both.  Independent
 of the HIP kernels: it turns the library's packed mantissa bytes into signed
 integer magnitudes +-q, and the oracle's +-q into the bytes the library must
-write.  A plane whose chunk has at most 2 bits (plane 0 of m = 1, 2, 5, 6)
-holds FP4 codes, every other plane FP6 codes; both encode +-chunk/2.
+write.
+
+Planes: m = 1, 2: FP4 codes of +-q/2.  m = 3, 4: FP6 codes of +-q/2.
+m = 5, 6: FP6 codes of +-(q >> 2)/2, then a "Lo2" plane of the 2-bit chunk
+q & 3: per 16 values, the 96 bits T of their FP6 codes of +-(q & 3)/8 (three
+little-endian dwords T0, T1, T2), stored as the two dwords T0 | (T1 >> 1) and
+T2 (the FP6 code of a value below 1/2 has only its sign and two lowest bits
+set, and T1's such bits moved down by one fill T0's zero bits).
+m = 7, 8: FP6 codes of +-(q >> 4)/2 and of +-(q & 15)/2.
 """
 from __future__ import annotations
 
@@ -58,13 +65,46 @@ def n_planes(m: int) -> int:
 
 
 def plane_fp4(m: int, p: int) -> bool:
-    """True if plane p of an m-bit tensor holds FP4 codes (its chunk has at most 2 bits)."""
-    chunk_bits = m if m <= 4 else (m - 4 if p == 0 else 4)
-    return chunk_bits <= 2
+    """True if plane p of an m-bit tensor holds FP4 codes."""
+    return m <= 2 and p == 0
+
+
+def plane_lo2(m: int, p: int) -> bool:
+    """True if plane p of an m-bit tensor is a Lo2 plane (the 2-bit low chunk of m = 5, 6)."""
+    return m in (5, 6) and p == 1
+
+
+def low_bits(m: int) -> int:
+    """Bits of the lower chunk of a two-plane magnitude."""
+    return 2 if m <= 6 else 4
 
 
 def plane_bytes(rows: int, length: int, m: int, p: int) -> int:
-    return rows * length * (4 if plane_fp4(m, p) else 6) // 8
+    return rows * length * (4 if plane_fp4(m, p) or plane_lo2(m, p) else 6) // 8
+
+
+def _field_bits():
+    """Positions, in the 96 bits of 16 FP6 codes, that a code of +-c/8 with
+    c <= 3 can set: each field's two lowest bits and its sign bit."""
+    return [6 * t + b for t in range(16) for b in (0, 1, 5)]
+
+
+_LO2_MASK = [sum(1 << (b - 32 * w) for b in _field_bits() if b // 32 == w) for w in range(3)]
+assert _LO2_MASK[0] & (_LO2_MASK[1] >> 1) == 0 and _LO2_MASK[0] | (_LO2_MASK[1] >> 1) == 0xFFFFFFFF
+
+
+def _e2m3_eighth_code(c: np.ndarray) -> np.ndarray:
+    """FP6 E2M3 code of +-|c|/8 for |c| <= 3 (subnormal: mantissa field |c|),
+    zero as code 0."""
+    c = np.asarray(c, dtype=np.int64)
+    if np.any(np.abs(c) > 3):
+        raise ValueError("a chunk does not fit a Lo2 plane")
+    code = np.abs(c) | np.where(c < 0, 32, 0)
+    return code.astype(np.uint64)
+
+
+# the subnormal codes 0..3 stand for 0, 1/8, 2/8, 3/8
+assert [8 * e2m3_value(k) for k in range(4)] == [0, 1, 2, 3]
 
 
 def _split_planes(mant: np.ndarray, rows: int, length: int, m: int):
@@ -80,10 +120,27 @@ def _split_planes(mant: np.ndarray, rows: int, length: int, m: int):
 
 def unpack_codes(mant: np.ndarray, rows: int, length: int, m: int) -> list:
     """Per plane: the codes [rows, length] from the packed little-endian bytes
-    (6-bit FP6 codes or 4-bit FP4 codes)."""
+    (6-bit FP6 codes, also for a Lo2 plane after undoing its squeeze, or 4-bit
+    FP4 codes)."""
     planes = []
     for p, b in enumerate(_split_planes(mant, rows, length, m)):
-        if plane_fp4(m, p):
+        if plane_lo2(m, p):
+            d = b.reshape(-1, 8).astype(np.uint64)
+            d0 = d[:, 0] | (d[:, 1] << 8) | (d[:, 2] << 16) | (d[:, 3] << 24)
+            d1 = d[:, 4] | (d[:, 5] << 8) | (d[:, 6] << 16) | (d[:, 7] << 24)
+            t0 = d0 & _LO2_MASK[0]
+            t1 = (d0 << 1) & _LO2_MASK[1]
+            if np.any(d1 & ~np.uint64(_LO2_MASK[2])):
+                raise AssertionError("a Lo2 plane has bits set outside its codes")
+            codes = np.zeros((d.shape[0], 16), np.uint32)
+            for k in range(16):
+                bit = 6 * k
+                words = (t0, t1, d1)
+                v = words[bit // 32] >> np.uint64(bit % 32)
+                if bit % 32 > 26:
+                    v = v | (words[bit // 32 + 1] << np.uint64(32 - bit % 32))
+                codes[:, k] = (v & np.uint64(63)).astype(np.uint32)
+        elif plane_fp4(m, p):
             codes = np.stack([b & 15, b >> 4], axis=-1).astype(np.uint32)
         else:
             t = b.reshape(rows * length // 4, 3).astype(np.uint32)
@@ -96,7 +153,15 @@ def unpack_codes(mant: np.ndarray, rows: int, length: int, m: int) -> list:
 def decode(mant: np.ndarray, rows: int, length: int, m: int) -> np.ndarray:
     """Signed magnitudes +-q [rows, length] (int32) from mantissa bytes."""
     codes = unpack_codes(mant, rows, length, m)
-    chunks = [(_CODE4_TO_CHUNK if plane_fp4(m, p) else _CODE_TO_CHUNK)[c] for p, c in enumerate(codes)]
+    chunks = []
+    for p, c in enumerate(codes):
+        if plane_lo2(m, p):
+            v = np.array([8 * e2m3_value(int(k)) for k in range(64)])[c]
+            if np.any((v != np.round(v)) | (np.abs(v) > 3)):
+                raise AssertionError("a Lo2 code does not stand for a 2-bit chunk")
+            chunks.append(v.astype(np.int64))
+        else:
+            chunks.append((_CODE4_TO_CHUNK if plane_fp4(m, p) else _CODE_TO_CHUNK)[c])
     if any(np.any(c == 10 ** 6) for c in chunks):
         raise AssertionError("a code does not stand for an integer chunk")
     if n_planes(m) == 1:
@@ -104,7 +169,7 @@ def decode(mant: np.ndarray, rows: int, length: int, m: int) -> np.ndarray:
     hi, lo = chunks[0], chunks[1]
     if np.any((hi != 0) & (lo != 0) & (np.sign(hi) != np.sign(lo))):
         raise AssertionError("the two chunks of a value carry different signs")
-    return (hi * 16 + lo).astype(np.int32)
+    return (hi * (1 << low_bits(m)) + lo).astype(np.int32)
 
 
 def encode(q: np.ndarray, m: int) -> np.ndarray:
@@ -115,7 +180,8 @@ def encode(q: np.ndarray, m: int) -> np.ndarray:
         planes = [q]
     else:
         mag, sgn = np.abs(q), np.sign(q)
-        planes = [sgn * (mag >> 4), sgn * (mag & 15)]
+        w = low_bits(m)
+        planes = [sgn * (mag >> w), sgn * (mag & ((1 << w) - 1))]
     lut = np.zeros(31, dtype=np.uint32)
     for c, code in _CHUNK_TO_CODE.items():
         lut[c + 15] = code
@@ -124,7 +190,19 @@ def encode(q: np.ndarray, m: int) -> np.ndarray:
         lut4[c + 15] = code
     out = []
     for p, pl in enumerate(planes):
-        if plane_fp4(m, p):
+        if plane_lo2(m, p):
+            codes = _e2m3_eighth_code(pl).reshape(rows * length // 16, 16)
+            t = [np.zeros(codes.shape[0], np.uint64) for _ in range(3)]
+            for k in range(16):
+                bit = 6 * k
+                t[bit // 32] |= (codes[:, k] << np.uint64(bit % 32)) & np.uint64(0xFFFFFFFF)
+                if bit % 32 > 26:
+                    t[bit // 32 + 1] |= codes[:, k] >> np.uint64(32 - bit % 32)
+            d0 = t[0] | (t[1] >> np.uint64(1))
+            d1 = t[2]
+            words = np.stack([d0, d1], axis=-1).astype(np.uint32)
+            out.append(words.view(np.uint8).reshape(-1))
+        elif plane_fp4(m, p):
             codes = lut4[pl + 15].reshape(rows * length // 2, 2)
             if np.any(codes > 15):
                 raise ValueError("a chunk does not fit an FP4 plane")

@@ -14,6 +14,13 @@ import paper_2110_15456_amd as fb
 THREADS = 16
 
 
+def chunk_drops(m: int):
+    """The precisions bfp_gemm takes an m-bit operand at by reading fewer
+    chunk planes: m itself, and for two planes the upper plane alone (q >> 2
+    for m = 5, 6; q >> 4 for m = 7, 8)."""
+    return [m] if m <= 4 else [m, m - (2 if m <= 6 else 4)]
+
+
 def announce(msg: str) -> None:
     """Name the case on stdout before its GPU work starts."""
     sys.stdout.write("\n[case] %s\n" % msg)

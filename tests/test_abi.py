@@ -118,6 +118,8 @@ def test_gemm_validation(lib):
     assert gm(lib, am=8, ma=5) == E_PREC    # only whole 4-bit chunks can be dropped
     assert gm(lib, am=4, ma=5) == E_PREC    # cannot raise precision
     assert gm(lib, bm=6, mb=1) == E_PREC
+    assert gm(lib, bm=6, mb=2) == E_PREC    # m = 6 drops a 2-bit chunk (to 4), m = 8 a 4-bit one
+    assert gm(lib, am=8, ma=6) == E_PREC
     assert gm(lib, a=ctypes.c_void_p(0x100001)) == E_ARG
     assert gm(lib, M=0) == OK and gm(lib, N=0, ldc=0) == OK
     # 32-bit tile offsets: K up to 11184784 (256 rows of FP6 codes < 2^31 bytes)
@@ -137,7 +139,7 @@ def test_gemm_tiled_validation(lib):
     assert gmt(lib, 1, am=6, ma=6) == E_UNSUP            # two chunk planes: default tile only
     assert gmt(lib, 2, bm=8, mb=8) == E_UNSUP
     assert gmt(lib, 3, g=32) == E_UNSUP                  # groups of 32: default tile only
-    assert gmt(lib, 1, am=6, ma=2, M=0) == OK            # the low chunk dropped: one plane, empty
+    assert gmt(lib, 1, am=6, ma=4, M=0) == OK            # the low chunk dropped: one plane, empty
     assert gmt(lib, 0, am=6, ma=6, M=0) == OK and gmt(lib, -1, g=32, N=0, ldc=0) == OK
     assert gmt(lib, 2, K=40) == E_SHAPE and gmt(lib, 3, C=None) == E_ARG and gmt(lib, 1, ldc=7) == E_SHAPE
 

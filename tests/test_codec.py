@@ -36,7 +36,7 @@ def test_round_trip_and_sizes(m):
     rows, length = 3, 64
     q = rng.integers(-(2 ** m - 1), 2 ** m, size=(rows, length))
     b = bfp_codec.encode(q, m)
-    bits = {1: 4, 2: 4, 3: 6, 4: 6, 5: 10, 6: 10, 7: 12, 8: 12}[m]
+    bits = {1: 4, 2: 4, 3: 6, 4: 6, 5: 10, 6: 10, 7: 12, 8: 12}[m]  # m = 5, 6: FP6 + Lo2
     assert b.size == rows * length * bits // 8
     assert np.array_equal(bfp_codec.decode(b, rows, length, m), q)
 
@@ -48,13 +48,40 @@ def test_fp4_plane_packing_order():
     b = bfp_codec.encode(q, 2)
     assert b.size == 8
     assert b[0] == (0x8 | 3) << 4 | 1 and b[7] == 2 << 4 and not b[1:7].any()
-    # m = 6: the upper chunk (q >> 4, two bits) in FP4, then the lower chunk in FP6
+    # m = 6: the upper chunk q >> 2 = 13 in FP6 (-6.5: sign 32, exponent 3,
+    # mantissa 5 -> code 61), then the 2-bit chunk q & 3 = 1 in the Lo2 plane
+    # (-1/8: the subnormal code 32 | 1)
     q6 = np.zeros((1, 16), np.int64)
     q6[0, 0] = -(3 * 16 + 5)
     b6 = bfp_codec.encode(q6, 6)
-    assert b6.size == 8 + 12
-    assert b6[0] == 0x8 | 3 and not b6[1:8].any()
+    assert b6.size == 12 + 8
+    assert b6[0] == 61 and not b6[1:12].any()
+    assert b6[12] == 33 and not b6[13:].any()
     assert bfp_codec.decode(b6, 1, 16, 6)[0, 0] == -53
+
+
+def test_lo2_plane_is_the_squeezed_fp6_codes():
+    """The Lo2 plane of m = 5, 6 holds the FP6 codes of +-(q & 3)/8: per 16
+    values the 96-bit code string T (dwords T0, T1, T2) stored as T0 | T1 >> 1
+    and T2.  Checked on every value position against a direct bit string."""
+    rng = np.random.default_rng(3)
+    for _ in range(20):
+        lo = rng.integers(-3, 4, 16)
+        q = np.sign(lo) * (4 * rng.integers(0, 8, 16) + np.abs(lo))
+        q[lo == 0] = 4 * rng.integers(0, 8, int((lo == 0).sum()))
+        b = bfp_codec.encode(q.reshape(1, 16), 5)
+        lo_bytes = b[12:20]
+        T = 0
+        for t in range(16):
+            c = int(abs(q[t]) & 3)
+            code = c | (32 if (q[t] < 0 and c) else 0)
+            assert bfp_codec.e2m3_value(code) * 8 == (c if q[t] >= 0 else -c)
+            T |= code << (6 * t)
+        t0, t1, t2 = T & 0xFFFFFFFF, (T >> 32) & 0xFFFFFFFF, T >> 64
+        d0, d1 = t0 | (t1 >> 1), t2
+        assert int.from_bytes(lo_bytes[:4].tobytes(), "little") == d0
+        assert int.from_bytes(lo_bytes[4:].tobytes(), "little") == d1
+        assert np.array_equal(bfp_codec.decode(b, 1, 16, 5)[0], q)
 
 
 def test_fp4_rejects_wide_chunks():

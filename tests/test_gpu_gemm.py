@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2110_15456_amd as fb
 from paper_2110_15456_amd import synth
-from gpu_util import announce, check_quantize, THREADS
+from gpu_util import announce, check_quantize, chunk_drops, THREADS
 
 pytestmark = pytest.mark.gpu
 TOL = 1e-6
@@ -55,8 +55,8 @@ def test_tiny_all_precisions(K):
         for bm in range(1, 9):
             announce("gemm tiny K=%d stored (%d,%d)" % (K, am, bm))
             A, B, oa, ob = operands(x[:4], x[4:], am, bm)
-            for m_a in sorted({am, am - 4} - {-3, -2, -1, 0}):
-                for m_b in sorted({bm, bm - 4} - {-3, -2, -1, 0}):
+            for m_a in chunk_drops(am):
+                for m_b in chunk_drops(bm):
                     check_gemm(A, B, oa, ob, m_a, m_b, partials=True)
 
 
@@ -70,8 +70,9 @@ def test_config1_256():
 
 
 SHAPES = [(300, 200, 592), (257, 129, 576), (129, 257, 144), (1, 1, 16), (5, 300, 4096), (64, 64, 2048)]
-# Every kernel variant: (planes, plane-0 format) of A x B, where m = 1, 2 is one
-# FP4 plane, 3, 4 one FP6 plane, 5, 6 an FP4 + FP6 pair and 7, 8 two FP6 planes.
+# Every kernel variant: the operand formats of A x B, where m = 1, 2 is one FP4
+# plane, 3, 4 one FP6 plane, 5, 6 an FP6 + Lo2 pair (split at 2 bits: whole
+# MFMA blocks) and 7, 8 two FP6 planes (split at 4 bits).
 PAIRS = [(2, 2), (2, 4), (4, 2), (4, 4),          # one plane each
          (1, 5), (2, 8), (4, 6), (3, 7),          # one x two
          (5, 2), (6, 3), (8, 1), (7, 4),          # two x one
@@ -94,15 +95,16 @@ def test_one_chunk_tiles(tile):
     """Every workgroup tile of the one-chunk, g = 16 GEMM (256x256, 256x128,
     256x64, 128x64, 128x128), forced through bfp_gemm_tiled, on shapes that span several
     tiles with ragged tails, partial and full slabs, and every one-plane operand
-    format pair (FP4 / FP6 codes, and an FP4 upper plane read alone)."""
+    format pair (FP4 / FP6 codes, and the FP6 upper plane of m = 5, 6 read
+    alone)."""
     # K = 576, 192, 64: ragged K whose exponent rows are whole dwords (the
     # dword exponent loads, last slab half full); 592, 144, 16: byte loads
     for M, N, K in [(300, 200, 592), (520, 72, 1024), (129, 257, 144), (1, 1, 16), (5, 300, 4096),
                     (384, 64, 128 * 5), (260, 136, 576), (130, 70, 192), (70, 130, 64)]:
         xa = synth.draw("half_normal", (M, K), 900 + M + K)
         xb = synth.draw("weights", (N, K), 901 + N + K)
-        for am, bm, m_a, m_b in [(2, 2, 2, 2), (2, 4, 2, 4), (4, 2, 4, 2), (3, 4, 3, 4), (6, 1, 2, 1),
-                                 (4, 5, 4, 1)]:
+        for am, bm, m_a, m_b in [(2, 2, 2, 2), (2, 4, 2, 4), (4, 2, 4, 2), (3, 4, 3, 4), (6, 1, 4, 1),
+                                 (4, 5, 4, 3)]:
             announce("gemm tile %d %dx%dx%d stored (%d,%d) at (%d,%d)" % (tile, M, N, K, am, bm, m_a, m_b))
             A, B, oa, ob = operands(xa, xb, am, bm)
             check_gemm(A, B, oa, ob, m_a, m_b, tile=tile)
@@ -191,9 +193,9 @@ def test_strided_output():
 def test_precision_lowering():
     xa = synth.draw("half_normal", (130, 320), 5)
     xb = synth.draw("grads", (70, 320), 6)
-    announce("gemm stored (8,6) used at (4,2) and mixed")
+    announce("gemm stored (8,6) used at (4,4) and mixed")
     A, B, oa, ob = operands(xa, xb, 8, 6, mode_b="stochastic", seed=3)
-    for m_a, m_b in [(4, 2), (8, 2), (4, 6), (8, 6)]:
+    for m_a, m_b in [(4, 4), (8, 4), (4, 6), (8, 6)]:
         check_gemm(A, B, oa, ob, m_a, m_b, partials=True)
 
 
@@ -273,8 +275,8 @@ def test_g32_tiny_all_precisions(K):
         for bm in range(1, 9):
             announce("gemm g=32 tiny K=%d stored (%d,%d)" % (K, am, bm))
             A, B, oa, ob = operands(x[:4], x[4:], am, bm, g=32)
-            for m_a in sorted({am, am - 4} - {-3, -2, -1, 0}):
-                for m_b in sorted({bm, bm - 4} - {-3, -2, -1, 0}):
+            for m_a in chunk_drops(am):
+                for m_b in chunk_drops(bm):
                     check_gemm(A, B, oa, ob, m_a, m_b, partials=True)
 
 

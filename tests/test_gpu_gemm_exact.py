@@ -24,7 +24,7 @@ import torch
 import oracle
 import paper_2110_15456_amd as fb
 from paper_2110_15456_amd import synth
-from gpu_util import announce, check_quantize, THREADS
+from gpu_util import announce, check_quantize, chunk_drops, THREADS
 
 pytestmark = pytest.mark.gpu
 SEEDS = range(100)
@@ -34,10 +34,6 @@ def stacked(K: int):
     xs = [synth.draw("normal", (8, K), 5000 + 7 * K + s) for s in SEEDS]
     return (np.ascontiguousarray(np.concatenate([x[:4] for x in xs])),
             np.ascontiguousarray(np.concatenate([x[4:] for x in xs])))
-
-
-def lower_precisions(m: int):
-    return [m] if m <= 4 else [m, m - 4]
 
 
 @pytest.mark.parametrize("mode", ["nearest", "stochastic", "truncate"])
@@ -52,8 +48,8 @@ def test_tiny_cases_exact(g, K, mode):
     for am in range(1, 9):
         for bm in range(1, 9):
             (Ta, qa, ea), (Tb, qb, eb) = A[am], B[bm]
-            for m_a in lower_precisions(am):
-                for m_b in lower_precisions(bm):
+            for m_a in chunk_drops(am):
+                for m_b in chunk_drops(bm):
                     announce("gemm stacked tiny g=%d K=%d %s stored (%d,%d) at (%d,%d)"
                              % (g, K, mode, am, bm, m_a, m_b))
                     C = fb.gemm(Ta, Tb, m_a, m_b)
