@@ -30,30 +30,37 @@
  *   exp  : uint8 [rows][len/g]   shared exponent E = the largest FP32 biased
  *          exponent field in the group (0 for a group of zeros/subnormals).
  *          One unit in the last place of the group is 2^(E - 127 - (m-1)).
- *   mant : chunk planes.  A magnitude q in [0, 2^m - 1] is split into 4-bit
- *          chunks, most significant first: one chunk (q itself) when m <= 4,
- *          two (hi = q >> 4, which has m - 4 bits, and lo = q & 15) when
- *          5 <= m <= 8.  Plane c holds chunk c of every value, with the
- *          value's sign, as the code of (+-chunk / 2) in the narrowest OCP MX
- *          element format that holds it exactly:
- *            FP4 E2M1 (4 bits: the sign, then the chunk itself in the three
- *              low bits) for a chunk of at most 2 bits, i.e. plane 0 when m
- *              is 1, 2, 5 or 6;
- *            FP6 E2M3 (6 bits) otherwise: every integer 0..15 halved is exact.
- *          Codes are packed little-endian, w bits per value (value t of a
- *          group at bits w*t .. w*t + w - 1; w = 4 or 6), so a group takes
- *          B_c = g/2 (FP4) or 3g/4 (FP6) bytes in plane c:
+ *   mant : chunk planes.  A magnitude q in [0, 2^m - 1] is stored as one
+ *          chunk (m <= 4: q itself) or two (m = 5, 6: hi = q >> 2, which has
+ *          m - 2 bits, and lo = q & 3; m = 7, 8: hi = q >> 4, which has m - 4
+ *          bits, and lo = q & 15).  Plane c holds chunk c of every value with
+ *          the value's sign, in one of three encodings:
+ *            FP4 E2M1 codes of +-chunk/2 (4 bits: the sign, then the chunk
+ *              itself in the three low bits) -- m = 1, 2;
+ *            FP6 E2M3 codes of +-chunk/2 (6 bits; every integer 0..15 halved
+ *              is exact) -- m = 3, 4, the hi plane of m = 5..8 and the lo
+ *              plane of m = 7, 8;
+ *            Lo2 -- the lo plane of m = 5, 6: per 16 values, the 96 bits of
+ *              their FP6 E2M3 codes of +-chunk/8 (subnormal codes: only a
+ *              field's sign and two lowest bits can be set), as the three
+ *              little-endian dwords T0, T1, T2, stored as the two dwords
+ *              T0 | (T1 >> 1) and T2 (T1's possible bits shifted down by one
+ *              fall exactly on T0's always-zero bits).
+ *          FP4 and FP6 codes are packed little-endian, w bits per value
+ *          (value t of a group at bits w*t .. w*t + w - 1; w = 4 or 6).  A
+ *          group takes B_c = g/2 (FP4, Lo2) or 3g/4 (FP6) bytes in plane c:
  *            plane 0, row r, group G at byte offset (r * (len/g) + G) * B_0,
  *            plane 1 at rows * (len/g) * B_0 + (r * (len/g) + G) * B_1.
- *          A zero magnitude is stored as code 0 (no sign).
- *          This is the paper's chunk-plane storage (section V-D) with 4-bit
- *          chunks, the width gfx950's block-scaled MFMA consumes at its full
- *          FP6/FP4 rate; a chunk of at most 2 bits is the paper's sign plus
- *          2-bit chunk, kept in a 4-bit code (the paper packs it in 3 bits;
- *          the matrix cores read 4).  The lower chunk's scale is 2^4 below the
- *          upper chunk's, as the paper decrements the lower 2-bit chunk's
- *          exponent.  Bits per value at g = 16, exponent included: 4.5
- *          (m <= 2), 6.5 (m = 3, 4), 10.5 (m = 5, 6), 12.5 (m = 7, 8).
+ *          A group of 32 is laid out as two consecutive groups of 16.
+ *          A zero chunk is stored as code 0 (no sign).
+ *          This is the paper's chunk-plane storage (section V-D): each plane
+ *          holds one chunk of every value with its sign, the upper chunk's
+ *          weight is the lower chunk's times 2^(bits of the lower chunk), and
+ *          a 2-bit chunk with its sign takes the paper's 3 bits (a Lo2 plane
+ *          packs 16 of them in 6 of its 8 bytes); the chunk widths are those
+ *          gfx950's block-scaled MFMA consumes at its full FP6/FP4 rate.
+ *          Bits per value at g = 16, exponent included: 4.5 (m <= 2), 6.5
+ *          (m = 3, 4), 10.5 (m = 5, 6), 12.5 (m = 7, 8).
  */
 #ifndef FASTBFP_H
 #define FASTBFP_H
@@ -88,7 +95,7 @@ int bfp_abi_version(void);
 /* Static, NUL-terminated description of a status code. */
 const char* bfp_status_str(int status);
 
-/* Number of 4-bit chunk planes for an m-bit magnitude: 1 if m <= 4, 2 if
+/* Number of chunk planes for an m-bit magnitude: 1 if m <= 4, 2 if
  * 5 <= m <= 8, 0 if m is outside 1..8. */
 int bfp_chunks(int m_bits);
 
@@ -145,14 +152,17 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
  * The products are exact; the cross-group sum is accumulated in FP32.
  *   a_mant/a_exp : A stored with a_m_bits (rows M, len K); likewise B (rows N).
  *   m_a, m_b     : the precisions the product is taken at.  Either the stored
- *                  width, or, for a two-chunk operand, the stored width minus
- *                  4: the low chunk plane is then skipped, i.e. the magnitude is
- *                  truncated to its top m - 4 bits (the paper's discard of a
+ *                  width, or, for a two-chunk operand, the width of its upper
+ *                  chunk (m - 2 for m = 5, 6; m - 4 for m = 7, 8): the low
+ *                  chunk plane is then skipped, i.e. the magnitude is
+ *                  truncated to its top bits (the paper's discard of a
  *                  low-order chunk, section V-D).  Anything else returns
  *                  BFP_E_PRECISION.
- *   Passes: the kernel issues chunks(m_a) * chunks(m_b) block-scaled MFMA
- *   passes per group pair (1 for m_a, m_b <= 4), the counterpart of the
- *   paper's (m_a/2)(m_b/2) fMAC rounds.
+ *   Passes: one block-scaled MFMA per chunk-plane pair and group pair, the
+ *   counterpart of the paper's (m_a/2)(m_b/2) fMAC rounds -- except that an
+ *   operand split at 2 bits (m = 5, 6) puts both of its chunks in one
+ *   32-value MFMA block, so it adds no pass of its own: (6,6) takes 2 MFMAs
+ *   per group of 16, (6, m <= 4) 1.
  *   g            : 16 or 32 (both operands).  A group of 32 fills a whole
  *                  MFMA block; a group of 16 leaves half of it zero.
  *   C            : FP32 with row stride ldc >= N (elements).
