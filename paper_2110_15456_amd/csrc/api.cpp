@@ -8,7 +8,11 @@
 
 namespace {
 
-bool group_supported(int g) { return g == 16 || g == 32; }
+bool group_supported(int g) { return g == 4 || g == 8 || g == 16 || g == 32 || g == 64; }
+
+// Rows hold whole 16-value units (the plane layout's unit): with g = 4 or 8
+// the grouped length must be a multiple of 16 as well as of g.
+bool length_ok(int64_t len, int g) { return len % g == 0 && len % 16 == 0; }
 
 // Largest K the GEMM accepts: 256 * (K / 16) * 12 < 2^31.
 constexpr int64_t kMaxK = ((int64_t(1) << 31) / (256 * 12) - 1) * 16;
@@ -18,7 +22,7 @@ int check_tensor(int64_t rows, int64_t len, int g, int m) {
   if (m < 1 || m > 8) return BFP_E_PRECISION;
   if (g <= 0) return BFP_E_ARG;
   if (!group_supported(g)) return BFP_E_UNSUPPORTED;
-  if (len % g != 0) return BFP_E_SHAPE;
+  if (!length_ok(len, g)) return BFP_E_SHAPE;
   return BFP_OK;
 }
 
@@ -35,6 +39,13 @@ int planes_used(int m_stored, int m_use) {
 
 int status_of(hipError_t e) { return e == hipSuccess ? BFP_OK : BFP_E_HIP; }
 
+// True when the block-scaled kernel (gemm_mx.h) takes the product: groups of
+// 16 or 32 and each operand at its stored width or with its low chunk plane
+// dropped; everything else runs on the general kernel (gemm_general.hip).
+bool fast_path(int a_m, int b_m, int g, int m_a, int m_b) {
+  return (g == 16 || g == 32) && planes_used(a_m, m_a) != 0 && planes_used(b_m, m_b) != 0;
+}
+
 int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, int64_t M, int64_t N, int64_t K, int g,
                int m_a, int m_b) {
   if (M < 0 || N < 0 || K < 0) return BFP_E_ARG;
@@ -42,8 +53,8 @@ int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, i
   if (a_m < 1 || a_m > 8 || b_m < 1 || b_m > 8) return BFP_E_PRECISION;
   if (g <= 0) return BFP_E_ARG;
   if (!group_supported(g)) return BFP_E_UNSUPPORTED;
-  if (K % g != 0) return BFP_E_SHAPE;
-  if (planes_used(a_m, m_a) == 0 || planes_used(b_m, m_b) == 0) return BFP_E_PRECISION;
+  if (!length_ok(K, g)) return BFP_E_SHAPE;
+  if (m_a < 1 || m_a > a_m || m_b < 1 || m_b > b_m) return BFP_E_PRECISION;
   // The kernels address a tile's operand rows through 32-bit buffer offsets:
   // 256 rows of an FP6 plane (12 bytes per 16 values) must span less than
   // 2^31 bytes (offsets at 2^31 and above are the zero-reading sentinel of
@@ -79,10 +90,11 @@ const char* bfp_status_str(int status) {
   switch (status) {
     case BFP_OK: return "ok";
     case BFP_E_ARG: return "invalid argument (null or misaligned pointer, negative size, bad enum)";
-    case BFP_E_SHAPE: return "shape mismatch (group size must divide the grouped axis; K and ldc must agree)";
-    case BFP_E_UNSUPPORTED: return "unsupported configuration (group size must be 16 or 32)";
-    case BFP_E_PRECISION: return "unsupported precision (m in 1..8; GEMM precision must be the stored width or drop "
-                                 "the low 4-bit chunk)";
+    case BFP_E_SHAPE: return "shape mismatch (the grouped axis must be a multiple of g and of 16; K and ldc must "
+                             "agree)";
+    case BFP_E_UNSUPPORTED: return "unsupported configuration (group size, size limit, or an entry point that takes "
+                                   "fewer group sizes or precisions)";
+    case BFP_E_PRECISION: return "unsupported precision (m in 1..8; a GEMM precision between 1 and the stored width)";
     case BFP_E_HIP: return "HIP runtime error at launch";
     default: return "unknown status";
   }
@@ -134,12 +146,18 @@ int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, co
   if (st != BFP_OK) return st;
   if (ldc < N) return BFP_E_SHAPE;
   if (tile < -1 || tile > 4) return BFP_E_ARG;
+  const bool fast = fast_path(a_m_bits, b_m_bits, g, m_a, m_b);
+  if (!fast && tile >= 0) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
   if (tile > 0 && (g != 16 || na != 1 || nb != 1)) return BFP_E_UNSUPPORTED;
   if (M == 0 || N == 0) return BFP_OK;
   if (!C || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!fast)
+    return status_of(fastbfp::launch_gemm_general(a_mant, a_exp, a_m_bits, m_a, b_mant, b_exp, b_m_bits, m_b, M, N, K,
+                                                  g, C, ldc, nullptr, s));
   return status_of(fastbfp::launch_gemm_mx(a_mant, a_exp, a_m_bits, na, b_mant, b_exp, b_m_bits, nb, M, N, K, g,
-                                           4 - m_a - m_b, C, ldc, tile, static_cast<hipStream_t>(stream)));
+                                           4 - m_a - m_b, C, ldc, tile, s));
 }
 
 int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
@@ -153,6 +171,7 @@ int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, cons
                  uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status_word, void* stream) {
   int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
   if (st != BFP_OK) return st;
+  if (!fast_path(a_m_bits, b_m_bits, g, m_a, m_b)) return BFP_E_UNSUPPORTED;
   if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
   st = check_tensor(M, N, 16, c_m_bits);
   if (st != BFP_OK) return st;
@@ -171,10 +190,9 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
   if (st != BFP_OK) return st;
   if (M == 0 || N == 0 || K == 0) return BFP_OK;
   if (!P) return BFP_E_ARG;
-  if ((M + 31) / 32 > 65535 || K / g > 65535) return BFP_E_UNSUPPORTED;
-  const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
-  return status_of(fastbfp::launch_group_partials(a_mant, a_m_bits, na, b_mant, b_m_bits, nb, M, N, K, g, P,
-                                                  static_cast<hipStream_t>(stream)));
+  // the group partials need no exponents: the decoder reads only mantissas
+  return status_of(fastbfp::launch_gemm_general(a_mant, nullptr, a_m_bits, m_a, b_mant, nullptr, b_m_bits, m_b, M, N,
+                                                K, g, nullptr, N, P, static_cast<hipStream_t>(stream)));
 }
 
 int bfp_quantize_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, uint64_t seed_r,
@@ -208,6 +226,7 @@ int bfp_quantize_adaptive(const float* x, int64_t R, int64_t C, int group_axis, 
   const int64_t rows = group_axis == 1 ? R : C, len = group_axis == 1 ? C : R;
   const int st = check_tensor(rows, len, g, 4);
   if (st != BFP_OK) return st;
+  if (g != 16 && g != 32) return BFP_E_UNSUPPORTED;
   if (!sums || !aligned(sums, 8)) return BFP_E_ARG;
   if (R != 0 && C != 0) {
     if (!x || !mant4 || !exp) return BFP_E_ARG;
@@ -227,6 +246,7 @@ int bfp_quantize_adaptive_noalloc(const float* x, int64_t R, int64_t C, int grou
   const int64_t rows = group_axis == 1 ? R : C, len = group_axis == 1 ? C : R;
   const int st = check_tensor(rows, len, g, 4);
   if (st != BFP_OK) return st;
+  if (g != 16 && g != 32) return BFP_E_UNSUPPORTED;
   if (!sums || !aligned(sums, 8)) return BFP_E_ARG;
   if (2 * fastbfp::adaptive_parts(R, C, group_axis, g) > fastbfp::kAdaptiveScratchDoubles) return BFP_E_UNSUPPORTED;
   if (R != 0 && C != 0) {

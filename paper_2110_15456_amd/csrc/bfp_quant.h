@@ -82,7 +82,7 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
                                                 uint32_t key1, uint32_t (&w)[NCH][NG * G * 6 / 32],
                                                 uint32_t (&E_out)[NG], bool& nonfinite, uint32_t (&s_lo)[NG],
                                                 uint32_t (&s_hi)[NG]) {
-  static_assert(NG == 1 || G == 16, "several groups per call: 16-value groups");
+  static_assert(NG == 1 || NG * G == 16 || NG * G == 32, "several groups per call: one or two 16-value units");
   constexpr int PK[2] = {P0, P1};
   constexpr int LEN = NG * G;  // values converted together (one packing unit)
 #pragma unroll
@@ -107,13 +107,14 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
 #pragma unroll
     for (int gi = 0; gi < NG; ++gi)
 #pragma unroll
-      for (int blk = 0; blk < G / 16; ++blk) {
+      for (int blk = 0; blk < (G + 15) / 16; ++blk) {
+        // one Philox block per 16 values of a group (a group of 4 or 8 uses
+        // the first G/4 words of its block)
         const uint64_t id = gid + (uint64_t)gi;
         const uint4 r = philox4x32_10(make_uint4((uint32_t)id, (uint32_t)(id >> 32), (uint32_t)blk, 0u), key0, key1);
-        noise[gi * G / 4 + 4 * blk + 0] = r.x;
-        noise[gi * G / 4 + 4 * blk + 1] = r.y;
-        noise[gi * G / 4 + 4 * blk + 2] = r.z;
-        noise[gi * G / 4 + 4 * blk + 3] = r.w;
+        const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+        for (int k = 0; k < (G < 16 ? G / 4 : 4); ++k) noise[gi * G / 4 + 4 * blk + k] = rw[k];
       }
   }
 

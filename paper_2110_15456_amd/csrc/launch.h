@@ -85,7 +85,11 @@ hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a
                               int scale_log2,
                               int c_m, int mode, uint64_t seed, uint8_t* c_mant, uint8_t* c_exp, uint32_t* status,
                               hipStream_t s);
-hipError_t launch_group_partials(const uint8_t* a_mant, int a_m, int na, const uint8_t* b_mant, int b_m, int nb,
-                                 int64_t M, int64_t N, int64_t K, int g, int32_t* P, hipStream_t s);
+// The general BFP GEMM (gemm_general.hip): any m_a <= a_m and m_b <= b_m, g in
+// {4, 8, 16, 32, 64} (K a multiple of g and of 16).  With P non-null it writes
+// the int32 group partials P[K/g][M][N] instead of C.
+hipError_t launch_gemm_general(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int m_a, const uint8_t* b_mant,
+                               const uint8_t* b_exp, int b_m, int m_b, int64_t M, int64_t N, int64_t K, int g,
+                               float* C, int64_t ldc, int32_t* P, hipStream_t s);
 
 }  // namespace fastbfp

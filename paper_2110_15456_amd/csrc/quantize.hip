@@ -88,7 +88,7 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
                                                        uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant0,
                                                        uint8_t* __restrict__ mant1, uint8_t* __restrict__ exps,
                                                        uint32_t* status, double* part) {
-  constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane
+  constexpr int GPL = G <= 16 ? 32 / G : 1;  // groups per lane: 32 values for g <= 16
   constexpr int CPG = G / 4;                         // 16-byte chunks per group
   constexpr int CPL = GPL * CPG;                     // 16-byte chunks per lane
   constexpr int LANES_PER_SWZ = 16 / CPL;
@@ -130,17 +130,29 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
   bool nonfinite;
   quantize_groups<G, GPL, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)gid, key0, key1, w, E, nonfinite, s_lo,
                                                           s_hi);
-  if (GPL == 2 && nmine == 2) {
-    // both groups: one packing unit of 32 values (its bytes are the two
-    // groups' bytes side by side) and two exponent bytes
-    stream_store(reinterpret_cast<uint16_t*>(exps + gid), (uint16_t)(E[0] | (E[GPL - 1] << 8)));
+  if (GPL > 1 && nmine == GPL) {
+    // every group: one packing unit of 32 values (its bytes are the groups'
+    // bytes side by side) and GPL exponent bytes
+    if constexpr (GPL == 2) {
+      stream_store(reinterpret_cast<uint16_t*>(exps + gid), (uint16_t)(E[0] | (E[GPL - 1] << 8)));
+    } else if constexpr (GPL >= 4) {
+      uint32_t e4[GPL / 4];
+#pragma unroll
+      for (int k = 0; k < GPL / 4; ++k)
+        e4[k] = E[4 * k] | (E[4 * k + 1] << 8) | (E[4 * k + 2] << 16) | (E[4 * k + 3] << 24);
+#pragma unroll
+      for (int k = 0; k < GPL / 4; ++k) stream_store(reinterpret_cast<uint32_t*>(exps + gid) + k, e4[k]);
+    }
     store_group<GPL * G, NCH, P0, P1, true>(mant0, mant1, gid / GPL, w);
     if (status && nonfinite) atomicOr(status, 1u);
   } else if (nmine > 0) {
-    // one group (GPL = 1, or the last group of an odd count): its own bytes
-    exps[gid] = (uint8_t)E[0];
-    store_plane<G, P0 != kPlaneFP6, true>(mant0, gid, w[0]);
-    if (NCH == 2) store_plane<G, P1 != kPlaneFP6, true>(mant1, gid, w[NCH - 1]);
+    // GPL = 1, or the last 16 values of the wave (every row holds whole
+    // 16-value units): their own bytes
+    constexpr int U = G < 16 ? 16 : G;  // values stored
+#pragma unroll
+    for (int k = 0; k < (G < 16 ? 16 / G : 1); ++k) exps[gid + k] = (uint8_t)E[k];
+    store_plane<U, P0 != kPlaneFP6, true>(mant0, gid * G / U, w[0]);
+    if (NCH == 2) store_plane<U, P1 != kPlaneFP6, true>(mant1, gid * G / U, w[NCH - 1]);
     if (status && nonfinite) atomicOr(status, 1u);
   }
   if (ADAPT) {
@@ -167,18 +179,21 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
                                                        int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
                                                        uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1,
                                                        uint8_t* __restrict__ exps, uint32_t* status, double* part) {
-  constexpr int JB = 4 * NGT;             // group rows per block
-  constexpr int WPG = G * 6 / 32;         // code dwords per group of an FP6 plane (an FP4 plane: G / 8)
-  constexpr int WP[2] = {P0 != kPlaneFP6 ? G / 8 : WPG, P1 != kPlaneFP6 ? G / 8 : WPG};  // code dwords per group
+  // A step converts U = max(G, 16) consecutive values of a column: NGU = U / G
+  // groups (a 16-value unit of groups of 4 or 8, or one group).
+  constexpr int U = G < 16 ? 16 : G, NGU = U / G;
+  constexpr int JB = 4 * NGT;             // unit rows per block
+  constexpr int WPG = U * 6 / 32;         // code dwords per unit of an FP6 plane (an FP4 or Lo2 plane: U / 8)
+  constexpr int WP[2] = {P0 != kPlaneFP6 ? U / 8 : WPG, P1 != kPlaneFP6 ? U / 8 : WPG};
   constexpr int ROWW = JB * WPG;          // LDS row stride, code dwords per output row
   __shared__ uint32_t sc[NCH][64][ROWW];
-  __shared__ uint8_t se[64][JB];
+  __shared__ uint8_t se[64][JB * NGU];
   const int64_t bx = blockIdx.x % nbx, by = blockIdx.x / nbx;
   const int lane = threadIdx.x & 63, slot = threadIdx.x >> 6;
   const int64_t c0 = bx * 64, c = c0 + lane;
-  const int64_t gpr = R / G;
+  const int64_t gpr = R / G, upr = R / U;  // groups and units per output row
   const int64_t jb = by * JB;
-  const int jn = (int)min((int64_t)JB, gpr - jb);  // group rows this block covers
+  const int jn = (int)min((int64_t)JB, upr - jb);  // unit rows this block covers
   bool any_bad = false;
   double num = 0.0, den = 0.0;
   if (c < C) {
@@ -186,30 +201,31 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       const int jl = slot * NGT + i;
       if (jl >= jn) break;
       const int64_t j = jb + jl;
-      uint32_t b[G];
-      const float* src = x + (j * G) * C + c;
+      uint32_t b[U];
+      const float* src = x + (j * U) * C + c;
 #pragma unroll
-      for (int t = 0; t < G; ++t) b[t] = __float_as_uint(stream_load(src + t * C));
+      for (int t = 0; t < U; ++t) b[t] = __float_as_uint(stream_load(src + t * C));
       uint32_t w[NCH][WPG];
-      uint32_t E, s_lo, s_hi;
+      uint32_t E[NGU], s_lo[NGU], s_hi[NGU];
       bool nonfinite;
-      quantize_group<G, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)(c * gpr + j), key0, key1, w, E, nonfinite, s_lo,
-                                                  s_hi);
+      quantize_groups<G, NGU, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)(c * gpr + j * NGU), key0, key1, w, E,
+                                                             nonfinite, s_lo, s_hi);
       if (ADAPT) {
-        num += ldexp((double)s_lo, (int)E - 130);
-        den += ldexp((double)s_hi, (int)E - 128);
+        num += ldexp((double)s_lo[0], (int)E[0] - 130);
+        den += ldexp((double)s_hi[0], (int)E[0] - 128);
       }
 #pragma unroll
       for (int p = 0; p < NCH; ++p)
 #pragma unroll
         for (int k = 0; k < WP[p]; ++k) sc[p][lane][jl * WP[p] + k] = w[p][k];
-      se[lane][jl] = (uint8_t)E;
+#pragma unroll
+      for (int k = 0; k < NGU; ++k) se[lane][jl * NGU + k] = (uint8_t)E[k];
       any_bad |= nonfinite;
     }
   }
   if (ADAPT) block_improvement(num, den, part);
   __syncthreads();
-  // Write-out: output row c0 + r gets jn groups starting at group jb.
+  // Write-out: output row c0 + r gets jn units starting at unit jb.
   const int ncols = (int)min((int64_t)64, C - c0);
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
@@ -217,48 +233,52 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
     for (int d = threadIdx.x; d < ncols * rw; d += 256) {
       const int r = d / rw, k = d % rw;
       if (k < jn * WP[p]) {
-        const int64_t o = ((c0 + r) * gpr + jb) * WP[p] + k;
+        const int64_t o = ((c0 + r) * upr + jb) * WP[p] + k;
         reinterpret_cast<uint32_t*>(p ? mant1 : mant0)[o] = sc[p][r][k];
       }
     }
   }
-  for (int d = threadIdx.x; d < ncols * JB; d += 256) {
-    const int r = d / JB, k = d % JB;
-    if (k < jn) exps[(c0 + r) * gpr + jb + k] = se[r][k];
+  for (int d = threadIdx.x; d < ncols * JB * NGU; d += 256) {
+    const int r = d / (JB * NGU), k = d % (JB * NGU);
+    if (k < jn * NGU) exps[(c0 + r) * gpr + jb * NGU + k] = se[r][k];
   }
   if (status && any_bad) atomicOr(status, 1u);
 }
 
-// BFP -> FP32: y = +-q * 2^(E-127-(m-1)).  One lane per group.  P0 / P1:
-// the plane formats (launch.h); with two planes q = c0 * 2^s + c1, s = 2 when
+// BFP -> FP32: y = +-q * 2^(E-127-(m-1)).  One lane per U = max(G, 16)
+// values (a 16-value unit of groups of 4 or 8, or one group).  P0 / P1: the
+// plane formats (launch.h); with two planes q = c0 * 2^s + c1, s = 2 when
 // plane 1 is a Lo2 plane and 4 otherwise (both chunks carry the sign).
 template <int G, int NCH, int P0, int P1>
 __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ mant, const uint8_t* __restrict__ exps,
-                                                    int64_t ngroups, int m, float* __restrict__ y) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (gid >= ngroups) return;
+                                                    int64_t nunits, int m, float* __restrict__ y) {
+  constexpr int U = G < 16 ? 16 : G, NGU = U / G;
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (u >= nunits) return;
   constexpr int PK[2] = {P0, P1};
-  constexpr int B0 = P0 != kPlaneFP6 ? G / 2 : G * 3 / 4;  // bytes per group in plane 0
-  uint32_t w[NCH][G * 6 / 32];
+  constexpr int B0 = P0 != kPlaneFP6 ? U / 2 : U * 3 / 4;  // bytes per unit in plane 0
+  uint32_t w[NCH][U * 6 / 32];
 #pragma unroll
   for (int p = 0; p < NCH; ++p) {
-    const int gb = PK[p] != kPlaneFP6 ? G / 2 : G * 3 / 4;
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(mant + p * ngroups * B0 + gid * gb);
+    const int gb = PK[p] != kPlaneFP6 ? U / 2 : U * 3 / 4;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(mant + p * nunits * B0 + u * gb);
 #pragma unroll
-    for (int i = 0; i < G * 6 / 32; ++i) w[p][i] = i < gb / 4 ? src[i] : 0u;
+    for (int i = 0; i < U * 6 / 32; ++i) w[p][i] = i < gb / 4 ? src[i] : 0u;
     if (PK[p] == kPlaneLo2) {
       // back to three FP6 code dwords per 16 values (last half first: in place)
 #pragma unroll
-      for (int u = G / 16 - 1; u >= 0; --u) {
+      for (int h = U / 16 - 1; h >= 0; --h) {
         uint32_t t0, t1, t2;
-        lo2_unpack(w[p][2 * u], w[p][2 * u + 1], t0, t1, t2);
-        w[p][3 * u] = t0;
-        w[p][3 * u + 1] = t1;
-        w[p][3 * u + 2] = t2;
+        lo2_unpack(w[p][2 * h], w[p][2 * h + 1], t0, t1, t2);
+        w[p][3 * h] = t0;
+        w[p][3 * h + 1] = t1;
+        w[p][3 * h + 2] = t2;
       }
     }
   }
-  const int e = (int)exps[gid] - 127 - (m - 1);
+  int e[NGU];
+#pragma unroll
+  for (int k = 0; k < NGU; ++k) e[k] = (int)exps[u * NGU + k] - 127 - (m - 1);
   auto chunk = [&](int p, int t) {
     if (PK[p] == kPlaneFP4) {
       const uint32_t nib = (w[p][t >> 3] >> (4 * (t & 7))) & 0xFu;
@@ -267,16 +287,16 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
     if (PK[p] == kPlaneLo2) return e2m3_eighth_decode(fp6_field(w[p], t));
     return e2m3_half_decode(fp6_field(w[p], t));
   };
-  float4* dst = reinterpret_cast<float4*>(y + gid * G);
+  float4* dst = reinterpret_cast<float4*>(y + u * U);
 #pragma unroll
-  for (int i = 0; i < G / 4; ++i) {
+  for (int i = 0; i < U / 4; ++i) {
     float v[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int t = 4 * i + k;
       int q = chunk(0, t);
       if (NCH == 2) q = q * (P1 == kPlaneLo2 ? 4 : 16) + chunk(NCH - 1, t);
-      v[k] = ldexpf((float)q, e);
+      v[k] = ldexpf((float)q, e[t / G]);
     }
     dst[i] = make_float4(v[0], v[1], v[2], v[3]);
   }
@@ -285,7 +305,7 @@ __global__ __launch_bounds__(256) void k_dequantize(const uint8_t* __restrict__ 
 template <int G, int MODE, int NCH, int P0, bool ADAPT = false, int P1 = kPlaneFP6>
 static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t seed, uint8_t* mant0, uint8_t* mant1,
                                 uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
-  constexpr int GPL = G == 16 ? 2 : 1;  // groups per lane (as in the kernel)
+  constexpr int GPL = G <= 16 ? 32 / G : 1;  // groups per lane (as in the kernel)
   const int64_t blocks = (ngroups + 256 * GPL - 1) / (256 * GPL);
   hipLaunchKernelGGL((k_quantize_rows<G, MODE, NCH, ADAPT, P0, P1>), dim3((unsigned)blocks), dim3(256), 0, s, x, ngroups,
                      (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
@@ -295,9 +315,9 @@ static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t
 template <int G, int MODE, int NCH, int P0, bool ADAPT = false, int P1 = kPlaneFP6>
 static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant0,
                                 uint8_t* mant1, uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
-  constexpr int NGT = 8;
-  const int64_t gpr = R / G;
-  const int64_t nbx = (C + 63) / 64, nby = (gpr + 4 * NGT - 1) / (4 * NGT);
+  constexpr int NGT = G == 64 ? 2 : 8;  // (the LDS gather holds 4 * NGT units of 64 columns)
+  const int64_t upr = R / (G < 16 ? 16 : G);  // units per output row (as in the kernel)
+  const int64_t nbx = (C + 63) / 64, nby = (upr + 4 * NGT - 1) / (4 * NGT);
   hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, P0, P1>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
                      C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
   return hipGetLastError();
@@ -311,17 +331,19 @@ static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uin
     if (m <= 6) return FN<G, MODE, 2, kPlaneFP6, false, kPlaneLo2>(__VA_ARGS__);  \
     return FN<G, MODE, 2, kPlaneFP6>(__VA_ARGS__);                                \
   } while (0)
+#define FASTBFP_QUANT_G(FN, G, ...)                                               \
+  do {                                                                            \
+    if (mode == kNearest) FASTBFP_QUANT_M(FN, G, kNearest, __VA_ARGS__);          \
+    if (mode == kStochastic) FASTBFP_QUANT_M(FN, G, kStochastic, __VA_ARGS__);    \
+    FASTBFP_QUANT_M(FN, G, kTruncate, __VA_ARGS__);                               \
+  } while (0)
 #define FASTBFP_DISPATCH_QUANT(FN, ...)                                           \
   do {                                                                            \
-    if (g == 16) {                                                                \
-      if (mode == kNearest) FASTBFP_QUANT_M(FN, 16, kNearest, __VA_ARGS__);       \
-      if (mode == kStochastic) FASTBFP_QUANT_M(FN, 16, kStochastic, __VA_ARGS__); \
-      FASTBFP_QUANT_M(FN, 16, kTruncate, __VA_ARGS__);                            \
-    } else {                                                                      \
-      if (mode == kNearest) FASTBFP_QUANT_M(FN, 32, kNearest, __VA_ARGS__);       \
-      if (mode == kStochastic) FASTBFP_QUANT_M(FN, 32, kStochastic, __VA_ARGS__); \
-      FASTBFP_QUANT_M(FN, 32, kTruncate, __VA_ARGS__);                            \
-    }                                                                             \
+    if (g == 4) FASTBFP_QUANT_G(FN, 4, __VA_ARGS__);                              \
+    if (g == 8) FASTBFP_QUANT_G(FN, 8, __VA_ARGS__);                              \
+    if (g == 16) FASTBFP_QUANT_G(FN, 16, __VA_ARGS__);                            \
+    if (g == 32) FASTBFP_QUANT_G(FN, 32, __VA_ARGS__);                            \
+    FASTBFP_QUANT_G(FN, 64, __VA_ARGS__);                                         \
   } while (0)
 
 hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,
@@ -605,8 +627,9 @@ hipError_t launch_weight_update(const float* w, const float* dw, float alpha, fl
 template <int G, int NCH, int P0, int P1 = kPlaneFP6>
 static hipError_t launch_deq_t(const uint8_t* mant, const uint8_t* exps, int64_t ngroups, int m, float* y,
                                hipStream_t s) {
-  const unsigned blocks = (unsigned)((ngroups + 255) / 256);
-  hipLaunchKernelGGL((k_dequantize<G, NCH, P0, P1>), dim3(blocks), dim3(256), 0, s, mant, exps, ngroups, m, y);
+  const int64_t nunits = G < 16 ? ngroups * G / 16 : ngroups;
+  const unsigned blocks = (unsigned)((nunits + 255) / 256);
+  hipLaunchKernelGGL((k_dequantize<G, NCH, P0, P1>), dim3(blocks), dim3(256), 0, s, mant, exps, nunits, m, y);
   return hipGetLastError();
 }
 
@@ -623,7 +646,13 @@ hipError_t launch_dequantize(const uint8_t* mant, const uint8_t* exps, int64_t r
                              float* y, hipStream_t s) {
   const int64_t ngroups = rows * (len / g);
   if (ngroups == 0) return hipSuccess;
-  return g == 16 ? launch_deq_g<16>(mant, exps, ngroups, m, y, s) : launch_deq_g<32>(mant, exps, ngroups, m, y, s);
+  switch (g) {
+    case 4: return launch_deq_g<4>(mant, exps, ngroups, m, y, s);
+    case 8: return launch_deq_g<8>(mant, exps, ngroups, m, y, s);
+    case 16: return launch_deq_g<16>(mant, exps, ngroups, m, y, s);
+    case 32: return launch_deq_g<32>(mant, exps, ngroups, m, y, s);
+    default: return launch_deq_g<64>(mant, exps, ngroups, m, y, s);
+  }
 }
 
 }  // namespace fastbfp

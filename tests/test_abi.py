@@ -69,7 +69,13 @@ def test_quantized_sizes(lib):
         assert lib.bfp_quantized_sizes(5, 96, 16, m, ctypes.byref(mb), ctypes.byref(eb)) == OK
         assert (mb.value, eb.value) == (5 * 96 * bits // 8, 5 * 6), m
     assert lib.bfp_quantized_sizes(3, 40, 16, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_SHAPE
-    assert lib.bfp_quantized_sizes(3, 64, 8, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_UNSUP
+    # g in {4, 8, 16, 32, 64}; rows hold whole 16-value units
+    for g, m, nbytes in ((4, 4, 3 * 64 * 6 // 8), (8, 2, 3 * 64 * 4 // 8), (64, 6, 3 * 64 * 10 // 8)):
+        assert lib.bfp_quantized_sizes(3, 64, g, m, ctypes.byref(mb), ctypes.byref(eb)) == OK
+        assert (mb.value, eb.value) == (nbytes, 3 * 64 // g), g
+    assert lib.bfp_quantized_sizes(3, 40, 8, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_SHAPE  # 40 % 16
+    assert lib.bfp_quantized_sizes(3, 64, 12, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_UNSUP
+    assert lib.bfp_quantized_sizes(3, 128, 128, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_UNSUP
     assert lib.bfp_quantized_sizes(3, 64, 16, 9, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC
     assert lib.bfp_quantized_sizes(3, 64, 16, 0, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC
     assert lib.bfp_quantized_sizes(-1, 64, 16, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_ARG
@@ -91,7 +97,8 @@ def test_quantize_validation(lib):
     assert q(lib, mode=-1) == E_ARG
     assert q(lib, C=40) == E_SHAPE
     assert q(lib, R=40, axis=0) == E_SHAPE
-    assert q(lib, g=8) == E_UNSUP
+    assert q(lib, g=12) == E_UNSUP and q(lib, g=128, C=128) == E_UNSUP
+    assert q(lib, g=8, C=40) == E_SHAPE
     assert q(lib, g=0) == E_ARG
     assert q(lib, m=9) == E_PREC
     assert q(lib, m=0) == E_PREC
@@ -111,15 +118,14 @@ def test_gemm_validation(lib):
     assert gm(lib, ae=None) == E_ARG
     assert gm(lib, K=40) == E_SHAPE
     assert gm(lib, ldc=7) == E_SHAPE
-    assert gm(lib, g=8) == E_UNSUP
+    assert gm(lib, g=128, K=128) == E_UNSUP and gm(lib, g=8, K=24) == E_SHAPE
+    assert gm(lib, g=8, M=0) == OK and gm(lib, g=64, M=0) == OK and gm(lib, g=4, M=0) == OK
     assert gm(lib, M=-1) == E_ARG
     assert gm(lib, am=9) == E_PREC
-    assert gm(lib, ma=3) == E_PREC          # m=4 is one chunk: nothing to drop
-    assert gm(lib, am=8, ma=5) == E_PREC    # only whole 4-bit chunks can be dropped
+    # any precision from 1 to the stored width (M = 0: accepted, nothing launched)
+    assert gm(lib, ma=3, M=0) == OK and gm(lib, am=8, ma=5, M=0) == OK and gm(lib, bm=6, mb=1, M=0) == OK
     assert gm(lib, am=4, ma=5) == E_PREC    # cannot raise precision
-    assert gm(lib, bm=6, mb=1) == E_PREC
-    assert gm(lib, bm=6, mb=2) == E_PREC    # m = 6 drops a 2-bit chunk (to 4), m = 8 a 4-bit one
-    assert gm(lib, am=8, ma=6) == E_PREC
+    assert gm(lib, ma=0) == E_PREC and gm(lib, bm=6, mb=7) == E_PREC
     assert gm(lib, a=ctypes.c_void_p(0x100001)) == E_ARG
     assert gm(lib, M=0) == OK and gm(lib, N=0, ldc=0) == OK
     # 32-bit tile offsets: K up to 11184784 (256 rows of FP6 codes < 2^31 bytes)
@@ -141,6 +147,9 @@ def test_gemm_tiled_validation(lib):
     assert gmt(lib, 3, g=32) == E_UNSUP                  # groups of 32: default tile only
     assert gmt(lib, 1, am=6, ma=4, M=0) == OK            # the low chunk dropped: one plane, empty
     assert gmt(lib, 0, am=6, ma=6, M=0) == OK and gmt(lib, -1, g=32, N=0, ldc=0) == OK
+    # products the block-scaled kernel does not take run on the general kernel: no tile to force
+    assert gmt(lib, 0, am=6, ma=3, M=0) == E_UNSUP and gmt(lib, 3, g=8, M=0) == E_UNSUP
+    assert gmt(lib, -1, am=6, ma=3, M=0) == OK and gmt(lib, -1, g=8, M=0) == OK
     assert gmt(lib, 2, K=40) == E_SHAPE and gmt(lib, 3, C=None) == E_ARG and gmt(lib, 1, ldc=7) == E_SHAPE
 
 
@@ -149,7 +158,8 @@ def test_group_partials_validation(lib):
     assert f(None, 4, FAKE, 4, 8, 8, 64, 16, 4, 4, FAKE, None) == E_ARG
     assert f(FAKE, 4, FAKE, 4, 8, 8, 64, 16, 4, 4, None, None) == E_ARG
     assert f(FAKE, 4, FAKE, 4, 8, 8, 60, 16, 4, 4, FAKE, None) == E_SHAPE
-    assert f(FAKE, 8, FAKE, 4, 8, 8, 64, 16, 3, 4, FAKE, None) == E_PREC
+    assert f(FAKE, 8, FAKE, 4, 8, 8, 64, 16, 9, 4, FAKE, None) == E_PREC
+    assert f(FAKE, 8, FAKE, 4, 8, 8, 64, 16, 3, 4, None, None) == E_ARG  # any lowering; P is null
     assert f(FAKE, 4, FAKE, 4, 0, 8, 64, 16, 4, 4, FAKE, None) == OK
 
 
@@ -237,7 +247,7 @@ def test_gemm_bfp_validation(lib):
     assert gb(lib, N=24) == E_SHAPE            # C's rows are grouped by 16
     assert gb(lib, K=40) == E_SHAPE
     assert gb(lib, cm=0) == E_PREC and gb(lib, cm=9) == E_PREC
-    assert gb(lib, am=8, ma=5) == E_PREC
+    assert gb(lib, am=8, ma=5) == E_UNSUP and gb(lib, g=8) == E_UNSUP  # the block-scaled kernel only
     assert gb(lib, g=8, K=64) == E_UNSUP
     assert gb(lib, cmant=ctypes.c_void_p(0x100002)) == E_ARG
     assert gb(lib, st=ctypes.c_void_p(0x100001)) == E_ARG
