@@ -26,7 +26,7 @@
  *   - All entry points are thread-safe.
  *
  * BFP tensor layout (rows x len values, groups of g consecutive values along
- * len; g in {16, 32}; len % g == 0)
+ * len; g in {4, 8, 16, 32, 64}; len a multiple of g and of 16)
  *   exp  : uint8 [rows][len/g]   shared exponent E = the largest FP32 biased
  *          exponent field in the group (0 for a group of zeros/subnormals).
  *          One unit in the last place of the group is 2^(E - 127 - (m-1)).
@@ -51,7 +51,10 @@
  *          group takes B_c = g/2 (FP4, Lo2) or 3g/4 (FP6) bytes in plane c:
  *            plane 0, row r, group G at byte offset (r * (len/g) + G) * B_0,
  *            plane 1 at rows * (len/g) * B_0 + (r * (len/g) + G) * B_1.
- *          A group of 32 is laid out as two consecutive groups of 16.
+ *          The planes are laid out in 16-value units: a group of 32 or 64 is
+ *          two or four consecutive units, and a unit holds 4 groups of 4 or 2
+ *          of 8 (their codes in the unit's order).  A Lo2 plane is defined per
+ *          unit only.
  *          A zero chunk is stored as code 0 (no sign).
  *          This is the paper's chunk-plane storage (section V-D): each plane
  *          holds one chunk of every value with its sign, the upper chunk's
@@ -100,9 +103,9 @@ const char* bfp_status_str(int status);
 int bfp_chunks(int m_bits);
 
 /* Host-side sizes of the two BFP arrays for a rows x len tensor.
- * Returns BFP_E_ARG for null outputs or negative sizes, BFP_E_SHAPE if
- * len % g != 0, BFP_E_UNSUPPORTED for g not in {16, 32}, BFP_E_PRECISION for m
- * outside 1..8. */
+ * Returns BFP_E_ARG for null outputs or negative sizes, BFP_E_SHAPE if len is
+ * not a multiple of g and of 16, BFP_E_UNSUPPORTED for g not in
+ * {4, 8, 16, 32, 64}, BFP_E_PRECISION for m outside 1..8. */
 int bfp_quantized_sizes(int64_t rows, int64_t len, int g, int m_bits, size_t* mant_bytes, size_t* exp_bytes);
 
 /*
@@ -116,7 +119,8 @@ int bfp_quantized_sizes(int64_t rows, int64_t len, int g, int m_bits, size_t* ma
  *                 len = R (transpose-on-quantize: every GEMM operand is then
  *                 K-contiguous, which serves the transposed operands of the
  *                 backward GEMMs of section II-B).
- *   g           : 16 or 32; must divide the grouped axis.
+ *   g           : 4, 8, 16, 32 or 64; the grouped axis must be a multiple of g
+ *                 and of 16 (BFP_E_SHAPE otherwise).
  *   m_bits      : magnitude width 1..8 (a sign bit is kept besides).
  *   round_mode  : bfp_round_t.
  *   seed        : stochastic rounding only.  The noise byte of output value t
@@ -151,20 +155,28 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
  *   P_G     = sum_{k in G} qa[i][k] * qb[j][k]   (exact integer products).
  * The products are exact; the cross-group sum is accumulated in FP32.
  *   a_mant/a_exp : A stored with a_m_bits (rows M, len K); likewise B (rows N).
- *   m_a, m_b     : the precisions the product is taken at.  Either the stored
- *                  width, or, for a two-chunk operand, the width of its upper
- *                  chunk (m - 2 for m = 5, 6; m - 4 for m = 7, 8): the low
- *                  chunk plane is then skipped, i.e. the magnitude is
- *                  truncated to its top bits (the paper's discard of a
- *                  low-order chunk, section V-D).  Anything else returns
- *                  BFP_E_PRECISION.
+ *   m_a, m_b     : the precisions the product is taken at, 1 .. the stored
+ *                  width (BFP_E_PRECISION otherwise): each magnitude is
+ *                  truncated to its top m_a (m_b) bits, the paper's discard of
+ *                  low-order bits (section V-D).  The width of a two-chunk
+ *                  operand's upper chunk (m - 2 for m = 5, 6; m - 4 for
+ *                  m = 7, 8) simply skips the low chunk plane.
  *   Passes: one block-scaled MFMA per chunk-plane pair and group pair, the
  *   counterpart of the paper's (m_a/2)(m_b/2) fMAC rounds -- except that an
  *   operand split at 2 bits (m = 5, 6) puts both of its chunks in one
  *   32-value MFMA block, so it adds no pass of its own: (6,6) takes 2 MFMAs
  *   per group of 16, (6, m <= 4) 1.
- *   g            : 16 or 32 (both operands).  A group of 32 fills a whole
- *                  MFMA block; a group of 16 leaves half of it zero.
+ *   g            : 4, 8, 16, 32 or 64 (both operands); K a multiple of g and
+ *                  of 16.  Groups of 16 and 32 at the stored width or with a
+ *                  low chunk plane dropped run on the block-scaled MFMA
+ *                  kernel (a group of 32 fills a whole MFMA block; a group of
+ *                  16 leaves half of it zero, except for operands split at 2
+ *                  bits).  Every other case -- groups of 4, 8 or 64, or a
+ *                  precision that is not a chunk boundary -- runs on a
+ *                  general kernel: int8 MFMA on the decoded, truncated
+ *                  magnitudes of one group at a time, each exact integer
+ *                  group partial scaled exactly by its power of two and added
+ *                  in FP32 (same result contract, lower throughput).
  *   C            : FP32 with row stride ldc >= N (elements).
  *   Size limits  : M, N < 2^31, K <= 11184784 (256 rows of 12 bytes per 16
  *                  values stay below 2^31 bytes: the kernels address operand
@@ -187,6 +199,8 @@ int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const ui
  *   tile =  1, 2, 3, 4 : 256 x 128, 256 x 64, 128 x 64, 128 x 128 -- only for
  *               one chunk plane per operand (m_a, m_b <= 4) with g = 16, else
  *               BFP_E_UNSUPPORTED.
+ * A product that bfp_gemm runs on its general kernel takes only tile = -1
+ * (BFP_E_UNSUPPORTED otherwise).
  * For one-chunk, g = 16 products bfp_gemm picks 128 x 64 when N <= 64;
  * 256 x 128 when A's plane holds FP4 codes (A stored with m = 1, 2, 5 or 6);
  * otherwise 256 x 256, or 128 x 128 when N <= 128; and it steps down to a
@@ -209,8 +223,10 @@ int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, co
  * axis 1, g = 16, c_m_bits, round_mode, seed) of the FP32 C that bfp_gemm
  * computes: the same values, the same noise addressing (gid = the index into
  * c_exp), without writing or re-reading FP32 C.
- *   Operands and precisions : as bfp_gemm (g = 16 or 32 for the operands;
- *                 the output is grouped by 16).
+ *   Operands and precisions : as bfp_gemm, for the products bfp_gemm runs
+ *                 on its block-scaled kernel only (groups of 16 or 32, each
+ *                 operand at its stored width or without its low chunk plane;
+ *                 BFP_E_UNSUPPORTED otherwise); the output is grouped by 16.
  *   c_m_bits    : 1..8.  round_mode, seed, status_word : as bfp_quantize.
  *   c_mant, c_exp : outputs sized by bfp_quantized_sizes(M, N, 16, c_m_bits).
  * N must be a multiple of 16 (BFP_E_SHAPE otherwise).
@@ -223,11 +239,12 @@ int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, cons
  * bfp_gemm_group_partials -- the exact integer group dot products
  *   P[G][i][j] = sum_{k in G} qa'[i][k] * qb'[j][k]
  * (parts M and A of section III-B), qa' and qb' being the magnitudes at m_a and
- * m_b bits with their signs, computed with int8 MFMA and combined across chunk
- * planes in integers (sum of 2^(4(ca+cb)) * P_{ca,cb}).  P is int32
- * [K/g][M][N].  Meant for verification: it writes K/g times more output than
- * bfp_gemm.  Same operand and precision rules as bfp_gemm (the exponents do not
- * enter P, so only the mantissa planes are passed).
+ * m_b bits with their signs, computed with int8 MFMA on the decoded
+ * magnitudes (an 8-bit magnitude as two 4-bit chunks combined in integers).
+ * P is int32 [K/g][M][N].  Meant for verification: it writes K/g times more
+ * output than bfp_gemm.  Same operand, group-size and precision rules as
+ * bfp_gemm (the exponents do not enter P, so only the mantissa planes are
+ * passed).
  */
 int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* b_mant, int b_m_bits, int64_t M,
                             int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream);
@@ -278,7 +295,8 @@ int bfp_weight_update(const float* w, const float* dw, float alpha, float* w_out
  * discarded (same shared exponents: value +-(q >> 2) * 2^(E - 128)); and
  *   sums[0] = sum_n |BFP(X_n, 4) - BFP(X_n, 2)|,  sums[1] = sum_n |BFP(X_n, 2)|,
  * so that r(X) = sums[0] / sums[1] (Eq. 2).
- *   x, R, C, group_axis, g, round_mode, seed, status_word : as bfp_quantize.
+ *   x, R, C, group_axis, round_mode, seed, status_word : as bfp_quantize.
+ *   g           : 16 or 32 (BFP_E_UNSUPPORTED otherwise).
  *   mant4, exp  : the m = 4 tensor (layout of bfp_quantize, m_bits = 4).
  *   mant2       : optional (may be NULL): the m = 2 tensor's mantissas (layout
  *                 of bfp_quantize, m_bits = 2: one plane of 4-bit codes, two
