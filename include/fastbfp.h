@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define FASTBFP_ABI_VERSION 5
+#define FASTBFP_ABI_VERSION 6
 
 typedef enum {
   BFP_ROUND_NEAREST = 0,    /* add half an LSB, then truncate (ties away from zero) */
@@ -139,6 +139,28 @@ int bfp_quantized_sizes(int64_t rows, int64_t len, int g, int m_bits, size_t* ma
  */
 int bfp_quantize(const float* x, int64_t R, int64_t C, int group_axis, int g, int m_bits, int round_mode,
                  uint64_t seed, uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream);
+
+/*
+ * bfp_quantize_nd -- bfp_quantize of an N-dimensional tensor grouped along any
+ * one axis (section III-A; the backward GEMMs of section II-B group their
+ * operands along other axes than the forward ones).
+ *   x           : FP32, contiguous row-major with ndim dimensions shape[0..ndim)
+ *                 (host array of ndim >= 1 sizes, each >= 0).
+ *   group_axis  : 0 <= group_axis < ndim; shape[group_axis] is a multiple of g
+ *                 and of 16 (BFP_E_SHAPE otherwise).
+ *   Output      : the BFP tensor with the group axis innermost: rows = the
+ *                 product of the other sizes in their order (the row of index
+ *                 (i_0, .., i_{a-1}, i_{a+1}, .., i_{n-1}) is that index in
+ *                 row-major order), len = shape[group_axis]; the layout and
+ *                 the noise addressing (gid = row * len/g + group) as
+ *                 bfp_quantize.  The last axis is bfp_quantize with group_axis
+ *                 1 and R = the product of the others; axis 0 of a 2-D tensor
+ *                 is group_axis 0.
+ *   The rest    : as bfp_quantize.  BFP_E_UNSUPPORTED if a size product
+ *                 exceeds 2^62 or the launch would exceed 2^31 workgroups.
+ */
+int bfp_quantize_nd(const float* x, int ndim, const int64_t* shape, int group_axis, int g, int m_bits, int round_mode,
+                    uint64_t seed, uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream);
 
 /*
  * bfp_dequantize -- BFP -> FP32: y[r][k] = +-q * 2^(E - 127 - (m-1)), the value

@@ -83,14 +83,13 @@ def _need_cuda(t: torch.Tensor, name: str, dtype=None):
 
 def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rounding: str = "nearest",
              seed: int = 0, status: torch.Tensor | None = None, out: BFPTensor | None = None) -> BFPTensor:
-    """FP32 -> BFP with groups of g along ``group_axis``.
-
-    group_axis -1 (or the last axis): groups along the last axis; leading axes
-    are flattened into rows.  group_axis 0 of a 2-D [R, C] tensor: groups down
-    the columns, written transposed as a [C, R] BFP tensor (K-contiguous for
-    the GEMM).  ``status``: optional int32/uint32 CUDA scalar whose bit 0 is set
-    on Inf/NaN input.  ``out``: optional preallocated BFPTensor of the result
-    shape (no allocation happens then).
+    """FP32 -> BFP with groups of g along ``group_axis`` (any axis of an N-D
+    tensor): a BFPTensor with the group axis innermost, rows = the other
+    axes' indices in order.  So the last axis keeps the leading axes as rows,
+    and axis 0 of a 2-D [R, C] tensor is written transposed as a [C, R] BFP
+    tensor (K-contiguous for the GEMM).  ``status``: optional int32/uint32
+    CUDA scalar whose bit 0 is set on Inf/NaN input.  ``out``: optional
+    preallocated BFPTensor of the result shape (no allocation happens then).
     """
     _need_cuda(x, "x", torch.float32)
     if rounding not in ROUNDING:
@@ -99,15 +98,8 @@ def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rou
         raise ValueError("x must have at least one dimension")
     nd = x.dim()
     ax = group_axis % nd
-    if ax == nd - 1:
-        C = x.shape[-1]
-        R = math.prod(x.shape[:-1])  # leading axes flattened into rows (also when C = 0)
-        axis_flag, rows, length = 1, R, C
-    elif nd == 2 and ax == 0:
-        R, C = x.shape
-        axis_flag, rows, length = 0, C, R
-    else:
-        raise ValueError("group_axis must be the last axis, or 0 of a 2-D tensor")
+    length = x.shape[ax]
+    rows = math.prod(x.shape[:ax]) * math.prod(x.shape[ax + 1:])
     t = out if out is not None else BFPTensor.empty(rows, length, g, m, x.device)
     if (t.rows, t.len, t.g, t.m) != (rows, length, g, m):
         raise ValueError("out has the wrong shape or format")
@@ -115,10 +107,16 @@ def quantize(x: torch.Tensor, group_axis: int = -1, g: int = 16, m: int = 4, rou
     if status is not None:
         _need_cuda(status, "status")
         st_ptr = ctypes.c_void_p(status.data_ptr())
-    lib = load()
-    check(lib.bfp_quantize(ctypes.c_void_p(x.data_ptr()), R, C, axis_flag, g, m, ROUNDING[rounding],
-                           ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(t.mant.data_ptr()),
-                           ctypes.c_void_p(t.exp.data_ptr()), st_ptr, _stream(x.device)), "bfp_quantize")
+    seed_c = ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF)
+    ptrs = (ctypes.c_void_p(t.mant.data_ptr()), ctypes.c_void_p(t.exp.data_ptr()), st_ptr, _stream(x.device))
+    if ax == nd - 1 or (nd == 2 and ax == 0):  # the 2-D entry point: rows of [R, C], or its columns
+        R, C = (rows, length) if ax == nd - 1 else tuple(x.shape)
+        check(load().bfp_quantize(ctypes.c_void_p(x.data_ptr()), R, C, 1 if ax == nd - 1 else 0, g, m,
+                                  ROUNDING[rounding], seed_c, *ptrs), "bfp_quantize")
+    else:
+        shape = (ctypes.c_int64 * nd)(*x.shape)
+        check(load().bfp_quantize_nd(ctypes.c_void_p(x.data_ptr()), nd, shape, ax, g, m, ROUNDING[rounding], seed_c,
+                                     *ptrs), "bfp_quantize_nd")
     return t
 
 

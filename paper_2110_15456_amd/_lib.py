@@ -24,6 +24,7 @@ SIGNATURES = {
     "bfp_quantized_sizes": (_I, [_I64, _I64, _I, _I, ctypes.POINTER(ctypes.c_size_t),
                                  ctypes.POINTER(ctypes.c_size_t)]),
     "bfp_quantize": (_I, [_P, _I64, _I64, _I, _I, _I, _I, _U64, _P, _P, _P, _P]),
+    "bfp_quantize_nd": (_I, [_P, _I, _P, _I, _I, _I, _I, _U64, _P, _P, _P, _P]),
     "bfp_dequantize": (_I, [_P, _P, _I64, _I64, _I, _I, _P, _P]),
     "bfp_gemm": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _I64, _P]),
     "bfp_gemm_tiled": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _I64, _I, _P]),
@@ -40,7 +41,7 @@ SIGNATURES = {
     "bfp_adaptive_threshold": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, _I64, _I64, _I64, _I64]),
     "bfp_adaptive_mantissa": (_I, [ctypes.c_double, ctypes.c_double, ctypes.c_double]),
 }
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 _lock = threading.Lock()
 _lib = None

@@ -124,9 +124,43 @@ int bfp_quantize(const float* x, int64_t R, int64_t C, int group_axis, int g, in
   if (!x || !mant || !exp) return BFP_E_ARG;
   if (!aligned(x, group_axis == 1 ? 16 : 4) || !aligned(mant, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (group_axis == 1)
+  if (group_axis == 1) {
+    if (fastbfp::quantize_rows_blocks(R, C, g) > 0x7fffffff) return BFP_E_UNSUPPORTED;
     return status_of(fastbfp::launch_quantize_rows(x, R, C, g, m_bits, round_mode, seed, mant, exp, status_word, s));
+  }
+  if (fastbfp::quantize_cols_blocks(R, C, g, 1) > 0x7fffffff) return BFP_E_UNSUPPORTED;
   return status_of(fastbfp::launch_quantize_cols(x, R, C, g, m_bits, round_mode, seed, mant, exp, status_word, s));
+}
+
+int bfp_quantize_nd(const float* x, int ndim, const int64_t* shape, int group_axis, int g, int m_bits, int round_mode,
+                    uint64_t seed, uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream) {
+  if (ndim < 1 || !shape || group_axis < 0 || group_axis >= ndim) return BFP_E_ARG;
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  // outer axes x group axis x inner axes; the output rows are the outer and
+  // inner indices in order
+  int64_t outer = 1, inner = 1;
+  const int64_t L = shape[group_axis];
+  for (int d = 0; d < ndim; ++d) {
+    if (shape[d] < 0) return BFP_E_ARG;
+    if (d == group_axis) continue;
+    int64_t& acc = d < group_axis ? outer : inner;
+    if (shape[d] != 0 && acc > (int64_t(1) << 62) / shape[d]) return BFP_E_UNSUPPORTED;
+    acc *= shape[d];
+  }
+  if (inner != 0 && outer > (int64_t(1) << 62) / inner) return BFP_E_UNSUPPORTED;
+  const int st = check_tensor(outer * inner, L, g, m_bits);
+  if (st != BFP_OK) return st;
+  if (outer == 0 || inner == 0 || L == 0) return BFP_OK;
+  if (!x || !mant || !exp) return BFP_E_ARG;
+  if (!aligned(x, inner == 1 ? 16 : 4) || !aligned(mant, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (inner == 1) {
+    if (fastbfp::quantize_rows_blocks(outer, L, g) > 0x7fffffff) return BFP_E_UNSUPPORTED;
+    return status_of(fastbfp::launch_quantize_rows(x, outer, L, g, m_bits, round_mode, seed, mant, exp, status_word, s));
+  }
+  if (fastbfp::quantize_cols_blocks(L, inner, g, outer) > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  return status_of(
+      fastbfp::launch_quantize_cols(x, L, inner, g, m_bits, round_mode, seed, mant, exp, status_word, s, outer));
 }
 
 int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int g, int m_bits, float* y,

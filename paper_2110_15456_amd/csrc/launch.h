@@ -37,8 +37,15 @@ __host__ __device__ constexpr int plane_group_bytes(int g, int m, int p) {
 
 hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
+// Groups down the columns of x[R][C], written transposed (rows = C, len = R);
+// with nbatch > 1, of each of the matrices x[nbatch][R][C], slice b's output
+// rows following slice b - 1's.
 hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
-                                uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
+                                uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s, int64_t nbatch = 1);
+// Workgroups launch_quantize_cols / launch_quantize_rows start (the caller
+// keeps them below 2^31).
+int64_t quantize_cols_blocks(int64_t R, int64_t C, int g, int64_t nbatch);
+int64_t quantize_rows_blocks(int64_t rows, int64_t len, int g);
 // Adaptive precision (Algorithm 1, Eq. 2): quantize at m = 4 into mant4/exps,
 // optionally write the low-chunk-discarded 2-bit mantissas to mant2, and set
 // sums[0] = sum |BFP(X,4) - BFP(X,2)|, sums[1] = sum |BFP(X,2)| (sums holds

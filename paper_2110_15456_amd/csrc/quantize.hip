@@ -176,7 +176,8 @@ __global__ __launch_bounds__(256) void k_quantize_rows(const float* __restrict__
 // every store instruction writes contiguous bytes of one output row.
 template <int G, int MODE, int NCH, int NGT, bool ADAPT, int P0, int P1>
 __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__ x, int64_t R, int64_t C,
-                                                       int64_t nbx, uint32_t m, uint32_t key0, uint32_t key1,
+                                                       int64_t nbx, int64_t nbxy, uint32_t m, uint32_t key0,
+                                                       uint32_t key1,
                                                        uint8_t* __restrict__ mant0, uint8_t* __restrict__ mant1,
                                                        uint8_t* __restrict__ exps, uint32_t* status, double* part) {
   // A step converts U = max(G, 16) consecutive values of a column: NGU = U / G
@@ -188,7 +189,13 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
   constexpr int ROWW = JB * WPG;          // LDS row stride, code dwords per output row
   __shared__ uint32_t sc[NCH][64][ROWW];
   __shared__ uint8_t se[64][JB * NGU];
-  const int64_t bx = blockIdx.x % nbx, by = blockIdx.x / nbx;
+  // A batch of matrices x[nbatch][R][C] (one launch for every slice of a
+  // tensor grouped along an axis that is neither first nor last): slice b's
+  // output rows are b * C .. b * C + C - 1.
+  const int64_t batch = blockIdx.x / nbxy, bid = blockIdx.x % nbxy;
+  const int64_t bx = bid % nbx, by = bid / nbx;
+  x += batch * R * C;
+  const int64_t row_base = batch * C;
   const int lane = threadIdx.x & 63, slot = threadIdx.x >> 6;
   const int64_t c0 = bx * 64, c = c0 + lane;
   const int64_t gpr = R / G, upr = R / U;  // groups and units per output row
@@ -208,7 +215,8 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
       uint32_t w[NCH][WPG];
       uint32_t E[NGU], s_lo[NGU], s_hi[NGU];
       bool nonfinite;
-      quantize_groups<G, NGU, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)(c * gpr + j * NGU), key0, key1, w, E,
+      quantize_groups<G, NGU, MODE, NCH, ADAPT, P0, P1, true>(b, m, (uint64_t)((row_base + c) * gpr + j * NGU), key0,
+                                                             key1, w, E,
                                                              nonfinite, s_lo, s_hi);
       if (ADAPT) {
         num += ldexp((double)s_lo[0], (int)E[0] - 130);
@@ -233,14 +241,14 @@ __global__ __launch_bounds__(256) void k_quantize_cols(const float* __restrict__
     for (int d = threadIdx.x; d < ncols * rw; d += 256) {
       const int r = d / rw, k = d % rw;
       if (k < jn * WP[p]) {
-        const int64_t o = ((c0 + r) * upr + jb) * WP[p] + k;
+        const int64_t o = ((row_base + c0 + r) * upr + jb) * WP[p] + k;
         reinterpret_cast<uint32_t*>(p ? mant1 : mant0)[o] = sc[p][r][k];
       }
     }
   }
   for (int d = threadIdx.x; d < ncols * JB * NGU; d += 256) {
     const int r = d / (JB * NGU), k = d % (JB * NGU);
-    if (k < jn * NGU) exps[(c0 + r) * gpr + jb * NGU + k] = se[r][k];
+    if (k < jn * NGU) exps[(row_base + c0 + r) * gpr + jb * NGU + k] = se[r][k];
   }
   if (status && any_bad) atomicOr(status, 1u);
 }
@@ -314,12 +322,15 @@ static hipError_t launch_rows_t(const float* x, int64_t ngroups, int m, uint64_t
 
 template <int G, int MODE, int NCH, int P0, bool ADAPT = false, int P1 = kPlaneFP6>
 static hipError_t launch_cols_t(const float* x, int64_t R, int64_t C, int m, uint64_t seed, uint8_t* mant0,
-                                uint8_t* mant1, uint8_t* exps, uint32_t* status, double* part, hipStream_t s) {
+                                uint8_t* mant1, uint8_t* exps, uint32_t* status, double* part, hipStream_t s,
+                                int64_t nbatch = 1) {
   constexpr int NGT = G == 64 ? 2 : 8;  // (the LDS gather holds 4 * NGT units of 64 columns)
   const int64_t upr = R / (G < 16 ? 16 : G);  // units per output row (as in the kernel)
   const int64_t nbx = (C + 63) / 64, nby = (upr + 4 * NGT - 1) / (4 * NGT);
-  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, P0, P1>), dim3((unsigned)(nbx * nby)), dim3(256), 0, s, x, R,
-                     C, nbx, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps, status, part);
+  const int64_t nbxy = nbx * nby;
+  hipLaunchKernelGGL((k_quantize_cols<G, MODE, NCH, NGT, ADAPT, P0, P1>), dim3((unsigned)(nbxy * nbatch)), dim3(256), 0,
+                     s, x, R, C, nbx, nbxy, (uint32_t)m, (uint32_t)seed, (uint32_t)(seed >> 32), mant0, mant1, exps,
+                     status, part);
   return hipGetLastError();
 }
 
@@ -355,10 +366,21 @@ hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g
 }
 
 hipError_t launch_quantize_cols(const float* x, int64_t R, int64_t C, int g, int m, int mode, uint64_t seed,
-                                uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s) {
-  if (R == 0 || C == 0) return hipSuccess;
-  uint8_t* mant1 = mant + C * (R / g) * plane_group_bytes(g, m, 0);  // plane 1 when m > 4
-  FASTBFP_DISPATCH_QUANT(launch_cols_t, x, R, C, m, seed, mant, mant1, exps, status, nullptr, s);
+                                uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s, int64_t nbatch) {
+  if (R == 0 || C == 0 || nbatch == 0) return hipSuccess;
+  uint8_t* mant1 = mant + nbatch * C * (R / g) * plane_group_bytes(g, m, 0);  // plane 1 when m > 4
+  FASTBFP_DISPATCH_QUANT(launch_cols_t, x, R, C, m, seed, mant, mant1, exps, status, nullptr, s, nbatch);
+}
+
+int64_t quantize_rows_blocks(int64_t rows, int64_t len, int g) {
+  const int64_t per_block = 256 * (g <= 16 ? 32 / g : 1);  // groups per k_quantize_rows workgroup
+  const int64_t ngroups = (len / g) > 0 && rows > INT64_MAX / (len / g) ? INT64_MAX : rows * (len / g);
+  return (ngroups + per_block - 1) / per_block;
+}
+
+int64_t quantize_cols_blocks(int64_t R, int64_t C, int g, int64_t nbatch) {
+  const int64_t U = g < 16 ? 16 : g, NGT = g == 64 ? 2 : 8;
+  return ((C + 63) / 64) * ((R / U + 4 * NGT - 1) / (4 * NGT)) * nbatch;
 }
 
 // The adaptive specialisations: plane 0 the m = 4 codes (FP6), plane 1 (if

@@ -163,6 +163,26 @@ def test_group_partials_validation(lib):
     assert f(FAKE, 4, FAKE, 4, 0, 8, 64, 16, 4, 4, FAKE, None) == OK
 
 
+def test_quantize_nd_validation(lib):
+    f = lib.bfp_quantize_nd
+
+    def qn(shape, axis, g=16, m=4, mode=0, x=FAKE, mant=FAKE, exp=FAKE):
+        arr = (ctypes.c_int64 * max(1, len(shape)))(*shape)
+        return f(x, len(shape), arr, axis, g, m, mode, 0, mant, exp, None, None)
+
+    assert qn((4, 64, 8), 3) == E_ARG and qn((4, 64, 8), -1) == E_ARG
+    assert qn((), 0) == E_ARG
+    assert qn((4, -1, 8), 0) == E_ARG
+    assert qn((4, 40, 8), 1) == E_SHAPE          # the grouped axis: a multiple of g and of 16
+    assert qn((4, 24, 8), 1, g=8) == E_SHAPE
+    assert qn((4, 64, 8), 1, g=12) == E_UNSUP and qn((4, 64, 8), 1, m=9) == E_PREC
+    assert qn((4, 64, 8), 1, mode=3) == E_ARG
+    assert qn((4, 64, 8), 1, x=None) == E_ARG
+    assert qn((0, 64, 8), 1) == OK and qn((4, 64, 0), 1) == OK and qn((4, 0, 8), 1) == OK
+    assert qn((1 << 32, 1 << 31, 16), 2) == E_UNSUP  # more than 2^62 rows
+    assert qn((1 << 40, 1 << 4), 1) == E_UNSUP       # more than 2^31 workgroups
+
+
 def test_dequantize_validation(lib):
     f = lib.bfp_dequantize
     assert f(None, FAKE, 4, 64, 16, 4, FAKE, None) == E_ARG

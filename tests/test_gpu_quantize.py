@@ -205,3 +205,39 @@ def test_stochastic_noise_independent_on_gpu():
         assert indep(u[:, p], u[:, q]) > 1e-7, (p, q)
     assert indep(u[:-1, 7].ravel(), u[1:, 7].ravel()) > 1e-7
     assert indep(u.ravel(), bits[1235].ravel()) > 1e-7
+
+
+@pytest.mark.parametrize("shape,axis", [((3, 64, 5), 1), ((2, 3, 48, 7), 2), ((2, 96, 3, 2), 1), ((5, 2, 32), 0),
+                                        ((4, 32, 6), 2), ((128,), 0), ((7, 64), 1), ((64, 7), 0)])
+def test_quantize_nd_any_axis(shape, axis):
+    """bfp_quantize_nd: an N-D tensor grouped along any axis is the 2-D
+    row-grouped conversion of the tensor with that axis moved last (the other
+    axes in order as rows), noise included; through the binding and through
+    the C ABI directly."""
+    import ctypes
+    x = synth.draw("grads", shape, 60 + len(shape) + axis)
+    L = shape[axis]
+    if L % 16:
+        pytest.skip("grouped axis not a multiple of 16")
+    moved = np.ascontiguousarray(np.moveaxis(x, axis, -1).reshape(-1, L))
+    for g in (16, 8) if L % 16 == 0 else (16,):
+        for m, mode in [(4, "stochastic"), (6, "nearest"), (2, "truncate")]:
+            announce("quantize nd %s axis %d g=%d m=%d %s" % (shape, axis, g, m, mode))
+            t = fb.quantize(torch.from_numpy(x).cuda(), group_axis=axis, g=g, m=m, rounding=mode, seed=21)
+            torch.cuda.synchronize()
+            q_o, E_o, _ = oracle.quantize(moved, g=g, m=m, mode=mode, seed=21)
+            assert (t.rows, t.len) == moved.shape
+            assert np.array_equal(t.exp.cpu().numpy(), E_o)
+            assert np.array_equal(t.mant.cpu().numpy(), bfp_codec.encode(q_o, m))
+            # the N-D entry point directly, also where the binding uses the 2-D one
+            lib = fb._lib.load()
+            u = fb.BFPTensor.empty(t.rows, t.len, g, m, "cuda")
+            xt = torch.from_numpy(x).cuda()
+            arr = (ctypes.c_int64 * len(shape))(*shape)
+            rc = lib.bfp_quantize_nd(ctypes.c_void_p(xt.data_ptr()), len(shape), arr, axis, g, m,
+                                     fb.ROUNDING[mode], ctypes.c_uint64(21), ctypes.c_void_p(u.mant.data_ptr()),
+                                     ctypes.c_void_p(u.exp.data_ptr()), None,
+                                     ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            assert rc == 0
+            torch.cuda.synchronize()
+            assert torch.equal(u.mant, t.mant) and torch.equal(u.exp, t.exp)
