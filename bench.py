@@ -42,11 +42,28 @@ def planes(m):
 
 
 def mfma_passes(pa, pb, g=G):
-    """MFMAs the GEMM issues per K-step and fragment pair: one per pair of
-    chunk planes, except that with groups of 16 two FP6 upper planes (m >= 7
-    on both sides) share one MFMA between the two cross products."""
-    n = planes(pa) * planes(pb)
-    return n - 1 if g == 16 and pa >= 7 and pb >= 7 else n
+    """MFMAs the block-scaled GEMM issues per group and fragment pair.  With
+    groups of 32: one per pair of chunk planes.  With groups of 16: an operand
+    split at 2 bits (m = 5, 6) fills a whole block, so it adds no pass (one
+    MFMA per chunk plane of the other operand); two operands split at 4 bits
+    (m = 7, 8) take 3 (the two cross products share one); otherwise one per
+    pair of chunk planes."""
+    if g == 32:
+        return planes(pa) * planes(pb)
+    split2 = lambda m: m in (5, 6)
+    if split2(pa):
+        return planes(pb)
+    if split2(pb):
+        return planes(pa)
+    if pa >= 7 and pb >= 7:
+        return 3
+    return planes(pa) * planes(pb)
+
+
+def mfma_issue_factor(pa, pb, g=G):
+    """Issued MFMA work over the algorithmic work 2 M N K: MFMAs per group x 32
+    values per block / g values per group."""
+    return mfma_passes(pa, pb, g) * 32 // g
 
 
 def code_bits(m):
@@ -187,7 +204,7 @@ def gemm_sweep(torch, fb, synth, dev, args):
             torch.cuda.synchronize()
             ms = a.elapsed_time(z) / reps
             tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
-            issued = tops * mfma_passes(pa, pb) * 2  # zero-padded half blocks, chunk passes
+            issued = tops * mfma_issue_factor(pa, pb)  # chunk passes and zero-padded half blocks
             out["%s(%d,%d)" % (name, pa, pb)] = {
                 "M": M, "N": N, "K": K, "ms": round(ms, 4), "eff_tops": round(tops, 1),
                 "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4),
@@ -214,7 +231,7 @@ def gemm_sweep(torch, fb, synth, dev, args):
         torch.cuda.synchronize()
         ms = a.elapsed_time(z) / 5
         tops = 2.0 * M * N * K / (ms * 1e-3) / 1e12
-        issued = tops * mfma_passes(pa, pb, 32)  # chunk passes, no padding
+        issued = tops * mfma_issue_factor(pa, pb, 32)  # chunk passes, no padding
         out["ffn_up_g32(%d,%d)" % (pa, pb)] = {
             "M": M, "N": N, "K": K, "g": 32, "ms": round(ms, 4), "eff_tops": round(tops, 1),
             "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4), "mfma_issued_tflops": round(issued, 1),
@@ -581,15 +598,16 @@ def main():
     d = kernels[dom]
     if dom.startswith("gemm"):
         mdom = int(dom.split("_m")[1])
-        issue = mfma_passes(mdom, mdom) * (2 if G == 16 else 1)  # chunk passes x zero-padded half blocks
+        issue = mfma_issue_factor(mdom, mdom)  # chunk passes x zero-padded half blocks
         roof = {"bound": "mfma", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_FP6_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(d["achieved"] / PEAK_FP6_TFLOPS, 4), "traffic": measured_traffic(dom),
                 "work_per_launch": "2*M*N*K = %.4g FLOP (BFP MACs, algorithmic)" % GEMM_OPS,
                 "issued": {"tflops": round(d["achieved"] * issue, 1),
                            "frac": round(d["achieved"] * issue / PEAK_FP6_TFLOPS, 4),
                            "factor": issue,
-                           "note": "MFMA work the kernel issues: the algorithmic work x chunk passes (m > 4: 2 x 2) x 2 "
-                                   "(a 16-value group fills half of a 32-value MFMA block)"}}
+                           "note": "MFMA work the kernel issues: the algorithmic work x MFMAs per group x 32 / g (a "
+                                   "16-value group fills half of a 32-value MFMA block, except an operand split at 2 "
+                                   "bits, m = 5, 6, which fills a whole block)"}}
     else:
         roof = {"bound": "hbm", "kernel": dom, "achieved": d["achieved"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(d["achieved"] / PEAK_HBM_GBS, 4), "traffic": measured_traffic(dom)}
