@@ -54,6 +54,12 @@ def _bind(lib):
     lib.oracle_quantize_group.restype = i32
     lib.oracle_quantize.argtypes = [P, i64, i64, i32, i32, i32, i32, u64, i64, i64, P, P]
     lib.oracle_quantize.restype = i64
+    lib.oracle_quantize_group_floor.argtypes = [P, i64, i32, i32, i32, P, P, i64, P, i32]
+    lib.oracle_quantize_group_floor.restype = i32
+    lib.oracle_quantize_floor.argtypes = [P, i64, i64, i32, i32, i32, i32, u64, i32, i64, i64, P, P]
+    lib.oracle_quantize_floor.restype = i64
+    lib.oracle_exponent_base.argtypes = [P, i64, i32]
+    lib.oracle_exponent_base.restype = i32
     lib.oracle_dequantize.argtypes = [P, P, i64, i32, i32, i64, i64, P]
     lib.oracle_gemm.argtypes = [P, P, i32, P, P, i32, i64, i64, i64, i32, i32, i32, P, i64, P, P]
     lib.oracle_group_partials.argtypes = [P, i32, P, i32, i64, i64, i32, i32, i32, P, i64, P]
@@ -141,6 +147,44 @@ def quantize_group(x, m: int, mode="nearest", noise=None):
     E = np.zeros(1, np.uint8)
     bad = lib.oracle_quantize_group(_ptr(x), 1, g, m, _MODES.get(mode, mode), _ptr(nz), _ptr(q), 1, _ptr(E))
     return q, int(E[0]), bool(bad)
+
+
+def quantize_group_floor(x, m: int, mode="nearest", noise=None, emin: int = 0):
+    """quantize_group with the shared exponent raised to at least emin."""
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    g = x.shape[0]
+    nz = np.zeros(g, np.uint8) if noise is None else np.ascontiguousarray(noise, dtype=np.uint8)
+    q = np.zeros(g, np.int16)
+    E = np.zeros(1, np.uint8)
+    bad = lib.oracle_quantize_group_floor(_ptr(x), 1, g, m, _MODES.get(mode, mode), _ptr(nz), _ptr(q), 1, _ptr(E), emin)
+    return q, int(E[0]), bool(bad)
+
+
+def exponent_base(x, ebits: int = 3) -> int:
+    """The packed layout's tensor exponent base: max exponent field - (2^ebits - 1), at least 0."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    return int(_load().oracle_exponent_base(_ptr(x), x.size, ebits))
+
+
+def quantize_packed(x, g: int = 16, m: int = 2, mode="nearest", seed: int = 0, ebits: int = 3, threads: int = 1):
+    """The packed layout's conversion (groups along rows): the tensor base, then
+    every group at max(its exponent, base).  Returns (q, E, base, bad)."""
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim != 2:
+        raise ValueError("oracle.quantize_packed takes a 2-D array")
+    R, C = x.shape
+    base = exponent_base(x, ebits)
+    q = np.zeros((R, C), np.int16)
+    E = np.zeros((R, C // g), np.uint8)
+    md = _MODES.get(mode, mode)
+
+    def work(a, b):
+        return lib.oracle_quantize_floor(_ptr(x), R, C, 1, g, m, md, seed, base, a, b, _ptr(q[a:]), _ptr(E[a:]))
+
+    bad = sum(_run(_split(R, threads), work, threads))
+    return q, E, base, bad
 
 
 def quantize(x, axis: int = -1, g: int = 16, m: int = 4, mode="nearest", seed: int = 0, threads: int = 1,

@@ -106,11 +106,32 @@ static int exponent_field(float v) {
  *          *E = the shared exponent field.
  * Returns 1 if a non-finite input was seen (a precondition violation), else 0.
  */
+static int quantize_group_floor(const float* x, int64_t stride, int g, int m, int mode, const uint8_t* noise,
+                                int16_t* q, int64_t qstride, uint8_t* E, int emin);
+
 int oracle_quantize_group(const float* x, int64_t stride, int g, int m, int mode, const uint8_t* noise,
                           int16_t* q, int64_t qstride, uint8_t* E) {
+  return quantize_group_floor(x, stride, g, m, mode, noise, q, qstride, E, 0);
+}
+
+/*
+ * The same conversion with the shared exponent raised to at least emin: the
+ * packed layout's exponent of section V-D has a few bits above a base shared
+ * by the tensor, so a group whose largest exponent lies below the base is
+ * converted at the base (its values aligned to the base's, coarser, LSB).
+ * With emin = 0 this is oracle_quantize_group.
+ */
+int oracle_quantize_group_floor(const float* x, int64_t stride, int g, int m, int mode, const uint8_t* noise,
+                                int16_t* q, int64_t qstride, uint8_t* E, int emin) {
+  return quantize_group_floor(x, stride, g, m, mode, noise, q, qstride, E, emin);
+}
+
+static int quantize_group_floor(const float* x, int64_t stride, int g, int m, int mode, const uint8_t* noise,
+                                int16_t* q, int64_t qstride, uint8_t* E, int emin) {
   int bad = 0;
-  /* (a) the largest exponent in the group becomes the shared exponent. */
-  int emax = 0;
+  /* (a) the largest exponent in the group becomes the shared exponent (no
+   * lower than emin). */
+  int emax = emin;
   for (int k = 0; k < g; ++k) {
     int e = exponent_field(x[k * stride]);
     if (e == 255) bad = 1;
@@ -158,8 +179,38 @@ int oracle_quantize_group(const float* x, int64_t stride, int g, int m, int mode
  * E[(r-r0)*(len/g) ...]; gid always uses the absolute row r.
  * Returns the number of groups that held a non-finite input.
  */
+/*
+ * The exponent base of the packed layout (section V-D: a group's exponent in
+ * ebits bits): the largest exponent field of the tensor's values minus
+ * 2^ebits - 1, and at least 0, so that every group's exponent, raised to at
+ * least the base, is the base plus an ebits-bit offset.
+ */
+int oracle_exponent_base(const float* x, int64_t n, int ebits) {
+  int emax = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    int e = exponent_field(x[i]);
+    if (e > emax) emax = e;
+  }
+  int base = emax - ((1 << ebits) - 1);
+  return base > 0 ? base : 0;
+}
+
+static int64_t quantize_rows_floor(const float* x, int64_t R, int64_t C, int axis, int g, int m, int mode,
+                                   uint64_t seed, int64_t r0, int64_t r1, int16_t* q, uint8_t* E, int emin);
+
 int64_t oracle_quantize(const float* x, int64_t R, int64_t C, int axis, int g, int m, int mode, uint64_t seed,
                         int64_t r0, int64_t r1, int16_t* q, uint8_t* E) {
+  return quantize_rows_floor(x, R, C, axis, g, m, mode, seed, r0, r1, q, E, 0);
+}
+
+/* oracle_quantize with every shared exponent raised to at least emin. */
+int64_t oracle_quantize_floor(const float* x, int64_t R, int64_t C, int axis, int g, int m, int mode, uint64_t seed,
+                              int emin, int64_t r0, int64_t r1, int16_t* q, uint8_t* E) {
+  return quantize_rows_floor(x, R, C, axis, g, m, mode, seed, r0, r1, q, E, emin);
+}
+
+static int64_t quantize_rows_floor(const float* x, int64_t R, int64_t C, int axis, int g, int m, int mode,
+                                   uint64_t seed, int64_t r0, int64_t r1, int16_t* q, uint8_t* E, int emin) {
   int64_t bad = 0;
   const int64_t out_len = (axis == 1) ? C : R; /* elements per output row */
   const int64_t ngroups = out_len / g;
@@ -178,8 +229,8 @@ int64_t oracle_quantize(const float* x, int64_t R, int64_t C, int axis, int g, i
         src = x + (j * g) * C + r; /* column r, rows j*g .. j*g+g-1 */
         stride = C;
       }
-      bad += oracle_quantize_group(src, stride, g, m, mode, noise, q + (r - r0) * out_len + j * g, 1,
-                                   E + (r - r0) * ngroups + j);
+      bad += quantize_group_floor(src, stride, g, m, mode, noise, q + (r - r0) * out_len + j * g, 1,
+                                  E + (r - r0) * ngroups + j, emin);
     }
   }
   return bad;

@@ -31,7 +31,7 @@ def exp_field(v: float) -> int:
     return e + 126
 
 
-def brute_quantize_group(xs, m, mode, noise):
+def brute_quantize_group(xs, m, mode, noise, emin=0):
     """Definition of section III-A in exact rationals.
 
     (a) shared exponent = largest exponent field; one LSB is the value of the
@@ -40,7 +40,7 @@ def brute_quantize_group(xs, m, mode, noise):
     the nearest multiple of the LSB, ties away from zero (found by comparing
     candidates); stochastic: floor(a + U/256); truncate: floor(a).  Largest
     magnitude 2^m - 1.  Subnormals count as zero."""
-    E = max(exp_field(v) for v in xs)
+    E = max([emin] + [exp_field(v) for v in xs])
     lsb = Fraction(2) ** (E - 127 - (m - 1))
     qmax = 2 ** m - 1
     out = []
@@ -125,6 +125,49 @@ def test_quantize_group_matches_rational_definition(m, mode):
         assert not bad
         assert E == E_want
         assert [int(v) for v in q] == want
+
+
+@pytest.mark.parametrize("m", [2, 4, 6, 8])
+@pytest.mark.parametrize("mode", MODES)
+def test_quantize_floor_matches_rational_definition(m, mode):
+    """The packed layout's conversion (section V-D: a few exponent bits above
+    a tensor base): a group whose largest exponent lies below the floor is
+    converted at the floor -- the same rational definition with E replaced by
+    max(E, floor), its values aligned to the coarser LSB."""
+    rng = np.random.default_rng(300 + m)
+    for trial in range(40):
+        xs = (rng.standard_normal(16) * np.exp2(rng.integers(-12, 4, 16))).astype(np.float32)
+        emin = int(rng.integers(110, 135))
+        noise = rng.integers(0, 256, 16)
+        q, E, _ = oracle.quantize_group_floor(xs, m, mode, noise, emin)
+        want, E_want = brute_quantize_group(list(xs), m, mode, noise, emin)
+        assert E == E_want == max(emin, max(exp_field(v) for v in xs))
+        assert [int(v) for v in q] == want
+
+
+def test_exponent_base_and_packed_groups():
+    """The tensor base is the largest exponent field minus 7 (a 3-bit group
+    exponent, section V-D), at least 0; every group's exponent then lies in
+    base .. base + 7, and a group entirely below the base (1/1024 here, eight
+    binades under 4.0) keeps only what its values are worth at the base's LSB:
+    1/1024 at m = 2 with E = 122 rounds to 0 (half an LSB is 1/128)."""
+    x = np.zeros((3, 16), np.float32)
+    x[0, 0] = 4.0           # exponent field 129: base 122
+    x[1, :] = 2.0 ** -10    # field 117 < 122
+    x[2, 3] = 2.0 ** -6     # field 121 < 122: LSB at m = 2 is 2^(122-127-1) = 2^-6 -> q = 1
+    assert oracle.exponent_base(x) == 122
+    q, E, base, bad = oracle.quantize_packed(x, m=2)
+    assert base == 122 and bad == 0
+    assert E.tolist() == [[129], [122], [122]]
+    assert not q[1].any() and q[2, 3] == 1 and q[0, 0] == 2
+    assert oracle.exponent_base(np.full((1, 16), 1e-30, np.float32)) == 0 + max(0, 27 - 7)
+    assert oracle.exponent_base(np.zeros((2, 16), np.float32)) == 0
+    # with every group within 7 binades of the largest, the packed conversion is the plain one
+    y = (np.random.default_rng(2).standard_normal((8, 64)) * 2.0 ** -3).astype(np.float32)
+    y[:, ::16] = 1.0
+    qp, Ep, _, _ = oracle.quantize_packed(y, m=4, mode="stochastic", seed=5)
+    qn, En, _ = oracle.quantize(y, m=4, mode="stochastic", seed=5)
+    assert np.array_equal(qp, qn) and np.array_equal(Ep, En)
 
 
 def test_quantize_exponent_is_group_max_and_range():
