@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define FASTBFP_ABI_VERSION 6
+#define FASTBFP_ABI_VERSION 7
 
 typedef enum {
   BFP_ROUND_NEAREST = 0,    /* add half an LSB, then truncate (ties away from zero) */
@@ -203,8 +203,9 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
  *   Size limits  : M, N < 2^31, K <= 11184784 (256 rows of 12 bytes per 16
  *                  values stay below 2^31 bytes: the kernels address operand
  *                  tiles with 32-bit offsets), and
- *                  ceil(M / 128) * ceil(N / 64) < 2^31; otherwise
- *                  BFP_E_UNSUPPORTED.
+ *                  ceil(M / 128) * ceil(N / 64) < 2^31 (on the general
+ *                  kernel also ceil(M / 32) * ceil(N / 32) < 2^31);
+ *                  otherwise BFP_E_UNSUPPORTED.
  * Preconditions for the stated accuracy: every group exponent E is at most 250,
  * and every scaled group sum, partial sum and |C| stays in the FP32 normal range.
  */
@@ -270,6 +271,82 @@ int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, cons
  */
 int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* b_mant, int b_m_bits, int64_t M,
                             int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream);
+
+/*
+ * Packed storage -- the paper's memory layout for variable-precision BFP
+ * (section V-D): every magnitude split into 2-bit chunks, each stored with the
+ * value's sign in 3 bits, the chunks of one position of all values in a group
+ * together, and a 3-bit shared exponent, so that a group of g = 16 takes
+ * e + 16 * ceil(m/2) * 3 bits (3.1875 bits per value at m = 2, 6.1875 at
+ * m = 4, with e = 3).  This is a storage form: bfp_gemm_packed reads it on the
+ * general kernel (the block-scaled kernel takes the chunk-plane layout above).
+ *   Groups      : 16 consecutive values along each row (len a multiple of 16).
+ *   Exponents   : a 3-bit exponent cannot hold an FP32 exponent field, so it is
+ *                 read as an offset above one base per tensor: exp starts with
+ *                 a little-endian uint32 holding E_max, the largest FP32
+ *                 exponent field in the tensor; the base is
+ *                 B = max(E_max - 7, 0); group gid (= row * len/16 + group)
+ *                 has the shared exponent E = max(its largest exponent field,
+ *                 B), stored as e = E - B in bits 3 gid .. 3 gid + 2 of the
+ *                 little-endian bit stream that follows the word (padded to
+ *                 24 bytes per 64 groups).  A group whose largest exponent is
+ *                 below B is quantized at B: its small values lose low bits.
+ *   Mantissas   : NP = ceil(m/2) planes, plane c (most significant first)
+ *                 holding chunk c of every magnitude q, (q >> 2 (NP-1-c)) & 3,
+ *                 as a 3-bit field: the chunk in bits 0-1, the value's sign in
+ *                 bit 2 when the chunk is nonzero (a zero chunk is stored as
+ *                 0).  A group's 16 fields are the 48 bits of 6 bytes (value t
+ *                 at bits 3t .. 3t+2, little-endian); plane c, group gid at
+ *                 byte offset (c * ngroups + gid) * 6, ngroups = rows * len/16.
+ *   Values      : one LSB of group gid is 2^(E - 127 - (m-1)) as in the chunk-
+ *                 plane layout; a tensor of Inf/NaN-free inputs whose groups
+ *                 all have exponents within 7 of E_max converts to the same
+ *                 (q, E) as bfp_quantize.
+ */
+
+/* Host-side sizes of a packed rows x len tensor: mant_bytes = ceil(m/2) * 6 *
+ * ngroups, exp_bytes = 4 + 24 * ceil(ngroups / 64).  So with ngroups a multiple
+ * of 64 the tensor takes (51/16, 99/16, ...) bits per value plus the 32-bit
+ * E_max word.  BFP_E_ARG for null outputs or negative sizes, BFP_E_SHAPE if
+ * len is not a multiple of 16, BFP_E_PRECISION for m outside 1..8,
+ * BFP_E_UNSUPPORTED for 2^56 groups or more. */
+int bfp_packed_sizes(int64_t rows, int64_t len, int m_bits, size_t* mant_bytes, size_t* exp_bytes);
+
+/*
+ * bfp_quantize_packed -- FP32 [R][C] -> packed BFP with groups of 16 along
+ * each row (section III-A steps (a)-(d), with the shared exponent raised to
+ * the tensor base; section V-D storage).
+ *   x           : FP32 [R][C], row-major, contiguous, 16-byte aligned; C a
+ *                 multiple of 16.
+ *   m_bits, round_mode, seed, status_word : as bfp_quantize (the same noise
+ *                 addressing: gid = row * C/16 + group).
+ *   mant, exp   : outputs sized by bfp_packed_sizes, 4-byte aligned.
+ * Three launches on the stream: the E_max word is cleared, reduced over x,
+ * then the groups are converted.
+ */
+int bfp_quantize_packed(const float* x, int64_t R, int64_t C, int m_bits, int round_mode, uint64_t seed,
+                        uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream);
+
+/* bfp_dequantize_packed -- packed BFP -> FP32 [rows][len]: y = +-q *
+ * 2^(E - 127 - (m-1)) (section III-A), exact whenever the result is a normal
+ * FP32 number.  y 16-byte aligned; mant, exp 4-byte aligned. */
+int bfp_dequantize_packed(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int m_bits, float* y,
+                          void* stream);
+
+/*
+ * bfp_gemm_packed -- bfp_gemm (section III-B) on operands in packed storage:
+ * A [M][K] stored with a_m_bits, B [N][K] with b_m_bits, each with its own
+ * base; m_a, m_b as bfp_gemm (1 .. the stored width: the magnitude truncated to
+ * its top bits, section V-D).  Runs on the general kernel: per group the
+ * chunk fields are unpacked to signed magnitudes, the exact integer group dot
+ * product P_G taken on int8 MFMA, scaled by 2^(ea + eb - 254 - (m_a-1) -
+ * (m_b-1)) and added in FP32.  C FP32 with row stride ldc >= N.  Size limits:
+ * as bfp_gemm, and ceil(M/32) * ceil(N/32) < 2^31.  exp pointers 4-byte
+ * aligned.
+ */
+int bfp_gemm_packed(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant,
+                    const uint8_t* b_exp, int b_m_bits, int64_t M, int64_t N, int64_t K, int m_a, int m_b, float* C,
+                    int64_t ldc, void* stream);
 
 /*
  * bfp_quantize_dual -- both groupings of one FP32 matrix from a single read:

@@ -22,7 +22,8 @@ import torch
 from ._lib import BFPError, check, load
 
 __all__ = ["BFPTensor", "BFPError", "quantize", "quantize_dual", "weight_update", "dequantize", "gemm", "gemm_bfp",
-           "gemm_group_partials", "quantize_adaptive", "quantize_adaptive_noalloc", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING"]
+           "gemm_group_partials", "quantize_adaptive", "quantize_adaptive_noalloc", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING",
+           "PackedBFPTensor", "packed_sizes", "quantize_packed", "dequantize_packed", "gemm_packed"]
 
 ROUNDING = {"nearest": 0, "stochastic": 1, "truncate": 2}
 
@@ -353,3 +354,79 @@ def gemm_group_partials(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b:
                                          B.m, A.rows, B.rows, A.len, A.g, m_a, m_b, ctypes.c_void_p(P.data_ptr()),
                                          _stream(A.device)), "bfp_gemm_group_partials")
     return P
+
+
+def packed_sizes(rows: int, length: int, m: int):
+    """(mantissa bytes, exponent bytes) of a rows x length packed BFP tensor."""
+    mb, eb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    check(load().bfp_packed_sizes(rows, length, m, ctypes.byref(mb), ctypes.byref(eb)), "bfp_packed_sizes")
+    return mb.value, eb.value
+
+
+@dataclass
+class PackedBFPTensor:
+    """A rows x len BFP tensor in the packed storage of section V-D (groups of
+    16 along len; see include/fastbfp.h): mant holds ceil(m/2) planes of 3-bit
+    chunk fields, exp a uint32 E_max word and 3-bit exponent offsets."""
+    mant: torch.Tensor
+    exp: torch.Tensor
+    rows: int
+    len: int
+    m: int
+    g: int = 16
+
+    @property
+    def device(self) -> torch.device:
+        return self.mant.device
+
+    @staticmethod
+    def empty(rows: int, length: int, m: int, device) -> "PackedBFPTensor":
+        mb, eb = packed_sizes(rows, length, m)
+        # int32 storage keeps the exponent stream 4-byte aligned
+        exp = torch.empty((eb + 3) // 4, dtype=torch.int32, device=device).view(torch.uint8)[:eb]
+        return PackedBFPTensor(torch.empty(mb, dtype=torch.uint8, device=device), exp, rows, length, m)
+
+
+def quantize_packed(x: torch.Tensor, m: int = 4, rounding: str = "nearest", seed: int = 0,
+                    status: torch.Tensor | None = None) -> PackedBFPTensor:
+    """FP32 [..., C] -> packed BFP, groups of 16 along the last axis (leading
+    axes flattened into rows), each group's exponent at least the tensor base
+    max(E_max - 7, 0)."""
+    _need_cuda(x, "x", torch.float32)
+    if rounding not in ROUNDING:
+        raise ValueError("rounding must be one of %s" % sorted(ROUNDING))
+    if x.dim() < 1:
+        raise ValueError("x must have at least one dimension")
+    C = x.shape[-1]
+    R = math.prod(x.shape[:-1])
+    t = PackedBFPTensor.empty(R, C, m, x.device)
+    check(load().bfp_quantize_packed(ctypes.c_void_p(x.data_ptr()), R, C, m, ROUNDING[rounding],
+                                     ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.c_void_p(t.mant.data_ptr()),
+                                     ctypes.c_void_p(t.exp.data_ptr()), _status_ptr(status), _stream(x.device)),
+          "bfp_quantize_packed")
+    return t
+
+
+def dequantize_packed(t: PackedBFPTensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Packed BFP -> FP32 [rows, len]."""
+    y = out if out is not None else torch.empty((t.rows, t.len), dtype=torch.float32, device=t.device)
+    _need_cuda(y, "out", torch.float32)
+    check(load().bfp_dequantize_packed(ctypes.c_void_p(t.mant.data_ptr()), ctypes.c_void_p(t.exp.data_ptr()), t.rows,
+                                       t.len, t.m, ctypes.c_void_p(y.data_ptr()), _stream(t.device)),
+          "bfp_dequantize_packed")
+    return y
+
+
+def gemm_packed(A: PackedBFPTensor, B: PackedBFPTensor, m_a: int | None = None, m_b: int | None = None,
+                out: torch.Tensor | None = None) -> torch.Tensor:
+    """C = A . B^T in FP32 [A.rows, B.rows] for packed A [M, K] and B [N, K]."""
+    m_a, m_b = _gemm_args(A, B, m_a, m_b)
+    C = out if out is not None else torch.empty((A.rows, B.rows), dtype=torch.float32, device=A.device)
+    _need_cuda(C, "out", torch.float32)
+    if C.dim() != 2 or C.shape[0] != A.rows or C.shape[1] != B.rows:
+        raise ValueError("out must be [%d, %d]" % (A.rows, B.rows))
+    check(load().bfp_gemm_packed(ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
+                                 ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows,
+                                 B.rows, A.len, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0),
+                                 _stream(A.device)), "bfp_gemm_packed")
+    return C

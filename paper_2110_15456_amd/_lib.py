@@ -30,6 +30,10 @@ SIGNATURES = {
     "bfp_gemm_tiled": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _I64, _I, _P]),
     "bfp_gemm_group_partials": (_I, [_P, _I, _P, _I, _I64, _I64, _I64, _I, _I, _I, _P, _P]),
     "bfp_gemm_bfp": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _I, _I, _U64, _P, _P, _P, _P]),
+    "bfp_packed_sizes": (_I, [_I64, _I64, _I, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]),
+    "bfp_quantize_packed": (_I, [_P, _I64, _I64, _I, _I, _U64, _P, _P, _P, _P]),
+    "bfp_dequantize_packed": (_I, [_P, _P, _I64, _I64, _I, _P, _P]),
+    "bfp_gemm_packed": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _P, _I64, _P]),
     "bfp_quantize_dual": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P, _P]),
     "bfp_weight_update": (_I, [_P, _P, ctypes.c_float, _P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P,
                                _P]),
@@ -41,7 +45,7 @@ SIGNATURES = {
     "bfp_adaptive_threshold": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, _I64, _I64, _I64, _I64]),
     "bfp_adaptive_mantissa": (_I, [ctypes.c_double, ctypes.c_double, ctypes.c_double]),
 }
-ABI_VERSION = 6
+ABI_VERSION = 7
 
 _lock = threading.Lock()
 _lib = None

@@ -66,6 +66,18 @@ int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, i
   return BFP_OK;
 }
 
+// The general kernel launches one 64-lane workgroup per 32 x 32 tile of C.
+bool general_grid_ok(int64_t M, int64_t N) { return ((M + 31) / 32) * ((N + 31) / 32) <= 0x7fffffff; }
+
+// Packed tensors: groups of 16 along rows, m in 1..8, fewer than 2^56 groups.
+int check_packed(int64_t rows, int64_t len, int m) {
+  if (rows < 0 || len < 0) return BFP_E_ARG;
+  if (m < 1 || m > 8) return BFP_E_PRECISION;
+  if (len % fastbfp::kPackedGroup != 0) return BFP_E_SHAPE;
+  if (rows > 0 && len / fastbfp::kPackedGroup > (int64_t(1) << 56) / rows) return BFP_E_UNSUPPORTED;
+  return BFP_OK;
+}
+
 int check_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, const uint8_t* mr,
                const uint8_t* er, const uint8_t* mc, const uint8_t* ec, const uint32_t* status_word) {
   if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
@@ -182,6 +194,7 @@ int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, co
   if (tile < -1 || tile > 4) return BFP_E_ARG;
   const bool fast = fast_path(a_m_bits, b_m_bits, g, m_a, m_b);
   if (!fast && tile >= 0) return BFP_E_UNSUPPORTED;
+  if (!fast && !general_grid_ok(M, N)) return BFP_E_UNSUPPORTED;
   const int na = planes_used(a_m_bits, m_a), nb = planes_used(b_m_bits, m_b);
   if (tile > 0 && (g != 16 || na != 1 || nb != 1)) return BFP_E_UNSUPPORTED;
   if (M == 0 || N == 0) return BFP_OK;
@@ -222,11 +235,62 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
                             int64_t N, int64_t K, int g, int m_a, int m_b, int32_t* P, void* stream) {
   int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
   if (st != BFP_OK) return st;
+  if (!general_grid_ok(M, N)) return BFP_E_UNSUPPORTED;
   if (M == 0 || N == 0 || K == 0) return BFP_OK;
   if (!P) return BFP_E_ARG;
   // the group partials need no exponents: the decoder reads only mantissas
   return status_of(fastbfp::launch_gemm_general(a_mant, nullptr, a_m_bits, m_a, b_mant, nullptr, b_m_bits, m_b, M, N,
                                                 K, g, nullptr, N, P, static_cast<hipStream_t>(stream)));
+}
+
+int bfp_packed_sizes(int64_t rows, int64_t len, int m_bits, size_t* mant_bytes, size_t* exp_bytes) {
+  if (!mant_bytes || !exp_bytes) return BFP_E_ARG;
+  const int st = check_packed(rows, len, m_bits);
+  if (st != BFP_OK) return st;
+  const int64_t ngroups = rows * (len / fastbfp::kPackedGroup);
+  *mant_bytes = (size_t)((m_bits + 1) / 2) * fastbfp::kPackedPlaneGroupBytes * (size_t)ngroups;
+  *exp_bytes = (size_t)fastbfp::packed_exp_bytes(ngroups);
+  return BFP_OK;
+}
+
+int bfp_quantize_packed(const float* x, int64_t R, int64_t C, int m_bits, int round_mode, uint64_t seed,
+                        uint8_t* mant, uint8_t* exp, uint32_t* status_word, void* stream) {
+  if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
+  const int st = check_packed(R, C, m_bits);
+  if (st != BFP_OK) return st;
+  if (R == 0 || C == 0) return BFP_OK;
+  if (!x || !mant || !exp) return BFP_E_ARG;
+  if (!aligned(x, 16) || !aligned(mant, 4) || !aligned(exp, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
+  if ((R * (C / 16) + 255) / 256 > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  return status_of(fastbfp::launch_quantize_packed(x, R, C, m_bits, round_mode, seed, mant, exp, status_word,
+                                                   static_cast<hipStream_t>(stream)));
+}
+
+int bfp_dequantize_packed(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int m_bits, float* y,
+                          void* stream) {
+  const int st = check_packed(rows, len, m_bits);
+  if (st != BFP_OK) return st;
+  if (rows == 0 || len == 0) return BFP_OK;
+  if (!mant || !exp || !y) return BFP_E_ARG;
+  if (!aligned(mant, 4) || !aligned(exp, 4) || !aligned(y, 16)) return BFP_E_ARG;
+  if ((rows * (len / 16) + 255) / 256 > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  return status_of(
+      fastbfp::launch_dequantize_packed(mant, exp, rows, len, m_bits, y, static_cast<hipStream_t>(stream)));
+}
+
+int bfp_gemm_packed(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant,
+                    const uint8_t* b_exp, int b_m_bits, int64_t M, int64_t N, int64_t K, int m_a, int m_b, float* C,
+                    int64_t ldc, void* stream) {
+  int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, fastbfp::kPackedGroup, m_a, m_b);
+  if (st != BFP_OK) return st;
+  if (ldc < N) return BFP_E_SHAPE;
+  if (!general_grid_ok(M, N)) return BFP_E_UNSUPPORTED;
+  if (M == 0 || N == 0) return BFP_OK;
+  if (!C || !a_exp || !b_exp) return BFP_E_ARG;
+  if (!aligned(a_exp, 4) || !aligned(b_exp, 4)) return BFP_E_ARG;
+  return status_of(fastbfp::launch_gemm_general(a_mant, a_exp, a_m_bits, m_a, b_mant, b_exp, b_m_bits, m_b, M, N, K,
+                                                fastbfp::kPackedGroup, C, ldc, nullptr,
+                                                static_cast<hipStream_t>(stream), true));
 }
 
 int bfp_quantize_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, uint64_t seed_r,

@@ -77,4 +77,17 @@ __device__ __forceinline__ uint32_t fp6_field(const uint32_t* w, int t) {
   return v & 0x3Fu;
 }
 
+// Packed exponents (section V-D reading): the tensor base max(E_max - 7, 0)
+// from the stream's leading E_max word, and the 3-bit offset of group gid
+// (bits 3 gid .. 3 gid + 2 of the dwords after it; a field crosses into the
+// next dword only inside a 24-byte block of 64 groups).
+__device__ __forceinline__ uint32_t packed_base(uint32_t emax) { return emax > 7u ? emax - 7u : 0u; }
+__device__ __forceinline__ uint32_t packed_exponent_offset(const uint32_t* expw, int64_t gid) {
+  const int64_t bit = 3 * gid;
+  const int sh = (int)(bit % 32);
+  uint32_t v = expw[1 + bit / 32] >> sh;
+  if (sh > 29) v |= expw[2 + bit / 32] << (32 - sh);
+  return v & 7u;
+}
+
 }  // namespace fastbfp

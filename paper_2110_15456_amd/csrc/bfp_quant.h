@@ -45,6 +45,63 @@ __device__ __forceinline__ v6u_t cvt_fp6_x32(v16f_t a, v16f_t b) {
   return r;
 }
 
+// Step (a): the shared exponent of a group of G values (their FP32 bit
+// patterns at b[0..G)): the largest biased exponent field.
+template <int G>
+__device__ __forceinline__ uint32_t group_exponent(const uint32_t* b) {
+  uint32_t E = 0;
+#pragma unroll
+  for (int t = 0; t < G; ++t) E = max(E, (b[t] >> 23) & 0xFFu);
+  return E;
+}
+
+// The stochastic-rounding noise of group gid: byte t of noise[0..G/4) is
+// value t's noise byte.  One Philox4x32-10 block per 16 values, with counter
+// (gid lo, gid hi, t div 16, 0) and key (key0, key1) (a group of 4 or 8 uses
+// the first G/4 words of its block).
+template <int G>
+__device__ __forceinline__ void group_noise(uint64_t gid, uint32_t key0, uint32_t key1, uint32_t* noise) {
+#pragma unroll
+  for (int blk = 0; blk < (G + 15) / 16; ++blk) {
+    const uint4 r = philox4x32_10(make_uint4((uint32_t)gid, (uint32_t)(gid >> 32), (uint32_t)blk, 0u), key0, key1);
+    noise[4 * blk] = r.x;
+    if constexpr (G >= 8) noise[4 * blk + 1] = r.y;
+    if constexpr (G >= 16) {
+      noise[4 * blk + 2] = r.z;
+      noise[4 * blk + 3] = r.w;
+    }
+  }
+}
+
+// Steps (b)-(d) for one value of bit pattern `bits`: its magnitude q in units
+// of the group's LSB, rounded as MODE says and saturated at qmax.  `align` is
+// 127 + (m - 1) - E, plus 1 for nearest and 8 for stochastic rounding (the
+// ldexp then scales |x| to 2, 1 or 256 times its magnitude in LSBs, exactly);
+// the noise byte is byte t mod 4 of noise word `nw` (t: the value's position).
+// Subnormals read as zero: by the FP32 flush mode of the including file
+// (FTZ), or explicitly.
+template <int MODE, bool FTZ>
+__device__ __forceinline__ uint32_t value_magnitude(uint32_t bits, int align, uint32_t nw, int t, uint32_t qmax) {
+  const uint32_t abits = (FTZ || ((bits >> 23) & 0xFFu)) ? (bits & 0x7FFFFFFFu) : 0u;
+  const float mag = __builtin_ldexpf(__uint_as_float(abits), align);
+  const uint32_t fl = (uint32_t)mag;  // truncating conversion: floor
+  uint32_t q;
+  if (MODE == kNearest) {
+    q = (fl + 1u) >> 1;  // half an LSB added
+  } else if (MODE == kTruncate) {
+    q = fl;
+  } else {
+    // (c) add the noise byte below the LSB, (d) truncate.
+    q = (fl + ((nw >> (8 * (t & 3))) & 0xFFu)) >> 8;
+  }
+  return min(q, qmax);  // a group maximum that rounds up to 2^m saturates
+}
+// The align argument of value_magnitude.
+template <int MODE>
+__device__ __forceinline__ int magnitude_align(uint32_t m, uint32_t E) {
+  return 127 + (int)m - 1 - (int)E + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
+}
+
 // Quantize NG consecutive groups (gid, gid + 1, ...) whose FP32 bit patterns
 // are in b[], packed together as one run of NG * G values.  Writes the packed
 // chunk planes to w[plane][...] and the shared exponents to E_out; nonfinite
@@ -95,9 +152,7 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
   uint32_t E[NG];
 #pragma unroll
   for (int gi = 0; gi < NG; ++gi) {
-    E[gi] = 0;
-#pragma unroll
-    for (int t = 0; t < G; ++t) E[gi] = max(E[gi], (b[gi * G + t] >> 23) & 0xFFu);
+    E[gi] = group_exponent<G>(b + gi * G);
     E_out[gi] = E[gi];
     nonfinite |= (E[gi] == 255u);
   }
@@ -105,17 +160,7 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
   uint32_t noise[LEN / 4];
   if (MODE == kStochastic) {
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi)
-#pragma unroll
-      for (int blk = 0; blk < (G + 15) / 16; ++blk) {
-        // one Philox block per 16 values of a group (a group of 4 or 8 uses
-        // the first G/4 words of its block)
-        const uint64_t id = gid + (uint64_t)gi;
-        const uint4 r = philox4x32_10(make_uint4((uint32_t)id, (uint32_t)(id >> 32), (uint32_t)blk, 0u), key0, key1);
-        const uint32_t rw[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-        for (int k = 0; k < (G < 16 ? G / 4 : 4); ++k) noise[gi * G / 4 + 4 * blk + k] = rw[k];
-      }
+    for (int gi = 0; gi < NG; ++gi) group_noise<G>(gid + (uint64_t)gi, key0, key1, noise + gi * G / 4);
   }
 
   const uint32_t qmax = (1u << m) - 1u;
@@ -123,8 +168,7 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
   // nearest, 256 for stochastic rounding).
   int align[NG];
 #pragma unroll
-  for (int gi = 0; gi < NG; ++gi)
-    align[gi] = 127 + (int)m - 1 - (int)E[gi] + (MODE == kNearest ? 1 : MODE == kStochastic ? 8 : 0);
+  for (int gi = 0; gi < NG; ++gi) align[gi] = magnitude_align<MODE>(m, E[gi]);
   typedef float v16f __attribute__((ext_vector_type(16)));
   constexpr int NH = LEN / 32 + (LEN % 32 != 0);
   v16f ev[NCH][NH], od[NCH][NH];
@@ -140,21 +184,8 @@ __device__ __forceinline__ void quantize_groups(const uint32_t (&b)[NG * G], uin
   }
 #pragma unroll
   for (int t = 0; t < LEN; ++t) {
-    // subnormals read as zero: by the FP32 flush mode of the including file
-    // (FTZ), or explicitly
-    const uint32_t abits = (FTZ || ((b[t] >> 23) & 0xFFu)) ? (b[t] & 0x7FFFFFFFu) : 0u;
-    const float mag = __builtin_ldexpf(__uint_as_float(abits), align[t / G]);
-    const uint32_t fl = (uint32_t)mag;  // truncating conversion: floor
-    uint32_t q;
-    if (MODE == kNearest) {
-      q = (fl + 1u) >> 1;
-    } else if (MODE == kTruncate) {
-      q = fl;
-    } else {
-      // (c) add the noise byte below the LSB, (d) truncate.
-      q = (fl + ((noise[t >> 2] >> (8 * (t & 3))) & 0xFFu)) >> 8;
-    }
-    q = min(q, qmax);  // a group maximum that rounds up to 2^m saturates
+    const uint32_t q = value_magnitude<MODE, FTZ>(b[t], align[t / G], MODE == kStochastic ? noise[t >> 2] : 0u, t,
+                                                  qmax);
     if (ADAPT) {
       s_lo[t / G] += q & 3u;
       s_hi[t / G] += q >> 2;

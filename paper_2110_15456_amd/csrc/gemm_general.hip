@@ -16,7 +16,8 @@
 // P_G is then scaled by 2^(ea + eb - 254 - (m_a-1) - (m_b-1)) (an exact
 // power-of-two scaling) and added to an FP32 accumulator: the fMAC's exponent
 // addition and FP32 accumulation.  With WRITE_P the kernel writes P_G instead
-// (bfp_gemm_group_partials).
+// (bfp_gemm_group_partials).  The same kernel takes operands in the packed
+// layout of packed.hip (bfp_gemm_packed).
 #include "bfp_device.h"
 #include "launch.h"
 
@@ -24,14 +25,16 @@ namespace fastbfp {
 
 namespace {
 
-// One operand as the decoder reads it: planes in 16-value units.
+// One operand as the decoder reads it: planes in 16-value units, or the
+// packed layout (3-bit fields of 2-bit chunks, g = 16).
 struct Opnd {
-  const uint8_t* p0;    // plane 0
-  const uint8_t* p1;    // plane 1 (m > 4)
-  const uint8_t* exps;  // [rows][len / g]
+  const uint8_t* p0;    // plane 0 (packed: all ceil(m/2) planes, plane c at c * rows * units * 6)
+  const uint8_t* p1;    // plane 1 (m > 4; unused when packed)
+  const uint8_t* exps;  // [rows][len / g], or the packed exponent stream
   int64_t units;        // 16-value units per row (len / 16)
   int64_t ngr;          // groups per row (len / g)
   int rows, m, m_use;
+  bool packed;
 };
 
 // Bytes of a 16-value unit of plane p of an m-bit tensor.
@@ -65,6 +68,27 @@ __device__ __forceinline__ void decode_chunks(const uint8_t* u, int k, int h, in
   }
 }
 
+// Signed magnitudes of values 8h .. 8h + 7 of packed group idx: per plane the
+// 24 bits of those values' 3-bit fields, chunk c of the magnitude weighted
+// 4^(ceil(m/2) - 1 - c), the sign from any nonzero chunk.
+__device__ __forceinline__ void decode_packed(const Opnd& o, int64_t idx, int h, int (&q)[8]) {
+  const int64_t plane_bytes = (int64_t)o.rows * o.units * 6;
+  int mag[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  uint32_t neg = 0;
+  for (int c = 0; c < (o.m + 1) / 2; ++c) {
+    const uint8_t* u = o.p0 + c * plane_bytes + idx * 6 + 3 * h;
+    const uint32_t w = (uint32_t)u[0] | ((uint32_t)u[1] << 8) | ((uint32_t)u[2] << 16);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const uint32_t f = (w >> (3 * t)) & 7u;
+      mag[t] = 4 * mag[t] + (int)(f & 3u);
+      neg |= ((f >> 2) & 1u) << t;
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < 8; ++t) q[t] = ((neg >> t) & 1u) ? -mag[t] : mag[t];
+}
+
 // Signed magnitudes of values 8h .. 8h + 7 of 16-value unit `unit` of row
 // `row`, truncated from m to m_use bits (zero past the last row).
 __device__ __forceinline__ void decode_q8(const Opnd& o, int row, int64_t unit, int h, int (&q)[8]) {
@@ -72,8 +96,12 @@ __device__ __forceinline__ void decode_q8(const Opnd& o, int row, int64_t unit, 
   for (int t = 0; t < 8; ++t) q[t] = 0;
   if (row >= o.rows) return;
   const int64_t idx = (int64_t)row * o.units + unit;
-  decode_chunks(o.p0 + idx * unit_bytes(o.m, 0), plane_kind(o.m, 0), h, q);
-  if (o.m > 4) {
+  if (o.packed) {
+    decode_packed(o, idx, h, q);
+  } else {
+    decode_chunks(o.p0 + idx * unit_bytes(o.m, 0), plane_kind(o.m, 0), h, q);
+  }
+  if (!o.packed && o.m > 4) {
     int lo[8];
     decode_chunks(o.p1 + idx * unit_bytes(o.m, 1), plane_kind(o.m, 1), h, lo);
     const int w = low_chunk_bits(o.m);
@@ -99,6 +127,14 @@ __device__ __forceinline__ long pack8(const int (&q)[8], int pass, int npass, in
     out |= (uint64_t)(uint8_t)(int8_t)c << (8 * t);
   }
   return (long)out;
+}
+
+// The shared exponent of group G of row `row`.
+__device__ __forceinline__ int opnd_exponent(const Opnd& o, int row, int64_t G) {
+  const int64_t gid = (int64_t)row * o.ngr + G;
+  if (!o.packed) return (int)o.exps[gid];
+  const uint32_t* w = reinterpret_cast<const uint32_t*>(o.exps);
+  return (int)(packed_base(w[0]) + packed_exponent_offset(w, gid));
 }
 
 typedef int v16i_t __attribute__((ext_vector_type(16)));
@@ -152,8 +188,8 @@ __global__ __launch_bounds__(64) void k_gemm_general(Opnd A, Opnd B, int g, int 
       } else {
         // the shared exponents: lane l holds row row0 + (l & 31)'s; element r
         // of every lane belongs to row (r / 4) * 8 + half * 4 + r % 4
-        const int ea_mine = ar < M ? (int)A.exps[(int64_t)ar * A.ngr + G] : 0;
-        const int eb = bc < N ? (int)B.exps[(int64_t)bc * B.ngr + G] : 0;
+        const int ea_mine = ar < M ? opnd_exponent(A, ar, G) : 0;
+        const int eb = bc < N ? opnd_exponent(B, bc, G) : 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int ea = __shfl(ea_mine, (r / 4) * 8 + half * 4 + (r % 4));
@@ -171,19 +207,21 @@ __global__ __launch_bounds__(64) void k_gemm_general(Opnd A, Opnd B, int g, int 
   }
 }
 
-Opnd make_opnd(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t K, int g, int m, int m_use) {
+Opnd make_opnd(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t K, int g, int m, int m_use,
+               bool packed) {
   const int64_t units = K / 16;
   const int64_t p0_bytes = rows * units * (plane_kind(m, 0) == kPlaneFP6 ? 12 : 8);
-  return Opnd{mant, mant + p0_bytes, exps, units, K / g, (int)rows, m, m_use};
+  return Opnd{mant, packed ? nullptr : mant + p0_bytes, exps, units, K / g, (int)rows, m, m_use, packed};
 }
 
 }  // namespace
 
 hipError_t launch_gemm_general(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int m_a, const uint8_t* b_mant,
                                const uint8_t* b_exp, int b_m, int m_b, int64_t M, int64_t N, int64_t K, int g,
-                               float* C, int64_t ldc, int32_t* P, hipStream_t s) {
+                               float* C, int64_t ldc, int32_t* P, hipStream_t s, bool packed) {
   if (M == 0 || N == 0) return hipSuccess;
-  const Opnd A = make_opnd(a_mant, a_exp, M, K, g, a_m, m_a), B = make_opnd(b_mant, b_exp, N, K, g, b_m, m_b);
+  const Opnd A = make_opnd(a_mant, a_exp, M, K, g, a_m, m_a, packed),
+             B = make_opnd(b_mant, b_exp, N, K, g, b_m, m_b, packed);
   const int tiles_m = (int)((M + 31) / 32), tiles_n = (int)((N + 31) / 32);
   const dim3 grid((unsigned)((int64_t)tiles_m * tiles_n));
   if (P)

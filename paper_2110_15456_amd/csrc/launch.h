@@ -35,6 +35,18 @@ __host__ __device__ constexpr int plane_group_bytes(int g, int m, int p) {
   return plane_kind(m, p) == kPlaneFP6 ? 3 * g / 4 : g / 2;
 }
 
+// Packed storage (section V-D; include/fastbfp.h): groups of 16, m even, m/2
+// planes of 3-bit fields (a 2-bit chunk with the value's sign), 6 bytes per
+// group and plane; exponents as a 32-bit E_max word, then 3 bits per group in
+// 24-byte blocks of 64 groups.
+constexpr int kPackedGroup = 16;
+constexpr int kPackedPlaneGroupBytes = 6;
+__host__ __device__ constexpr int64_t packed_exp_bytes(int64_t ngroups) { return 4 + 24 * ((ngroups + 63) / 64); }
+hipError_t launch_quantize_packed(const float* x, int64_t rows, int64_t len, int m, int mode, uint64_t seed,
+                                  uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
+hipError_t launch_dequantize_packed(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int m,
+                                    float* y, hipStream_t s);
+
 hipError_t launch_quantize_rows(const float* x, int64_t rows, int64_t len, int g, int m, int mode, uint64_t seed,
                                 uint8_t* mant, uint8_t* exps, uint32_t* status, hipStream_t s);
 // Groups down the columns of x[R][C], written transposed (rows = C, len = R);
@@ -97,6 +109,6 @@ hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a
 // the int32 group partials P[K/g][M][N] instead of C.
 hipError_t launch_gemm_general(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int m_a, const uint8_t* b_mant,
                                const uint8_t* b_exp, int b_m, int m_b, int64_t M, int64_t N, int64_t K, int g,
-                               float* C, int64_t ldc, int32_t* P, hipStream_t s);
+                               float* C, int64_t ldc, int32_t* P, hipStream_t s, bool packed = false);
 
 }  // namespace fastbfp

@@ -212,3 +212,78 @@ def encode(q: np.ndarray, m: int) -> np.ndarray:
             v = codes[:, 0] | (codes[:, 1] << 6) | (codes[:, 2] << 12) | (codes[:, 3] << 18)
             out.append(np.stack([v & 255, (v >> 8) & 255, (v >> 16) & 255], axis=-1).astype(np.uint8).reshape(-1))
     return np.concatenate(out)
+
+
+# ---------------------------------------------------------------------------
+# Packed storage (section V-D): 2-bit chunks with the value's sign in 3-bit
+# fields, ceil(m/2) planes, 16 fields per group in 6 bytes; a uint32 E_max
+# word, then 3-bit exponent offsets above B = max(E_max - 7, 0).
+
+
+def packed_planes(m: int) -> int:
+    return (m + 1) // 2
+
+
+def encode_packed(q: np.ndarray, E: np.ndarray, emax: int, m: int):
+    """(mant, exp) bytes for +-q [rows, length] with group exponents E
+    [rows, length/16] and the tensor's largest exponent field emax."""
+    q = np.asarray(q, dtype=np.int64)
+    rows, length = q.shape
+    ng = rows * length // 16
+    base = max(emax - 7, 0)
+    e3 = np.asarray(E, dtype=np.int64).reshape(-1) - base
+    if np.any((e3 < 0) | (e3 > 7)):
+        raise ValueError("a group exponent is outside base .. base + 7")
+    mag, neg = np.abs(q).reshape(ng, 16), (q < 0).reshape(ng, 16)
+    npl = packed_planes(m)
+    mant = np.zeros((npl, ng, 6), np.uint8)
+    for c in range(npl):
+        ch = (mag >> (2 * (npl - 1 - c))) & 3
+        field = np.where(ch != 0, ch | (neg.astype(np.int64) << 2), 0)
+        bits = np.zeros(ng, np.uint64)
+        for t in range(16):
+            bits |= field[:, t].astype(np.uint64) << np.uint64(3 * t)
+        for k in range(6):
+            mant[c, :, k] = ((bits >> np.uint64(8 * k)) & np.uint64(255)).astype(np.uint8)
+    stream = np.zeros(24 * ((ng + 63) // 64), np.uint8)
+    gid = np.arange(ng)
+    for b in range(3):
+        pos = 3 * gid + b
+        np.add.at(stream, pos // 8, (((e3 >> b) & 1) << (pos % 8)).astype(np.uint8))  # distinct bits: add is OR
+    exp = np.concatenate([np.frombuffer(np.uint32(emax).tobytes(), np.uint8), stream])
+    return mant.reshape(-1), exp
+
+
+def decode_packed(mant: np.ndarray, exp: np.ndarray, rows: int, length: int, m: int):
+    """(+-q [rows, length] int32, E [rows, length/16] int64, emax) from packed
+    bytes; raises if a nonzero chunk's sign disagrees with another's."""
+    ng = rows * length // 16
+    npl = packed_planes(m)
+    mb = np.ascontiguousarray(mant, dtype=np.uint8).reshape(npl, ng, 6).astype(np.uint64)
+    mag = np.zeros((ng, 16), np.int64)
+    sgn = np.full((ng, 16), -1, np.int64)  # -1: no nonzero chunk seen yet
+    for c in range(npl):
+        bits = np.zeros(ng, np.uint64)
+        for k in range(6):
+            bits |= mb[c, :, k] << np.uint64(8 * k)
+        for t in range(16):
+            f = ((bits >> np.uint64(3 * t)) & np.uint64(7)).astype(np.int64)
+            ch, s = f & 3, f >> 2
+            if np.any((ch == 0) & (s == 1)):
+                raise AssertionError("a zero chunk is stored with a sign")
+            nz = ch != 0
+            if np.any(nz & (sgn[:, t] >= 0) & (sgn[:, t] != s)):
+                raise AssertionError("the chunks of a value carry different signs")
+            sgn[nz, t] = s[nz]
+            mag[:, t] = 4 * mag[:, t] + ch
+    q = np.where(sgn == 1, -mag, mag).reshape(rows, length).astype(np.int32)
+    eb = np.ascontiguousarray(exp, dtype=np.uint8)
+    emax = int(np.frombuffer(eb[:4].tobytes(), np.uint32)[0])
+    base = max(emax - 7, 0)
+    stream = eb[4:]
+    E = np.full(ng, base, np.int64)
+    gid = np.arange(ng)
+    for b in range(3):
+        pos = 3 * gid + b
+        E += ((stream[pos // 8].astype(np.int64) >> (pos % 8)) & 1) << b
+    return q, E.reshape(rows, length // 16), emax

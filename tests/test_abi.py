@@ -293,3 +293,68 @@ def test_dual_and_update_validation(lib):
     assert u(*args(dw=FAKE)) == E_ARG        # dw overlaps w_out
     assert u(*args(R=24)) == E_SHAPE
     assert u(*args(w=None, R=0)) == OK
+
+
+def test_packed_sizes_match_the_paper(lib):
+    """Section V-D: a group of g values takes e + g * (m/2) * 3 bits (a 2-bit
+    chunk and its sign in 3 bits); with e = 3 and g = 16 that is 51/16 bits per
+    value at m = 2 and 99/16 at m = 4 (printed rounded as 3.2 and 6.2).  The
+    library's sizes add only the 32-bit E_max word when the group count is a
+    multiple of 64."""
+    from fractions import Fraction
+    mb, eb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    for m, bits in [(2, Fraction(51, 16)), (4, Fraction(99, 16)), (6, Fraction(147, 16)), (8, Fraction(195, 16))]:
+        for rows, length in [(64, 16), (8, 1024), (1024, 1024)]:
+            assert lib.bfp_packed_sizes(rows, length, m, ctypes.byref(mb), ctypes.byref(eb)) == OK
+            n = rows * length
+            assert Fraction(8 * (mb.value + eb.value - 4), n) == bits, (m, rows, length)
+            assert eb.value == 4 + 3 * n // 16 // 8
+    assert round(float(Fraction(51, 16)), 1) == 3.2 and round(float(Fraction(99, 16)), 1) == 6.2
+    # odd widths take ceil(m/2) planes; a partial block of 64 groups is padded to 24 bytes
+    assert lib.bfp_packed_sizes(3, 32, 3, ctypes.byref(mb), ctypes.byref(eb)) == OK
+    assert (mb.value, eb.value) == (2 * 6 * 6, 4 + 24)
+    assert lib.bfp_packed_sizes(0, 32, 4, ctypes.byref(mb), ctypes.byref(eb)) == OK and mb.value == 0
+    assert lib.bfp_packed_sizes(3, 40, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_SHAPE
+    assert lib.bfp_packed_sizes(3, 32, 9, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC
+    assert lib.bfp_packed_sizes(3, 32, 0, ctypes.byref(mb), ctypes.byref(eb)) == E_PREC
+    assert lib.bfp_packed_sizes(-1, 32, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_ARG
+    assert lib.bfp_packed_sizes(3, 32, 4, None, ctypes.byref(eb)) == E_ARG
+    assert lib.bfp_packed_sizes(1 << 40, 1 << 21, 4, ctypes.byref(mb), ctypes.byref(eb)) == E_UNSUP
+
+
+def test_packed_validation(lib):
+    qp, dq, gp = lib.bfp_quantize_packed, lib.bfp_dequantize_packed, lib.bfp_gemm_packed
+    assert qp(None, 4, 64, 4, 0, 0, FAKE, FAKE, None, None) == E_ARG
+    assert qp(FAKE, 4, 64, 4, 0, 0, None, FAKE, None, None) == E_ARG
+    assert qp(FAKE, 4, 64, 4, 3, 0, FAKE, FAKE, None, None) == E_ARG
+    assert qp(FAKE, 4, 40, 4, 0, 0, FAKE, FAKE, None, None) == E_SHAPE
+    assert qp(FAKE, 4, 64, 9, 0, 0, FAKE, FAKE, None, None) == E_PREC
+    assert qp(ctypes.c_void_p(0x100004), 4, 64, 4, 0, 0, FAKE, FAKE, None, None) == E_ARG
+    assert qp(FAKE, 4, 64, 4, 0, 0, FAKE, ctypes.c_void_p(0x100002), None, None) == E_ARG
+    assert qp(None, 0, 64, 4, 0, 0, None, None, None, None) == OK
+    assert qp(FAKE, 1 << 40, 1 << 16, 4, 0, 0, FAKE, FAKE, None, None) == E_UNSUP  # > 2^31 workgroups
+    assert dq(None, FAKE, 4, 64, 4, FAKE, None) == E_ARG
+    assert dq(FAKE, FAKE, 4, 40, 4, FAKE, None) == E_SHAPE
+    assert dq(FAKE, FAKE, 4, 64, 0, FAKE, None) == E_PREC
+    assert dq(FAKE, FAKE, 4, 64, 4, ctypes.c_void_p(0x100004), None) == E_ARG
+    assert dq(FAKE, FAKE, 0, 64, 4, None, None) == OK
+
+    def g(a=FAKE, ae=FAKE, am=4, b=FAKE, be=FAKE, bm=4, M=8, N=8, K=64, ma=4, mb=4, C=FAKE, ldc=8):
+        return gp(a, ae, am, b, be, bm, M, N, K, ma, mb, C, ldc, None)
+
+    assert g(a=None) == E_ARG and g(C=None) == E_ARG and g(be=None) == E_ARG
+    assert g(ae=ctypes.c_void_p(0x100002)) == E_ARG
+    assert g(K=40) == E_SHAPE and g(ldc=7) == E_SHAPE
+    assert g(ma=5) == E_PREC and g(am=9) == E_PREC and g(mb=0) == E_PREC
+    assert g(M=0) == OK and g(am=8, ma=3, N=0, ldc=0) == OK
+
+
+def test_general_kernel_grid_bound(lib):
+    """The general kernel's 32 x 32 tiles bound M and N more tightly than the
+    block-scaled kernel's: such shapes are rejected, not launched."""
+    n = 1 << 21  # 2^29 tiles of 128 x 64 (accepted there), 2^32 of 32 x 32
+    assert ((n + 127) // 128) * ((n + 63) // 64) < 2 ** 31 <= ((n + 31) // 32) ** 2
+    assert gm(lib, g=8, M=n, N=n, ldc=n) == E_UNSUP
+    assert gm(lib, g=16, M=n, N=n, ldc=n, am=6, ma=3) == E_UNSUP
+    assert lib.bfp_gemm_group_partials(FAKE, 4, FAKE, 4, n, n, 64, 16, 4, 4, FAKE, None) == E_UNSUP
+    assert lib.bfp_gemm_packed(FAKE, FAKE, 4, FAKE, FAKE, 4, n, n, 64, 4, 4, FAKE, n, None) == E_UNSUP

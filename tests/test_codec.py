@@ -87,3 +87,43 @@ def test_lo2_plane_is_the_squeezed_fp6_codes():
 def test_fp4_rejects_wide_chunks():
     with pytest.raises(ValueError):
         bfp_codec.encode(np.full((1, 16), 4), 2)
+
+
+def test_packed_fields_worked_by_hand():
+    """Section V-D's chunk storage at m = 4: q = 5 (chunks 01, 01), q = -3
+    (chunks 00, 11 with the sign), q = 0 and q = -12 (chunks 11, 00 with the
+    sign) as the first four values of one group; the other values are zero."""
+    q = np.zeros((1, 16), np.int64)
+    q[0, :4] = [5, -3, 0, -12]
+    mant, exp = bfp_codec.encode_packed(q, np.array([[130]]), emax=133, m=4)
+    # plane 0 (upper chunks): fields 1, 0, 0, 4|3 -> bits 1 | 7 << 9
+    # plane 1 (lower chunks): fields 1, 4|3, 0, 0 -> bits 1 | 7 << 3
+    p0 = 1 | (7 << 9)
+    p1 = 1 | (7 << 3)
+    assert mant.tolist() == [p0 & 255, p0 >> 8, 0, 0, 0, 0, p1 & 255, p1 >> 8, 0, 0, 0, 0]
+    # E_max 133 -> base 126; the group's offset 130 - 126 = 4 in bits 0..2
+    assert exp.tolist() == [133, 0, 0, 0, 4] + [0] * 23
+    q2, E2, emax = bfp_codec.decode_packed(mant, exp, 1, 16, 4)
+    assert np.array_equal(q2, q) and E2.tolist() == [[130]] and emax == 133
+
+
+@pytest.mark.parametrize("m", range(1, 9))
+def test_packed_round_trip_and_sizes(m):
+    rng = np.random.default_rng(100 + m)
+    rows, length = 5, 16 * 29  # 145 groups: two full blocks of 64 and a partial one
+    q = rng.integers(-(2 ** m - 1), 2 ** m, size=(rows, length))
+    E = rng.integers(200, 208, size=(rows, length // 16))
+    mant, exp = bfp_codec.encode_packed(q, E, emax=207, m=m)
+    ng = rows * length // 16
+    assert mant.size == ((m + 1) // 2) * 6 * ng and exp.size == 4 + 24 * 3
+    q2, E2, emax = bfp_codec.decode_packed(mant, exp, rows, length, m)
+    assert np.array_equal(q2, q) and np.array_equal(E2, E) and emax == 207
+    # the exponent fields cross byte boundaries: group 1's bits are 3..5, group 2's 6..8
+    assert (int(exp[4]) >> 3) & 7 == E.reshape(-1)[1] - 200
+    assert ((int(exp[4]) >> 6) | (int(exp[5]) << 2)) & 7 == E.reshape(-1)[2] - 200
+
+
+def test_packed_rejects_exponents_outside_the_window():
+    q = np.zeros((1, 16), np.int64)
+    with pytest.raises(ValueError):
+        bfp_codec.encode_packed(q, np.array([[100]]), emax=120, m=2)  # 100 < 113
