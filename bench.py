@@ -97,6 +97,8 @@ def parse():
     p.add_argument("--gemm-pairs", choices=("default", "all", "resnet"), default="default",
                    help="GEMM sweep: six pairs on four shapes, all 16 operand-format pairs on ffn_up, or the "
                         "ResNet-18 im2col shapes alone")
+    p.add_argument("--formats-only", action="store_true",
+                   help="only the packed-storage, group-size and lowered-precision sweep (general kernel)")
     p.add_argument("--quantize-only", action="store_true",
                    help="run only the 64M quantize sweep (per distribution) and print its JSON")
     p.add_argument("--cpu-only", action="store_true",
@@ -384,6 +386,69 @@ def epilogue_sweep(torch, fb, synth, dev, args):
     return out
 
 
+def format_sweep(torch, fb, synth, dev, args):
+    """The cases the block-scaled kernel does not read as stored: the packed
+    storage of section V-D (conversion with its E_max pass), group sizes 8
+    and 64, and a GEMM taken below the stored width (stored 4, used at 2;
+    stored 6, used at 3), on the out-projection shape (8192 x 4096 x 4096)
+    and an 8192 x 8192 conversion.  Each GEMM is timed on both routes: the
+    default one (bfp_gemm_ws: the operands repacked into a workspace, then
+    the block-scaled kernel; the repack is inside the timed region) and the
+    allocation-free general kernel (bfp_gemm / bfp_gemm_packed)."""
+    out = {}
+
+    def timed(fn, reps=3):
+        fn()
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        z.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(z) / reps
+
+    n = 8192 * 8192
+    x = torch.from_numpy(synth.draw("half_normal", (8192, 8192), 21)).to(dev)
+    for m in (2, 4):
+        for mode in ("nearest", "stochastic"):
+            ms = timed(lambda: fb.quantize_packed(x, m=m, rounding=mode, seed=1234), reps=6)
+            mb, eb = fb.packed_sizes(8192, 8192, m)
+            moved = 2 * n * 4 + mb + eb  # x read by the E_max pass and by the conversion
+            out["packed_quantize_m%d_%s" % (m, mode)] = {
+                "us": round(ms * 1e3, 2), "GB_s_moved": round(moved / (ms * 1e-3) / 1e9, 1),
+                "frac_hbm": round(moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                "bits_per_value": round(8.0 * (mb + eb) / n, 4)}
+            log(args, "packed quantize m=%d %s: %.1f us" % (m, mode, ms * 1e3))
+    del x
+    M, N, K = 8192, 4096, 4096
+    X = torch.from_numpy(synth.draw("normal", (M, K), 41)).to(dev)
+    W = torch.from_numpy(synth.draw("weights", (N, K), 42)).to(dev)
+    C = torch.empty((M, N), dtype=torch.float32, device=dev)
+    cases = []
+    for m in (2, 4):
+        A, B = fb.quantize_packed(X, m=m), fb.quantize_packed(W, m=m)
+        cases.append(("packed(%d,%d)" % (m, m), lambda ws, A=A, B=B: fb.gemm_packed(A, B, out=C, workspace=ws)))
+    for g in (8, 64):
+        A, B = fb.quantize(X, g=g, m=4), fb.quantize(W, g=g, m=4)
+        cases.append(("g%d(4,4)" % g, lambda ws, A=A, B=B: fb.gemm(A, B, out=C, workspace=ws)))
+    for stored, used in ((4, 2), (6, 3)):
+        A, B = fb.quantize(X, g=G, m=stored), fb.quantize(W, g=G, m=stored)
+        cases.append(("stored%d_used(%d,%d)" % (stored, used, used),
+                      lambda ws, A=A, B=B, u=used: fb.gemm(A, B, u, u, out=C, workspace=ws)))
+    tops = lambda ms: 2.0 * M * N * K / (ms * 1e-3) / 1e12
+    for name, fn in cases:
+        ms = timed(lambda: fn(True))
+        ms_general = timed(lambda: fn(False), reps=2)
+        out["out_proj_" + name] = {"ms": round(ms, 4), "eff_tops": round(tops(ms), 1),
+                                   "frac_int8_peak": round(tops(ms) / PEAK_INT8_TOPS, 4),
+                                   "general_kernel_ms": round(ms_general, 3),
+                                   "general_kernel_eff_tops": round(tops(ms_general), 1)}
+        log(args, "GEMM out_proj %s: %.3f ms repacked, %.3f ms on the general kernel" % (name, ms, ms_general))
+    del X, W, C, cases
+    return out
+
+
 def calibration_copy(torch, dev):
     """A plain 256 MiB device copy (torch), three times: its profiler
     counters calibrate the HBM byte counts of the other kernels."""
@@ -538,6 +603,9 @@ def main():
             res["copy_calibration_bytes"] = calibration_copy(torch, dev)
         print(json.dumps(res), flush=True)
         return
+    if args.formats_only:
+        print(json.dumps({"format_sweep": format_sweep(torch, fb, synth, dev, args)}), flush=True)
+        return
     if args.gemm_only:
         if args.gemm_pairs == "resnet":
             print(json.dumps({"resnet_sweep": resnet_sweep(torch, fb, synth, dev, args)}), flush=True)
@@ -634,6 +702,8 @@ def main():
         torch.cuda.empty_cache()
         result["quantize_sweep"] = quantize_sweep(torch, fb, synth, dev, args)
         result["epilogue_sweep"] = epilogue_sweep(torch, fb, synth, dev, args)
+        torch.cuda.empty_cache()
+        result["format_sweep"] = format_sweep(torch, fb, synth, dev, args)
     if not args.no_cpu:
         log(args, "timing the CPU oracle on a sample ...")
         result["cpu_baseline"] = cpu_baseline(args)

@@ -198,7 +198,9 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
  *                  general kernel: int8 MFMA on the decoded, truncated
  *                  magnitudes of one group at a time, each exact integer
  *                  group partial scaled exactly by its power of two and added
- *                  in FP32 (same result contract, lower throughput).
+ *                  in FP32 (same result contract, far lower throughput;
+ *                  bfp_gemm_ws runs these cases on the block-scaled kernel
+ *                  with a caller workspace).
  *   C            : FP32 with row stride ldc >= N (elements).
  *   Size limits  : M, N < 2^31, K <= 11184784 (256 rows of 12 bytes per 16
  *                  values stay below 2^31 bytes: the kernels address operand
@@ -212,6 +214,61 @@ int bfp_dequantize(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_
 int bfp_gemm(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
              int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, float* C, int64_t ldc,
              void* stream);
+
+/*
+ * bfp_repack -- re-encodes a stored BFP tensor into the chunk-plane layout at
+ * m_use bits with groups of 16 or 32, the form the block-scaled GEMM kernel
+ * reads.  The values are those the stored tensor stands for at m_use bits:
+ * every magnitude truncated to its top m_use bits (the paper's discard of
+ * low-order bits, section V-D), the exponents unchanged.
+ *   mant, exp   : the source, rows x len with groups of g in the chunk-plane
+ *                 layout (packed = 0; g in {4, 8, 16, 32, 64}), or in the
+ *                 packed storage (packed = 1; g must be 16), stored with
+ *                 m_bits (1..8).
+ *   m_use       : 1 .. m_bits (BFP_E_PRECISION otherwise).
+ *   out_mant, out_exp : the result, sized by bfp_repack_sizes: rows x len_out
+ *                 with groups of g_out, m_use bits, where
+ *                   g = 4, 8     : len_out = len * 16/g, g_out = 16 -- group G
+ *                                  becomes 16-value unit G: its g values,
+ *                                  then 16 - g zeros, with the group's
+ *                                  exponent;
+ *                   g = 16, 32   : len_out = len, g_out = g;
+ *                   g = 64       : len_out = len, g_out = 32 -- both halves of
+ *                                  a group take its exponent.
+ *                 A product of two tensors repacked from the same g sums the
+ *                 same exact per-group terms T_G as the stored tensors at
+ *                 (m_a, m_b): the padding zeros meet zeros, and the two halves
+ *                 of a group of 64 add up to its integer dot product.
+ * Pointers: mant and out_mant 4-byte aligned, exp too when packed.
+ */
+int bfp_repack_sizes(int64_t rows, int64_t len, int g, int m_use, size_t* mant_bytes, size_t* exp_bytes,
+                     int64_t* len_out, int* g_out);
+int bfp_repack(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int g, int m_bits, int packed,
+               int m_use, uint8_t* out_mant, uint8_t* out_exp, void* stream);
+
+/*
+ * bfp_gemm_ws -- bfp_gemm (the same product and result contract, section
+ * III-B) with a caller workspace, so that every case runs on the block-scaled
+ * MFMA kernel: an operand the kernel cannot read as stored -- a group size of
+ * 4, 8 or 64, a precision that is not a chunk boundary, or packed storage
+ * (packed = 1: both operands in the packed storage, g = 16) -- is first
+ * re-encoded into the workspace by bfp_repack at (m_a, m_b), and the kernel
+ * then runs on K_out = len_out with groups of g_out.  Products bfp_gemm
+ * already runs on that kernel need no workspace.  bfp_gemm itself keeps
+ * running the other cases on its general kernel, allocation- and
+ * workspace-free, at a far lower rate.
+ *   workspace   : device memory of at least bfp_gemm_ws_size bytes (may be
+ *                 NULL when that is 0), 256-byte aligned; its contents on
+ *                 entry do not matter and are overwritten.  Calls that share
+ *                 a workspace must not overlap.
+ *   Size limits : as bfp_gemm, with K_out in place of K (BFP_E_UNSUPPORTED).
+ *   BFP_E_ARG   : also for a workspace below the required size.
+ */
+int bfp_gemm_ws_size(int a_m_bits, int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int packed,
+                     size_t* bytes);
+int bfp_gemm_ws(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+                int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int packed, float* C,
+                int64_t ldc, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * bfp_gemm_tiled -- bfp_gemm (the same product, section III-B) with the C tile
@@ -279,7 +336,7 @@ int bfp_gemm_group_partials(const uint8_t* a_mant, int a_m_bits, const uint8_t* 
  * together, and a 3-bit shared exponent, so that a group of g = 16 takes
  * e + 16 * ceil(m/2) * 3 bits (3.1875 bits per value at m = 2, 6.1875 at
  * m = 4, with e = 3).  This is a storage form: bfp_gemm_packed reads it on the
- * general kernel (the block-scaled kernel takes the chunk-plane layout above).
+ * general kernel, or after bfp_repack on the block-scaled kernel (bfp_gemm_ws).
  *   Groups      : 16 consecutive values along each row (len a multiple of 16).
  *   Exponents   : a 3-bit exponent cannot hold an FP32 exponent field, so it is
  *                 read as an offset above one base per tensor: exp starts with
@@ -342,7 +399,9 @@ int bfp_dequantize_packed(const uint8_t* mant, const uint8_t* exp, int64_t rows,
  * product P_G taken on int8 MFMA, scaled by 2^(ea + eb - 254 - (m_a-1) -
  * (m_b-1)) and added in FP32.  C FP32 with row stride ldc >= N.  Size limits:
  * as bfp_gemm, and ceil(M/32) * ceil(N/32) < 2^31.  exp pointers 4-byte
- * aligned.
+ * aligned.  Allocation- and workspace-free; bfp_gemm_ws with packed = 1 runs
+ * the same product on the block-scaled kernel (operands unpacked into a
+ * caller workspace).
  */
 int bfp_gemm_packed(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant,
                     const uint8_t* b_exp, int b_m_bits, int64_t M, int64_t N, int64_t K, int m_a, int m_b, float* C,

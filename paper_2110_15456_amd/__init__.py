@@ -23,7 +23,8 @@ from ._lib import BFPError, check, load
 
 __all__ = ["BFPTensor", "BFPError", "quantize", "quantize_dual", "weight_update", "dequantize", "gemm", "gemm_bfp",
            "gemm_group_partials", "quantize_adaptive", "quantize_adaptive_noalloc", "adaptive_threshold", "adaptive_mantissa", "chunks", "quantized_sizes", "ROUNDING",
-           "PackedBFPTensor", "packed_sizes", "quantize_packed", "dequantize_packed", "gemm_packed"]
+           "PackedBFPTensor", "packed_sizes", "quantize_packed", "dequantize_packed", "gemm_packed", "repack",
+           "gemm_ws_size"]
 
 ROUNDING = {"nearest": 0, "stochastic": 1, "truncate": 2}
 
@@ -297,21 +298,65 @@ def _gemm_args(A: BFPTensor, B: BFPTensor, m_a, m_b):
     return (A.m if m_a is None else int(m_a)), (B.m if m_b is None else int(m_b))
 
 
-def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = None,
-         out: torch.Tensor | None = None, tile: int | None = None) -> torch.Tensor:
-    """C = A . B^T in FP32 [A.rows, B.rows] for BFP A [M, K] and B [N, K].
-
-    m_a / m_b: precision of each operand in the product (default: stored m;
-    for a two-chunk operand, m - 4 drops the low chunk plane).
-    tile: None lets the library choose the workgroup tile from the shape
-    (bfp_gemm); 0..4 forces one (bfp_gemm_tiled: the default tile, 256x128,
-    256x64, 128x64, 128x128 -- the last four for m_a, m_b <= 4 and g = 16 only).
-    """
+def gemm_ws_size(A, B, m_a: int | None = None, m_b: int | None = None) -> int:
+    """Workspace bytes bfp_gemm_ws needs for this product (0 when the
+    block-scaled kernel reads both operands as stored)."""
     m_a, m_b = _gemm_args(A, B, m_a, m_b)
+    nb = ctypes.c_size_t(0)
+    check(load().bfp_gemm_ws_size(A.m, B.m, A.rows, B.rows, A.len, A.g, m_a, m_b,
+                                  1 if isinstance(A, PackedBFPTensor) else 0, ctypes.byref(nb)), "bfp_gemm_ws_size")
+    return nb.value
+
+
+def _gemm_out(A, B, out):
     C = out if out is not None else torch.empty((A.rows, B.rows), dtype=torch.float32, device=A.device)
     _need_cuda(C, "out", torch.float32)
     if C.dim() != 2 or C.shape[0] != A.rows or C.shape[1] != B.rows:
         raise ValueError("out must be [%d, %d]" % (A.rows, B.rows))
+    return C
+
+
+def _gemm_with_workspace(A, B, m_a, m_b, C, workspace):
+    """bfp_gemm_ws: operands the block-scaled kernel cannot read as stored are
+    repacked into a workspace (torch-allocated unless one is given)."""
+    packed = 1 if isinstance(A, PackedBFPTensor) else 0
+    need = gemm_ws_size(A, B, m_a, m_b)
+    if need == 0:
+        ws = None
+    elif isinstance(workspace, torch.Tensor):
+        _need_cuda(workspace, "workspace", torch.uint8)
+        ws = workspace
+        if ws.numel() < need:
+            raise ValueError("workspace needs %d bytes" % need)
+    else:
+        ws = torch.empty(need, dtype=torch.uint8, device=A.device)
+    check(load().bfp_gemm_ws(ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
+                             ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows,
+                             B.rows, A.len, A.g, m_a, m_b, packed, ctypes.c_void_p(C.data_ptr()), C.stride(0),
+                             ctypes.c_void_p(ws.data_ptr()) if ws is not None else None,
+                             ws.numel() if ws is not None else 0, _stream(A.device)), "bfp_gemm_ws")
+    return C
+
+
+def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = None,
+         out: torch.Tensor | None = None, tile: int | None = None, workspace=True) -> torch.Tensor:
+    """C = A . B^T in FP32 [A.rows, B.rows] for BFP A [M, K] and B [N, K].
+
+    m_a / m_b: precision of each operand in the product (default: stored m;
+    any value from 1 to the stored width).
+    tile: None lets the library choose the workgroup tile from the shape;
+    0..4 forces one (bfp_gemm_tiled: the default tile, 256x128, 256x64,
+    128x64, 128x128 -- the last four for m_a, m_b <= 4 and g = 16 only).
+    workspace: True (default) runs every product on the block-scaled kernel,
+    repacking an operand it cannot read as stored (groups of 4, 8, 64; a
+    precision between chunk boundaries) into a workspace allocated here
+    (bfp_gemm_ws), or into a given uint8 CUDA tensor; False calls bfp_gemm,
+    which runs such products on its allocation-free general kernel.
+    """
+    m_a, m_b = _gemm_args(A, B, m_a, m_b)
+    C = _gemm_out(A, B, out)
+    if tile is None and workspace is not False:
+        return _gemm_with_workspace(A, B, m_a, m_b, C, workspace)
     args = (ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
             ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows, B.rows,
             A.len, A.g, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0))
@@ -320,6 +365,23 @@ def gemm(A: BFPTensor, B: BFPTensor, m_a: int | None = None, m_b: int | None = N
     else:
         check(load().bfp_gemm_tiled(*args, int(tile), _stream(A.device)), "bfp_gemm_tiled")
     return C
+
+
+def repack(t, m_use: int | None = None) -> BFPTensor:
+    """bfp_repack: t (a BFPTensor, or a PackedBFPTensor) re-encoded at m_use
+    bits (default: its width) in the chunk-plane layout with groups of 16 (t's
+    g <= 16; groups of 4 and 8 zero-padded to 16-value units) or 32."""
+    m_use = t.m if m_use is None else int(m_use)
+    mb, eb, lo, go = ctypes.c_size_t(0), ctypes.c_size_t(0), ctypes.c_int64(0), ctypes.c_int(0)
+    check(load().bfp_repack_sizes(t.rows, t.len, t.g, m_use, ctypes.byref(mb), ctypes.byref(eb), ctypes.byref(lo),
+                                  ctypes.byref(go)), "bfp_repack_sizes")
+    r = BFPTensor(torch.empty(mb.value, dtype=torch.uint8, device=t.device),
+                  torch.empty((t.rows, lo.value // go.value), dtype=torch.uint8, device=t.device), t.rows, lo.value,
+                  go.value, m_use)
+    check(load().bfp_repack(ctypes.c_void_p(t.mant.data_ptr()), ctypes.c_void_p(t.exp.data_ptr()), t.rows, t.len, t.g,
+                            t.m, 1 if isinstance(t, PackedBFPTensor) else 0, m_use, ctypes.c_void_p(r.mant.data_ptr()),
+                            ctypes.c_void_p(r.exp.data_ptr()), _stream(t.device)), "bfp_repack")
+    return r
 
 
 def gemm_bfp(A: BFPTensor, B: BFPTensor, c_m: int, m_a: int | None = None, m_b: int | None = None,
@@ -418,13 +480,14 @@ def dequantize_packed(t: PackedBFPTensor, out: torch.Tensor | None = None) -> to
 
 
 def gemm_packed(A: PackedBFPTensor, B: PackedBFPTensor, m_a: int | None = None, m_b: int | None = None,
-                out: torch.Tensor | None = None) -> torch.Tensor:
-    """C = A . B^T in FP32 [A.rows, B.rows] for packed A [M, K] and B [N, K]."""
+                out: torch.Tensor | None = None, workspace=True) -> torch.Tensor:
+    """C = A . B^T in FP32 [A.rows, B.rows] for packed A [M, K] and B [N, K].
+    workspace: as for gemm (True: unpacked into a workspace and run on the
+    block-scaled kernel; False: bfp_gemm_packed's general kernel)."""
     m_a, m_b = _gemm_args(A, B, m_a, m_b)
-    C = out if out is not None else torch.empty((A.rows, B.rows), dtype=torch.float32, device=A.device)
-    _need_cuda(C, "out", torch.float32)
-    if C.dim() != 2 or C.shape[0] != A.rows or C.shape[1] != B.rows:
-        raise ValueError("out must be [%d, %d]" % (A.rows, B.rows))
+    C = _gemm_out(A, B, out)
+    if workspace is not False:
+        return _gemm_with_workspace(A, B, m_a, m_b, C, workspace)
     check(load().bfp_gemm_packed(ctypes.c_void_p(A.mant.data_ptr()), ctypes.c_void_p(A.exp.data_ptr()), A.m,
                                  ctypes.c_void_p(B.mant.data_ptr()), ctypes.c_void_p(B.exp.data_ptr()), B.m, A.rows,
                                  B.rows, A.len, m_a, m_b, ctypes.c_void_p(C.data_ptr()), C.stride(0),

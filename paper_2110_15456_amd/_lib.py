@@ -34,6 +34,11 @@ SIGNATURES = {
     "bfp_quantize_packed": (_I, [_P, _I64, _I64, _I, _I, _U64, _P, _P, _P, _P]),
     "bfp_dequantize_packed": (_I, [_P, _P, _I64, _I64, _I, _P, _P]),
     "bfp_gemm_packed": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _P, _I64, _P]),
+    "bfp_repack_sizes": (_I, [_I64, _I64, _I, _I, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t),
+                              ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int)]),
+    "bfp_repack": (_I, [_P, _P, _I64, _I64, _I, _I, _I, _I, _P, _P, _P]),
+    "bfp_gemm_ws_size": (_I, [_I, _I, _I64, _I64, _I64, _I, _I, _I, _I, ctypes.POINTER(ctypes.c_size_t)]),
+    "bfp_gemm_ws": (_I, [_P, _P, _I, _P, _P, _I, _I64, _I64, _I64, _I, _I, _I, _I, _P, _I64, _P, ctypes.c_size_t, _P]),
     "bfp_quantize_dual": (_I, [_P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P, _P]),
     "bfp_weight_update": (_I, [_P, _P, ctypes.c_float, _P, _I64, _I64, _I, _I, _I, _U64, _U64, _P, _P, _P, _P, _P,
                                _P]),

@@ -46,10 +46,21 @@ bool fast_path(int a_m, int b_m, int g, int m_a, int m_b) {
   return (g == 16 || g == 32) && planes_used(a_m, m_a) != 0 && planes_used(b_m, m_b) != 0;
 }
 
+// The shape and precision rules of a GEMM (no pointers).
+int check_gemm_shape(int a_m, int b_m, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b);
+
 int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, int64_t M, int64_t N, int64_t K, int g,
                int m_a, int m_b) {
   if (M < 0 || N < 0 || K < 0) return BFP_E_ARG;
   if ((M > 0 && K > 0 && !a_mant) || (N > 0 && K > 0 && !b_mant)) return BFP_E_ARG;
+  const int st = check_gemm_shape(a_m, b_m, M, N, K, g, m_a, m_b);
+  if (st != BFP_OK) return st;
+  if (!aligned(a_mant, 4) || !aligned(b_mant, 4)) return BFP_E_ARG;
+  return BFP_OK;
+}
+
+int check_gemm_shape(int a_m, int b_m, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b) {
+  if (M < 0 || N < 0 || K < 0) return BFP_E_ARG;
   if (a_m < 1 || a_m > 8 || b_m < 1 || b_m > 8) return BFP_E_PRECISION;
   if (g <= 0) return BFP_E_ARG;
   if (!group_supported(g)) return BFP_E_UNSUPPORTED;
@@ -62,7 +73,6 @@ int check_gemm(const uint8_t* a_mant, int a_m, const uint8_t* b_mant, int b_m, i
   // must fit in 31 bits.
   if (M > 0x7fffffff || N > 0x7fffffff || K > kMaxK) return BFP_E_UNSUPPORTED;
   if (((M + 127) / 128) * ((N + 63) / 64) > 0x7fffffff) return BFP_E_UNSUPPORTED;
-  if (!aligned(a_mant, 4) || !aligned(b_mant, 4)) return BFP_E_ARG;
   return BFP_OK;
 }
 
@@ -78,6 +88,36 @@ int check_packed(int64_t rows, int64_t len, int m) {
   return BFP_OK;
 }
 
+size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+
+// How bfp_gemm_ws runs a product: which operands it repacks into the layout
+// of the block-scaled kernel, the K and group size that kernel then sees, and
+// the workspace the repacked operands take (A's mantissas and exponents, then
+// B's, each 256-byte aligned).
+struct WsPlan {
+  bool rep_a, rep_b;
+  int64_t k_out;
+  int g_out;
+  size_t a_mant, a_exp, b_mant, b_exp, bytes;
+};
+
+int ws_plan(int a_m, int b_m, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int packed, WsPlan* p) {
+  if (packed != 0 && packed != 1) return BFP_E_ARG;
+  if (packed && g != 16) return BFP_E_UNSUPPORTED;
+  const bool native = g == 16 || g == 32;
+  p->rep_a = packed || !native || planes_used(a_m, m_a) == 0;
+  p->rep_b = packed || !native || planes_used(b_m, m_b) == 0;
+  fastbfp::repack_shape(K, g, &p->k_out, &p->g_out);
+  if (p->k_out > kMaxK) return BFP_E_UNSUPPORTED;
+  p->a_mant = p->a_exp = p->b_mant = p->b_exp = 0;
+  if (p->rep_a && bfp_quantized_sizes(M, p->k_out, p->g_out, m_a, &p->a_mant, &p->a_exp) != BFP_OK)
+    return BFP_E_UNSUPPORTED;
+  if (p->rep_b && bfp_quantized_sizes(N, p->k_out, p->g_out, m_b, &p->b_mant, &p->b_exp) != BFP_OK)
+    return BFP_E_UNSUPPORTED;
+  p->bytes = align256(p->a_mant) + align256(p->a_exp) + align256(p->b_mant) + align256(p->b_exp);
+  return BFP_OK;
+}
+
 int check_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, const uint8_t* mr,
                const uint8_t* er, const uint8_t* mc, const uint8_t* ec, const uint32_t* status_word) {
   if (round_mode < BFP_ROUND_NEAREST || round_mode > BFP_ROUND_TRUNCATE) return BFP_E_ARG;
@@ -86,6 +126,7 @@ int check_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int roun
   if (g != 16) return BFP_E_UNSUPPORTED;
   if (R % 16 != 0) return BFP_E_SHAPE;
   if (C >= (int64_t(1) << 22)) return BFP_E_UNSUPPORTED;
+  if (((R + 63) / 64) * ((C + 63) / 64) > 0x7fffffff) return BFP_E_UNSUPPORTED;  // 64 x 64 tiles in an int
   if (R == 0 || C == 0) return BFP_OK;
   if (!x || !mr || !er || !mc || !ec) return BFP_E_ARG;
   if (!aligned(x, 16) || !aligned(mr, 4) || !aligned(mc, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
@@ -291,6 +332,92 @@ int bfp_gemm_packed(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, c
   return status_of(fastbfp::launch_gemm_general(a_mant, a_exp, a_m_bits, m_a, b_mant, b_exp, b_m_bits, m_b, M, N, K,
                                                 fastbfp::kPackedGroup, C, ldc, nullptr,
                                                 static_cast<hipStream_t>(stream), true));
+}
+
+int bfp_repack_sizes(int64_t rows, int64_t len, int g, int m_use, size_t* mant_bytes, size_t* exp_bytes,
+                     int64_t* len_out, int* g_out) {
+  if (!mant_bytes || !exp_bytes || !len_out || !g_out) return BFP_E_ARG;
+  const int st = check_tensor(rows, len, g, m_use);
+  if (st != BFP_OK) return st;
+  int64_t lo;
+  int go;
+  fastbfp::repack_shape(len, g, &lo, &go);
+  if (rows > 0 && lo / 16 > (int64_t(1) << 56) / rows) return BFP_E_UNSUPPORTED;
+  *len_out = lo;
+  *g_out = go;
+  return bfp_quantized_sizes(rows, lo, go, m_use, mant_bytes, exp_bytes);
+}
+
+int bfp_repack(const uint8_t* mant, const uint8_t* exp, int64_t rows, int64_t len, int g, int m_bits, int packed,
+               int m_use, uint8_t* out_mant, uint8_t* out_exp, void* stream) {
+  if (packed != 0 && packed != 1) return BFP_E_ARG;
+  if (packed && g != 16) return BFP_E_UNSUPPORTED;
+  int st = packed ? check_packed(rows, len, m_bits) : check_tensor(rows, len, g, m_bits);
+  if (st != BFP_OK) return st;
+  if (m_use < 1 || m_use > m_bits) return BFP_E_PRECISION;
+  size_t mb, eb;
+  int64_t lo;
+  int go;
+  st = bfp_repack_sizes(rows, len, g, m_use, &mb, &eb, &lo, &go);
+  if (st != BFP_OK) return st;
+  if (rows == 0 || len == 0) return BFP_OK;
+  if (!mant || !exp || !out_mant || !out_exp) return BFP_E_ARG;
+  if (!aligned(mant, 4) || !aligned(out_mant, 4) || (packed && !aligned(exp, 4))) return BFP_E_ARG;
+  if ((rows * (lo / 16) + 255) / 256 > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  return status_of(fastbfp::launch_repack(mant, exp, rows, len, g, m_bits, m_use, packed != 0, out_mant, out_exp,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int bfp_gemm_ws_size(int a_m_bits, int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int packed,
+                     size_t* bytes) {
+  if (!bytes) return BFP_E_ARG;
+  int st = check_gemm_shape(a_m_bits, b_m_bits, M, N, K, g, m_a, m_b);
+  if (st != BFP_OK) return st;
+  WsPlan p;
+  st = ws_plan(a_m_bits, b_m_bits, M, N, K, g, m_a, m_b, packed, &p);
+  if (st != BFP_OK) return st;
+  *bytes = p.bytes;
+  return BFP_OK;
+}
+
+int bfp_gemm_ws(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
+                int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int packed, float* C,
+                int64_t ldc, void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_gemm(a_mant, a_m_bits, b_mant, b_m_bits, M, N, K, g, m_a, m_b);
+  if (st != BFP_OK) return st;
+  if (ldc < N) return BFP_E_SHAPE;
+  WsPlan p;
+  st = ws_plan(a_m_bits, b_m_bits, M, N, K, g, m_a, m_b, packed, &p);
+  if (st != BFP_OK) return st;
+  if (M == 0 || N == 0) return BFP_OK;
+  if (!C || (K > 0 && (!a_exp || !b_exp))) return BFP_E_ARG;
+  if (packed && (!aligned(a_exp, 4) || !aligned(b_exp, 4))) return BFP_E_ARG;
+  if (p.bytes > 0 && (!workspace || workspace_bytes < p.bytes || !aligned(workspace, 256))) return BFP_E_ARG;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  const uint8_t *am = a_mant, *ae = a_exp, *bm = b_mant, *be = b_exp;
+  int a_m = a_m_bits, b_m = b_m_bits;
+  // (with K = 0 nothing is repacked or read: the kernel writes zeros)
+  if (p.rep_a) {
+    a_m = m_a;
+    if (K > 0) {
+      uint8_t *om = ws, *oe = ws + align256(p.a_mant);
+      st = status_of(fastbfp::launch_repack(a_mant, a_exp, M, K, g, a_m_bits, m_a, packed != 0, om, oe, s));
+      if (st != BFP_OK) return st;
+      am = om, ae = oe;
+    }
+  }
+  if (p.rep_b) {
+    b_m = m_b;
+    if (K > 0) {
+      uint8_t *om = ws + align256(p.a_mant) + align256(p.a_exp), *oe = om + align256(p.b_mant);
+      st = status_of(fastbfp::launch_repack(b_mant, b_exp, N, K, g, b_m_bits, m_b, packed != 0, om, oe, s));
+      if (st != BFP_OK) return st;
+      bm = om, be = oe;
+    }
+  }
+  return status_of(fastbfp::launch_gemm_mx(am, ae, a_m, planes_used(a_m, m_a), bm, be, b_m, planes_used(b_m, m_b), M,
+                                           N, p.k_out, p.g_out, 4 - m_a - m_b, C, ldc, -1, s));
 }
 
 int bfp_quantize_dual(const float* x, int64_t R, int64_t C, int g, int m_bits, int round_mode, uint64_t seed_r,

@@ -107,6 +107,13 @@ hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a
 // The general BFP GEMM (gemm_general.hip): any m_a <= a_m and m_b <= b_m, g in
 // {4, 8, 16, 32, 64} (K a multiple of g and of 16).  With P non-null it writes
 // the int32 group partials P[K/g][M][N] instead of C.
+// Re-encoding of a stored tensor (chunk planes with groups of g, or packed)
+// into the chunk-plane layout at m_use bits that the block-scaled kernel reads:
+// len_out = len * 16/g for g < 16 (one group per zero-padded 16-value unit),
+// else len; groups of g_out = 16 (g <= 16) or 32 (g >= 32).
+void repack_shape(int64_t len, int g, int64_t* len_out, int* g_out);
+hipError_t launch_repack(const uint8_t* mant, const uint8_t* exps, int64_t rows, int64_t len, int g, int m, int m_use,
+                         bool packed, uint8_t* out_mant, uint8_t* out_exps, hipStream_t s);
 hipError_t launch_gemm_general(const uint8_t* a_mant, const uint8_t* a_exp, int a_m, int m_a, const uint8_t* b_mant,
                                const uint8_t* b_exp, int b_m, int m_b, int64_t M, int64_t N, int64_t K, int g,
                                float* C, int64_t ldc, int32_t* P, hipStream_t s, bool packed = false);

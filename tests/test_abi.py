@@ -358,3 +358,69 @@ def test_general_kernel_grid_bound(lib):
     assert gm(lib, g=16, M=n, N=n, ldc=n, am=6, ma=3) == E_UNSUP
     assert lib.bfp_gemm_group_partials(FAKE, 4, FAKE, 4, n, n, 64, 16, 4, 4, FAKE, None) == E_UNSUP
     assert lib.bfp_gemm_packed(FAKE, FAKE, 4, FAKE, FAKE, 4, n, n, 64, 4, 4, FAKE, n, None) == E_UNSUP
+
+
+def test_repack_sizes(lib):
+    mb, eb, lo, go = ctypes.c_size_t(0), ctypes.c_size_t(0), ctypes.c_int64(0), ctypes.c_int(0)
+    args = (ctypes.byref(mb), ctypes.byref(eb), ctypes.byref(lo), ctypes.byref(go))
+    # groups of 4 and 8: one zero-padded 16-value unit per group; 64: groups of 32
+    for g, m, want_len, want_g in [(4, 4, 256, 16), (8, 2, 128, 16), (16, 6, 64, 16), (32, 8, 64, 32), (64, 3, 64, 32)]:
+        assert lib.bfp_repack_sizes(3, 64, g, m, *args) == OK
+        assert (lo.value, go.value) == (want_len, want_g)
+        want_mb, want_eb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+        assert lib.bfp_quantized_sizes(3, want_len, want_g, m, ctypes.byref(want_mb), ctypes.byref(want_eb)) == OK
+        assert (mb.value, eb.value) == (want_mb.value, want_eb.value)
+    assert lib.bfp_repack_sizes(3, 40, 8, 4, *args) == E_SHAPE
+    assert lib.bfp_repack_sizes(3, 64, 12, 4, *args) == E_UNSUP
+    assert lib.bfp_repack_sizes(3, 64, 16, 9, *args) == E_PREC
+    assert lib.bfp_repack_sizes(3, 64, 16, 4, None, *args[1:]) == E_ARG
+
+
+def test_repack_validation(lib):
+    f = lib.bfp_repack
+    assert f(FAKE, FAKE, 4, 64, 16, 4, 0, 5, FAKE, FAKE, None) == E_PREC      # cannot raise the width
+    assert f(FAKE, FAKE, 4, 64, 16, 4, 0, 0, FAKE, FAKE, None) == E_PREC
+    assert f(FAKE, FAKE, 4, 64, 16, 4, 2, 2, FAKE, FAKE, None) == E_ARG       # packed is 0 or 1
+    assert f(FAKE, FAKE, 4, 64, 8, 4, 1, 2, FAKE, FAKE, None) == E_UNSUP      # packed storage has g = 16
+    assert f(None, FAKE, 4, 64, 16, 4, 0, 2, FAKE, FAKE, None) == E_ARG
+    assert f(FAKE, FAKE, 4, 64, 16, 4, 0, 2, None, FAKE, None) == E_ARG
+    assert f(FAKE, ctypes.c_void_p(0x100002), 4, 64, 16, 4, 1, 2, FAKE, FAKE, None) == E_ARG  # packed exps
+    assert f(FAKE, FAKE, 4, 40, 16, 4, 0, 2, FAKE, FAKE, None) == E_SHAPE
+    assert f(None, None, 0, 64, 8, 4, 0, 2, None, None, None) == OK
+
+
+def test_gemm_ws_size_and_validation(lib):
+    nb = ctypes.c_size_t(0)
+
+    def size(am=4, bm=4, M=8, N=8, K=64, g=16, ma=4, mb=4, packed=0):
+        st = lib.bfp_gemm_ws_size(am, bm, M, N, K, g, ma, mb, packed, ctypes.byref(nb))
+        return st, nb.value
+
+    # products the block-scaled kernel reads as stored need no workspace
+    assert size() == (OK, 0) and size(g=32) == (OK, 0) and size(am=6, ma=4) == (OK, 0)
+    assert size(am=8, bm=6, ma=4, mb=4) == (OK, 0)
+    # the others: the operands that need it, repacked
+    st, n_a = size(am=4, ma=2)                   # A lowered: its 8 x 64 at m = 2 (FP4: 4 bytes per row-group) + exps
+    assert st == OK and n_a == 256 + 256
+    st, n_both = size(g=8)                       # both operands, K_out = 128: 768 mantissa + 64 exponent bytes each
+    assert st == OK and n_both == 2 * (768 + 256)
+    assert size(packed=1)[0] == OK and size(packed=1)[1] > 0
+    assert size(packed=1, g=8)[0] == E_UNSUP
+    assert size(packed=2)[0] == E_ARG
+    assert size(ma=5)[0] == E_PREC and size(K=40)[0] == E_SHAPE
+    kmax = ((1 << 31) // (256 * 12) - 1) * 16
+    k4 = (kmax // 64 + 1) * 16                   # K_out = 4 K just beyond the kernel's limit
+    assert k4 <= kmax < 4 * k4 and size(K=k4, g=4)[0] == E_UNSUP and size(K=k4 - 16, g=4)[0] == OK
+    assert lib.bfp_gemm_ws_size(4, 4, 8, 8, 64, 16, 4, 4, 0, None) == E_ARG
+
+    def ws(workspace=FAKE, nbytes=1 << 20, ldc=8, C=FAKE, **kw):
+        a = dict(am=4, bm=4, M=8, N=8, K=64, g=16, ma=4, mb=4, packed=0)
+        a.update(kw)
+        return lib.bfp_gemm_ws(FAKE, FAKE, a["am"], FAKE, FAKE, a["bm"], a["M"], a["N"], a["K"], a["g"], a["ma"],
+                               a["mb"], a["packed"], C, ldc, workspace, nbytes, None)
+
+    assert ws(g=8, workspace=None) == E_ARG                       # a workspace is needed
+    assert ws(g=8, nbytes=n_both - 1) == E_ARG                    # too small
+    assert ws(g=8, workspace=ctypes.c_void_p(0x100010)) == E_ARG  # not 256-byte aligned
+    assert ws(ldc=7) == E_SHAPE and ws(C=None) == E_ARG
+    assert ws(M=0, g=8, workspace=None, nbytes=0) == OK           # empty: nothing launched

@@ -118,14 +118,18 @@ def test_dequantize_packed(m):
 
 
 def check_gemm(A, B, qa, ea, qb, eb, m_a, m_b, exact=False):
-    C = fb.gemm_packed(A, B, m_a, m_b)
-    torch.cuda.synchronize()
-    Cg = C.cpu().numpy().astype(np.float64)
+    """bfp_gemm_packed (general kernel) and bfp_gemm_ws (unpacked into a
+    workspace, block-scaled kernel), each against the oracle."""
     Co, S = oracle.gemm(qa, ea, A.m, qb, eb, B.m, g=16, m_a=m_a, m_b=m_b, threads=THREADS)
-    err = np.abs(Cg - Co)
-    assert np.all(err <= 1e-6 * S), "max err/sum|T| = %.3g" % float((err / np.maximum(S, 1e-300)).max())
-    if exact:
-        assert np.array_equal(Cg, Co)
+    for ws in (False, True):
+        C = fb.gemm_packed(A, B, m_a, m_b, workspace=ws)
+        torch.cuda.synchronize()
+        Cg = C.cpu().numpy().astype(np.float64)
+        err = np.abs(Cg - Co)
+        assert np.all(err <= 1e-6 * S), "workspace=%s: max err/sum|T| = %.3g" % (
+            ws, float((err / np.maximum(S, 1e-300)).max()))
+        if exact:
+            assert np.array_equal(Cg, Co), "workspace=%s: not exact" % ws
 
 
 STORED = [(2, 2), (2, 4), (4, 2), (4, 4), (6, 6), (8, 8), (3, 5), (8, 1)]
