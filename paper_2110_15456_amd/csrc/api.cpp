@@ -302,7 +302,7 @@ int bfp_quantize_packed(const float* x, int64_t R, int64_t C, int m_bits, int ro
   if (R == 0 || C == 0) return BFP_OK;
   if (!x || !mant || !exp) return BFP_E_ARG;
   if (!aligned(x, 16) || !aligned(mant, 4) || !aligned(exp, 4) || !aligned(status_word, 4)) return BFP_E_ARG;
-  if ((R * (C / 16) + 255) / 256 > 0x7fffffff) return BFP_E_UNSUPPORTED;
+  if ((R * (C / 16) + 255) / 256 > 0x7fffffff) return BFP_E_UNSUPPORTED;  // 256 groups per workgroup
   return status_of(fastbfp::launch_quantize_packed(x, R, C, m_bits, round_mode, seed, mant, exp, status_word,
                                                    static_cast<hipStream_t>(stream)));
 }

@@ -21,42 +21,77 @@ namespace {
 
 __global__ void k_packed_header_clear(uint32_t* hdr) { *hdr = 0u; }
 
-// hdr = max(hdr, the largest exponent field of x[0 .. 4 n4)).
+// hdr = max(hdr, the largest exponent field of x[0 .. 4 n4)): kExpMaxGranules
+// 16-byte granules per block, in rounds of four independent loads per thread.
+// The word only grows, so a block whose maximum is not above the value it
+// reads skips its atomic.
+constexpr int kExpMaxGranules = 4096;
 __global__ __launch_bounds__(256) void k_exponent_max(const u32x4* __restrict__ x, int64_t n4, uint32_t* hdr) {
+  const int64_t i0 = (int64_t)blockIdx.x * kExpMaxGranules + threadIdx.x;
   uint32_t e = 0;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
-    const u32x4 v = stream_load(x + i);
-    e = max(max(e, (v.x >> 23) & 0xFFu), (v.y >> 23) & 0xFFu);
-    e = max(max(e, (v.z >> 23) & 0xFFu), (v.w >> 23) & 0xFFu);
+#pragma unroll
+  for (int r = 0; r < kExpMaxGranules / 1024; ++r) {
+    u32x4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t i = i0 + 1024 * r + 256 * j;
+      v[j] = i < n4 ? stream_load(x + i) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      e = max(max(e, (v[j].x >> 23) & 0xFFu), (v[j].y >> 23) & 0xFFu);
+      e = max(max(e, (v[j].z >> 23) & 0xFFu), (v[j].w >> 23) & 0xFFu);
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) e = max(e, (uint32_t)__shfl_xor((int)e, off));
   __shared__ uint32_t red[4];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = e;
   __syncthreads();
-  if (threadIdx.x == 0) atomicMax(hdr, max(max(red[0], red[1]), max(red[2], red[3])));
+  if (threadIdx.x == 0) {
+    const uint32_t bmax = max(max(red[0], red[1]), max(red[2], red[3]));
+    if (bmax > __atomic_load_n(hdr, __ATOMIC_RELAXED)) atomicMax(hdr, bmax);
+  }
 }
 
-
-// One lane per group of 16 values along the rows.  NP = ceil(m / 2) chunk planes.
+// One lane per group of 16 values along the rows, a wave per 64 groups.  The
+// wave's 4 KB of input come into its LDS region by four direct global->LDS
+// loads of 1 KB contiguous each; chunk c (16 bytes) of lane l's group lands in
+// slot 4 l + (c ^ ((l / 4) % 4)), so that the 16 lanes served together on the
+// read-back hit all 64 banks.  NP = ceil(m / 2) chunk planes.
 template <int MODE, int NP>
 __global__ __launch_bounds__(256) void k_quantize_packed(const float* __restrict__ x, int64_t ngroups, uint32_t m,
                                                          uint32_t key0, uint32_t key1, uint8_t* __restrict__ mant,
                                                          uint32_t* __restrict__ expw, uint32_t* status) {
+  __shared__ __attribute__((aligned(16))) uint32_t stage[4][64 * 16];
   __shared__ uint32_t e3s[256];
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g0 = ((int64_t)blockIdx.x * 4 + wave) * 64;  // the wave's first group
+  const int64_t gid = g0 + lane;
+  const int nvalid = (int)max((int64_t)0, min((int64_t)64, ngroups - g0));
   const uint32_t base = packed_base(expw[0]);
   uint32_t e3 = 0;
-  if (gid < ngroups) {
-    uint32_t b[16];
-    const u32x4* src = reinterpret_cast<const u32x4*>(x + gid * 16);
+  if (nvalid > 0) {
+    typedef __attribute__((address_space(3))) void lds_void;
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(x) + g0 * 64;
+    const int last = nvalid * 4 - 1;  // chunks of groups past the end reread the last valid one (unused)
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const u32x4 v = stream_load(src + k);
-      b[4 * k] = v.x;
-      b[4 * k + 1] = v.y;
-      b[4 * k + 2] = v.z;
-      b[4 * k + 3] = v.w;
+      const int slot = 64 * k + lane, l = slot / 4, c = (slot % 4) ^ ((l / 4) % 4);
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(src + min(4 * l + c, last) * 16),
+                                       (lds_void*)&stage[wave][64 * 4 * k], 16, 0, kStreamPolicy);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the wave reads back what its own loads wrote
+  }
+  if (lane < nvalid) {
+    uint32_t b[16];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(&stage[wave][4 * (4 * lane + (c ^ ((lane / 4) % 4)))]);
+      b[4 * c] = v.x;
+      b[4 * c + 1] = v.y;
+      b[4 * c + 2] = v.z;
+      b[4 * c + 3] = v.w;
     }
     // (a) the group's exponent, raised to the tensor base
     const uint32_t Eg = group_exponent<16>(b);
@@ -93,9 +128,7 @@ __global__ __launch_bounds__(256) void k_quantize_packed(const float* __restrict
   // from the fields of lanes 32d/3 .. (32d + 31)/3.
   e3s[threadIdx.x] = e3;
   __syncthreads();
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t g0 = (int64_t)blockIdx.x * 256 + wave * 64;
-  if (lane < 6 && g0 < ngroups) {
+  if (lane < 6 && nvalid > 0) {
     uint32_t w = 0;
     for (int l = (32 * lane) / 3; l <= (32 * lane + 31) / 3; ++l) {
       const int sh = 3 * l - 32 * lane;  // -2 .. 31
@@ -169,8 +202,8 @@ hipError_t launch_quantize_packed(const float* x, int64_t rows, int64_t len, int
   // E_max of the tensor first (the base every group's exponent is stored above)
   hipLaunchKernelGGL(k_packed_header_clear, dim3(1), dim3(1), 0, s, expw);
   const int64_t n4 = n / 4;
-  const unsigned blocks = (unsigned)min((int64_t)2048, (n4 + 255) / 256);
-  hipLaunchKernelGGL(k_exponent_max, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const u32x4*>(x), n4, expw);
+  hipLaunchKernelGGL(k_exponent_max, dim3((unsigned)((n4 + kExpMaxGranules - 1) / kExpMaxGranules)), dim3(256), 0, s,
+                     reinterpret_cast<const u32x4*>(x), n4, expw);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (mode == kStochastic) return quantize_packed_mode<kStochastic>(x, ngroups, m, seed, mant, expw, status, s);
