@@ -48,18 +48,34 @@ __device__ __forceinline__ void block_improvement(double num, double den, double
 }
 
 // out[0..1] = the sums of the nparts partial pairs at part, in a fixed order
-// (one block): the result does not depend on scheduling.
-__global__ __launch_bounds__(256) void k_improvement_finalize(double* out, const double* part, int64_t nparts) {
-  __shared__ double red[2][256];
+// (one block of 1024 threads: thread t adds pairs t, t + 1024, ... in order,
+// reading them in batches of eight independent pairs, then a fixed tree over
+// the threads): the result does not depend on scheduling.
+__global__ __launch_bounds__(1024) void k_improvement_finalize(double* out, const double* part, int64_t nparts) {
+  __shared__ double red[2][1024];
   double num = 0.0, den = 0.0;
-  for (int64_t i = threadIdx.x; i < nparts; i += 256) {
+  int64_t i = threadIdx.x;
+  for (; i + 7 * 1024 < nparts; i += 8 * 1024) {
+    double a[8], b[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      a[j] = part[2 * (i + 1024 * j)];
+      b[j] = part[2 * (i + 1024 * j) + 1];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      num += a[j];
+      den += b[j];
+    }
+  }
+  for (; i < nparts; i += 1024) {
     num += part[2 * i];
     den += part[2 * i + 1];
   }
   red[0][threadIdx.x] = num;
   red[1][threadIdx.x] = den;
   __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
+  for (int w = 512; w > 0; w >>= 1) {
     if ((int)threadIdx.x < w) {
       red[0][threadIdx.x] += red[0][threadIdx.x + w];
       red[1][threadIdx.x] += red[1][threadIdx.x + w];
@@ -435,7 +451,7 @@ static hipError_t launch_adaptive_parts(const float* x, int64_t R, int64_t C, in
     const hipError_t e = launch_adaptive_kernel(x, R, C, group_axis, g, mode, seed, mant4, mant2, exps, part, status, s);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_improvement_finalize, dim3(1), dim3(256), 0, s, out, part, nparts);
+  hipLaunchKernelGGL(k_improvement_finalize, dim3(1), dim3(1024), 0, s, out, part, nparts);
   return hipGetLastError();
 }
 
