@@ -67,8 +67,9 @@ def mfma_issue_factor(pa, pb, g=G):
 
 
 def code_bits(m):
-    """Mantissa bits per value: 4-bit codes for a chunk of at most 2 bits, 6-bit
-    codes otherwise (plane 0 of m = 1, 2, 5, 6 is the 4-bit one)."""
+    """Mantissa bits per value of the chunk-plane layout: one FP4 plane (4) for
+    m = 1, 2; one FP6 plane (6) for m = 3, 4; an FP6 and a Lo2 plane (6 + 4)
+    for m = 5, 6; two FP6 planes (12) for m = 7, 8."""
     return {1: 4, 2: 4, 3: 6, 4: 6, 5: 10, 6: 10, 7: 12, 8: 12}[m]
 
 
