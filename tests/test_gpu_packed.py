@@ -162,3 +162,36 @@ def test_gemm_packed_ragged_and_wide_range():
             A, qa, ea = check_packed(xa, am, "stochastic", seed=5)
             B, qb, eb = check_packed(xb, bm, "nearest")
             check_gemm(A, B, qa, ea, qb, eb, am, bm)
+
+
+def test_packed_full_size_sampled():
+    """The bench's packed conversion (8192 x 8192 half-normal, seed 1234): the
+    whole exponent stream (E_max word and every group's 3-bit offset), and the
+    mantissa bytes of 32 sampled rows, against the oracle."""
+    R = C = 8192
+    x = synth.draw("half_normal", (R, C), 21)
+    xt = torch.from_numpy(x).cuda()
+    ng = R * C // 16
+    emax = max_exponent_field(x)
+    for m, mode in [(2, "stochastic"), (4, "nearest")]:
+        announce("quantize_packed full size 8192x8192 m=%d %s" % (m, mode))
+        t = fb.quantize_packed(xt, m=m, rounding=mode, seed=1234)
+        torch.cuda.synchronize()
+        q, E, base, bad = oracle.quantize_packed(x, g=16, m=m, mode=mode, seed=1234, threads=THREADS)
+        assert bad == 0 and base == max(emax - 7, 0)
+        exp = t.exp.cpu().numpy()
+        stream = exp[4:]
+        assert int(np.frombuffer(exp[:4].tobytes(), np.uint32)[0]) == emax
+        gid = np.arange(ng)
+        e3 = np.zeros(ng, np.int64)
+        for b in range(3):
+            pos = 3 * gid + b
+            e3 |= ((stream[pos // 8].astype(np.int64) >> (pos % 8)) & 1) << b
+        assert np.array_equal(base + e3, E.reshape(-1).astype(np.int64)), "exponent stream differs"
+        mant = t.mant.cpu().numpy()
+        npl = (m + 1) // 2
+        for r0 in np.random.default_rng(m).choice(R // 8, 4, replace=False) * 8:
+            g0, g1 = int(r0) * (C // 16), (int(r0) + 8) * (C // 16)
+            sl = np.concatenate([mant[(c * ng + g0) * 6:(c * ng + g1) * 6] for c in range(npl)])
+            want, _ = bfp_codec.encode_packed(q[r0:r0 + 8], E[r0:r0 + 8], emax, m)
+            assert np.array_equal(sl, want), "mantissas of rows %d..%d differ" % (r0, r0 + 7)

@@ -168,3 +168,39 @@ def test_gemm_ws_caller_workspace_reused():
         torch.cuda.synchronize()
         Co, S = oracle.gemm(qa, ea, 4, qb, eb, 4, g=8, threads=THREADS)
         assert np.all(np.abs(C.cpu().numpy().astype(np.float64) - Co) <= 1e-6 * S)
+
+
+def test_gemm_ws_full_size_sampled():
+    """The format sweep's out-projection GEMM (8192 x 4096 x 4096, the bench's
+    inputs) on both routes: 48 sampled rows of C (all 4096 columns) against the
+    oracle, for packed operands, groups of 8 and 64, and precisions below the
+    stored width."""
+    M, N, K = 8192, 4096, 4096
+    xa = synth.bf16_round(synth.draw("normal", (M, K), 41))
+    xb = synth.bf16_round(synth.draw("weights", (N, K), 42))
+    ta, tb = torch.from_numpy(xa).cuda(), torch.from_numpy(xb).cuda()
+    rows = np.sort(np.random.default_rng(7).choice(M, 48, replace=False))
+    cases = [("packed", 16, 2, 2, 2, 2), ("packed", 16, 4, 4, 3, 4), ("chunk", 8, 4, 4, 4, 4),
+             ("chunk", 64, 4, 4, 4, 4), ("chunk", 16, 4, 4, 2, 2), ("chunk", 16, 6, 6, 3, 3)]
+    for kind, g, am, bm, m_a, m_b in cases:
+        announce("gemm_ws full size 8192x4096x4096 %s g=%d stored (%d,%d) at (%d,%d)" % (kind, g, am, bm, m_a, m_b))
+        if kind == "packed":
+            A, B = fb.quantize_packed(ta, m=am), fb.quantize_packed(tb, m=bm)
+            qa, ea, _, _ = oracle.quantize_packed(xa, g=16, m=am, threads=THREADS)
+            qb, eb, _, _ = oracle.quantize_packed(xb, g=16, m=bm, threads=THREADS)
+        else:
+            A, B = fb.quantize(ta, g=g, m=am), fb.quantize(tb, g=g, m=bm)
+            qa, ea, _ = oracle.quantize(xa, g=g, m=am, threads=THREADS)
+            qb, eb, _ = oracle.quantize(xb, g=g, m=bm, threads=THREADS)
+        if kind == "chunk":  # (the packed exponent stream is checked in full in test_gpu_packed.py)
+            assert np.array_equal(A.exp.cpu().numpy()[rows], ea[rows])
+        Co, S = oracle.gemm(qa, ea, am, qb, eb, bm, g=g, m_a=m_a, m_b=m_b, rows=rows, threads=THREADS)
+        gemm = fb.gemm_packed if kind == "packed" else fb.gemm
+        for ws in (True, False):
+            C = gemm(A, B, m_a, m_b, workspace=ws)
+            torch.cuda.synchronize()
+            Cg = C[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+            err = np.abs(Cg - Co)
+            assert np.all(err <= 1e-6 * S), "workspace=%s: max err/sum|T| = %.3g" % (
+                ws, float((err / np.maximum(S, 1e-300)).max()))
+        del A, B, C
