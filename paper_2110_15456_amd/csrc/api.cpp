@@ -109,6 +109,10 @@ int ws_plan(int a_m, int b_m, int64_t M, int64_t N, int64_t K, int g, int m_a, i
   p->rep_b = packed || !native || planes_used(b_m, m_b) == 0;
   fastbfp::repack_shape(K, g, &p->k_out, &p->g_out);
   if (p->k_out > kMaxK) return BFP_E_UNSUPPORTED;
+  // the repack kernel: one thread per output 16-value unit, 256 per workgroup
+  if ((p->rep_a && (M * (p->k_out / 16) + 255) / 256 > 0x7fffffff) ||
+      (p->rep_b && (N * (p->k_out / 16) + 255) / 256 > 0x7fffffff))
+    return BFP_E_UNSUPPORTED;
   p->a_mant = p->a_exp = p->b_mant = p->b_exp = 0;
   if (p->rep_a && bfp_quantized_sizes(M, p->k_out, p->g_out, m_a, &p->a_mant, &p->a_exp) != BFP_OK)
     return BFP_E_UNSUPPORTED;

@@ -412,6 +412,10 @@ def test_gemm_ws_size_and_validation(lib):
     k4 = (kmax // 64 + 1) * 16                   # K_out = 4 K just beyond the kernel's limit
     assert k4 <= kmax < 4 * k4 and size(K=k4, g=4)[0] == E_UNSUP and size(K=k4 - 16, g=4)[0] == OK
     assert lib.bfp_gemm_ws_size(4, 4, 8, 8, 64, 16, 4, 4, 0, None) == E_ARG
+    # the repack kernel's workgroup count (one thread per output unit) beyond 31 bits
+    big_m = (1 << 31) - 1
+    assert size(M=big_m, N=16, K=16 * 4096, g=8, ma=4, mb=4)[0] == E_UNSUP
+    assert size(M=16, N=big_m, K=16 * 4096, g=16, ma=4, mb=2, am=4, bm=4)[0] == E_UNSUP
 
     def ws(workspace=FAKE, nbytes=1 << 20, ldc=8, C=FAKE, **kw):
         a = dict(am=4, bm=4, M=8, N=8, K=64, g=16, ma=4, mb=4, packed=0)
