@@ -65,3 +65,45 @@ def test_tiny_cases_exact(g, K, mode):
                         bad = np.argwhere(Cg != Co.astype(np.float32))
                         assert bad.size == 0, "K = 2g not one rounding at %s: gpu %r oracle %r" % (
                             bad[0].tolist(), float(Cg[tuple(bad[0])]), float(Co[tuple(bad[0])]))
+
+
+def _at_exponent(x: np.ndarray, g: int, E: int) -> np.ndarray:
+    """x with every group of g along the rows scaled so that its largest
+    magnitude lies in [2^(E-127), 2^(E-126)): every shared exponent is E."""
+    x = x.astype(np.float64).reshape(x.shape[0], -1, g)
+    top = np.abs(x).max(axis=2, keepdims=True)
+    y = x / top * 1.5 * 2.0 ** (E - 127)
+    return np.ascontiguousarray(y.reshape(x.shape[0], -1).astype(np.float32))
+
+
+@pytest.mark.parametrize("g", [16, 32])
+@pytest.mark.parametrize("big", ["A", "B"])
+def test_exponent_range_edge_exact(g, big):
+    """The stated domain's top edge: one operand's group exponents all at 250
+    (the largest the header allows; a chunk weight of up to +4 then still fits
+    the 8-bit block scale), the other's near 100, K = g, every operand-format
+    variant (m = 2, 4, 6, 8 on either side) and its chunk drops: C must equal
+    the oracle exactly."""
+    xa = synth.draw("normal", (64, g), 9100 + g)
+    xb = synth.draw("normal", (48, g), 9200 + g)
+    hi, lo = 250, 100
+    xa = _at_exponent(xa, g, hi if big == "A" else lo)
+    xb = _at_exponent(xb, g, lo if big == "A" else hi)
+    A, B = {}, {}
+    for m in (2, 4, 6, 8):
+        announce("quantize exponent edge g=%d big=%s m=%d" % (g, big, m))
+        A[m] = check_quantize(xa, -1, g, m, "nearest")
+        B[m] = check_quantize(xb, -1, g, m, "nearest")
+        assert A[m][2].max() == (hi if big == "A" else lo) and B[m][2].max() == (lo if big == "A" else hi)
+    for am in (2, 4, 6, 8):
+        for bm in (2, 4, 6, 8):
+            (Ta, qa, ea), (Tb, qb, eb) = A[am], B[bm]
+            for m_a in chunk_drops(am):
+                for m_b in chunk_drops(bm):
+                    announce("gemm exponent edge g=%d big=%s stored (%d,%d) at (%d,%d)" % (g, big, am, bm, m_a, m_b))
+                    Cg = fb.gemm(Ta, Tb, m_a, m_b).cpu().numpy()
+                    Co, _ = oracle.gemm(qa, ea, am, qb, eb, bm, g=g, m_a=m_a, m_b=m_b, threads=THREADS)
+                    assert np.isfinite(Co).all()
+                    bad = np.argwhere(Cg.astype(np.float64) != Co)
+                    assert bad.size == 0, "exponent edge not exact at %s: gpu %r oracle %r" % (
+                        bad[0].tolist(), float(Cg[tuple(bad[0])]), float(Co[tuple(bad[0])]))
