@@ -355,8 +355,29 @@ typedef int v6i __attribute__((ext_vector_type(6)));
 // wait), and mma_drain() covers the reads after it.  The statement is not
 // volatile: a volatile one would also keep the scheduler from moving fragment
 // reads across it.
-template <int FA, int FB>
+// SA / SB: which byte of sa / sb is the block scale (the instruction's
+// op_sel bits for its second / first source): 0 for the low byte, 1 for the
+// next, so that one 16-bit exponent read serves both K-steps of a slab.
+#define FASTBFP_MFMA_ASM(SEL, CB, BG) \
+  "s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 " SEL " cbsz:" #CB " blgp:" #BG
+#define FASTBFP_MFMA_SEL(CB, BG, BOP, AOP)                                                                      \
+  {                                                                                                            \
+    if constexpr (SA == 0 && SB == 0)                                                                          \
+      asm(FASTBFP_MFMA_ASM("op_sel_hi:[0,0,0]", CB, BG) : "+a"(acc) : "v"(BOP), "v"(AOP), "v"(sb), "v"(sa));    \
+    else if constexpr (SA == 0)                                                                                \
+      asm(FASTBFP_MFMA_ASM("op_sel:[1,0,0] op_sel_hi:[0,0,0]", CB, BG)                                         \
+          : "+a"(acc) : "v"(BOP), "v"(AOP), "v"(sb), "v"(sa));                                                 \
+    else if constexpr (SB == 0)                                                                                \
+      asm(FASTBFP_MFMA_ASM("op_sel:[0,1,0] op_sel_hi:[0,0,0]", CB, BG)                                         \
+          : "+a"(acc) : "v"(BOP), "v"(AOP), "v"(sb), "v"(sa));                                                 \
+    else                                                                                                       \
+      asm(FASTBFP_MFMA_ASM("op_sel:[1,1,0] op_sel_hi:[0,0,0]", CB, BG)                                         \
+          : "+a"(acc) : "v"(BOP), "v"(AOP), "v"(sb), "v"(sa));                                                 \
+  }
+template <int FA, int FB, int SA = 0, int SB = 0>
 __device__ __forceinline__ void mma(v4f& acc, const v8i& a, const v8i& b, int sa, int sb) {
+  static_assert(SA == 0 || SA == 1, "scale byte 0 or 1");
+  static_assert(SB == 0 || SB == 1, "scale byte 0 or 1");
   // B's fragment is the instruction's first operand and A's the second, so
   // the result is the tile of C transposed: a lane's four accumulators are
   // four consecutive columns of one row of C (see the epilogue).
@@ -366,22 +387,20 @@ __device__ __forceinline__ void mma(v4f& acc, const v8i& a, const v8i& b, int sa
   const v6i a6 = __builtin_shufflevector(a, a, 0, 1, 2, 3, 4, 5);
   const v6i b6 = __builtin_shufflevector(b, b, 0, 1, 2, 3, 4, 5);
   if constexpr (FA && FB)
-    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:4"
-        : "+a"(acc) : "v"(b4), "v"(a4), "v"(sb), "v"(sa));
+    FASTBFP_MFMA_SEL(4, 4, b4, a4)
   else if constexpr (FA)
-    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:2 blgp:4"
-        : "+a"(acc) : "v"(b6), "v"(a4), "v"(sb), "v"(sa));
+    FASTBFP_MFMA_SEL(2, 4, b6, a4)
   else if constexpr (FB)
-    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:4 blgp:2"
-        : "+a"(acc) : "v"(b4), "v"(a6), "v"(sb), "v"(sa));
+    FASTBFP_MFMA_SEL(4, 2, b4, a6)
   else
-    asm("s_nop 1\n\tv_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %4 op_sel_hi:[0,0,0] cbsz:2 blgp:2"
-        : "+a"(acc) : "v"(b6), "v"(a6), "v"(sb), "v"(sa));
+    FASTBFP_MFMA_SEL(2, 2, b6, a6)
 #else
-  acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b, a, acc, mfma_fmt<FB>::value, mfma_fmt<FA>::value, 0, sb, 0,
-                                                         sa);
+  acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b, a, acc, mfma_fmt<FB>::value, mfma_fmt<FA>::value, SB, sb,
+                                                         SA, sa);
 #endif
 }
+#undef FASTBFP_MFMA_SEL
+#undef FASTBFP_MFMA_ASM
 // Wait states between the last MFMA and any other read of its accumulators
 // (a 16x16x128 block-scaled MFMA needs at most 19).  Every accumulator then
 // passes through an empty statement that comes after them (volatile
@@ -696,16 +715,19 @@ __global__ __launch_bounds__(CF::NT) void k_gemm_mx(const uint8_t* __restrict__ 
       constexpr int BPP = TM;           // blocks per phase
       constexpr int NPH = CF::KSTEPS;   // phases per slab
       v8i bf[2][TN], af[2];
-      int be[2][TN], ae[2];
+      // A lane's exponents of both K-steps (groups 2 lb and 2 lb + 1) are
+      // adjacent bytes: one 16-bit read per fragment in the first phase, and
+      // each MFMA takes its K-step's byte of it as the block scale.
+      int be[TN], ae[TM];
+      auto rd16 = [&](int off) { return (int)*reinterpret_cast<const uint16_t*>(xcur + off); };
       auto read_b = [&](int ks, int j) {
-        bf[ks & 1][j] = CF::G == 16 ? op_b<FA, FB>(rd(slot_addr(CF::OFF_B, FB, b_r, j, ks)), ks)
-                                    : op32(FB, CF::OFF_B, b_r, j);
-        be[ks & 1][j] = (int)xcur[eb_lane + j * 16 * ER + ks];
+        bf[ks & 1][j] = op_b<FA, FB>(rd(slot_addr(CF::OFF_B, FB, b_r, j, ks)), ks);
+        if (ks == 0) be[j] = rd16(eb_lane + j * 16 * ER);
       };
       auto read_a = [&](int blk) {
         const int ks = blk / BPP, i = blk % BPP;
-        af[blk & 1] = CF::G == 16 ? op_a<FA, FB>(rd(slot_addr(0, FA, a_r, i, ks)), ks) : op32(FA, 0, a_r, i);
-        ae[blk & 1] = (int)xcur[ea_lane + i * 16 * ER + ks];
+        af[blk & 1] = op_a<FA, FB>(rd(slot_addr(0, FA, a_r, i, ks)), ks);
+        if (ks == 0) ae[i] = rd16(ea_lane + i * 16 * ER);
       };
 #pragma unroll
       for (int j = 0; j < TN; ++j) read_b(0, j);
@@ -725,8 +747,12 @@ __global__ __launch_bounds__(CF::NT) void k_gemm_mx(const uint8_t* __restrict__ 
           for (int j = bi * TN / BPP; j < (bi + 1) * TN / BPP; ++j) read_b(ph + 1, j);
         }
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          mma<FA, FB>(acc[i][j], af[blk & 1], bf[ph & 1][j], ae[blk & 1], be[ph & 1][j]);
+        for (int j = 0; j < TN; ++j) {
+          if (ph == 0)
+            mma<FA, FB, 0, 0>(acc[i][j], af[blk & 1], bf[0][j], ae[i], be[j]);
+          else
+            mma<FA, FB, 1, 1>(acc[i][j], af[blk & 1], bf[1][j], ae[i], be[j]);
+        }
         issue_after(blk, NPH * BPP);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -787,22 +813,28 @@ __global__ __launch_bounds__(CF::NT) void k_gemm_mx(const uint8_t* __restrict__ 
       const int c_r = CA ? a_r : b_r, d_r = CA ? b_r : a_r;
       const int c_e = CA ? ea_lane : eb_lane, d_e = CA ? eb_lane : ea_lane;
       u32x4 dr[2][ND][TD];  // D's raw slots per K-step (an FP4 / Lo2 slot only in [0])
-      int de[2][TD];
+      int de[TD];
       v8i dd[ND][TD];       // D's repeated operands of the current K-step
       u32x4 ch[2], cl[TC];  // C's FP6 slots (per block) and Lo2 slots (per fragment)
-      int ce[2];
+      // Exponents: both K-steps' bytes of a fragment in one 16-bit read (in
+      // K-step 0); each MFMA takes its K-step's byte (the weights added to
+      // both bytes stay below 256 for exponents up to 250).
+      int ce[TC];
+      auto rd16 = [&](int off) { return (int)*reinterpret_cast<const uint16_t*>(xcur + off); };
       auto read_d = [&](int ks, int t) {
         static_for<ND>([&](auto pc) {
           constexpr int p = decltype(pc)::value, k = p == 0 ? DK0 : DK1, off = p == 0 ? DP0 : DP1;
           if (k == kPlaneFP6 || ks == 0) dr[k == kPlaneFP6 ? ks : 0][p][t] = rd(slot_addr(off, k != kPlaneFP6, d_r, t, ks));
         });
-        de[ks][t] = (int)xcur[d_e + t * 16 * ER + ks];
+        if (ks == 0) de[t] = rd16(d_e + t * 16 * ER);
       };
       auto read_c = [&](int blk) {
         const int ks = blk / TC, c = blk % TC;
         ch[blk & 1] = rd(slot_addr(C0, 0, c_r, c, ks));
-        if (ks == 0) cl[c] = rd(slot_addr(C1, 1, c_r, c, 0));
-        ce[blk & 1] = (int)xcur[c_e + c * 16 * ER + ks];
+        if (ks == 0) {
+          cl[c] = rd(slot_addr(C1, 1, c_r, c, 0));
+          ce[c] = rd16(c_e + c * 16 * ER);
+        }
       };
       // the group repeated in both halves, from a raw slot of a plane of kind k
       auto make_dup = [&](int k, const u32x4& x, int ks) -> v8i {
@@ -835,18 +867,19 @@ __global__ __launch_bounds__(CF::NT) void k_gemm_mx(const uint8_t* __restrict__ 
         lo2_unpack(cl[c][2 * ks], cl[c][2 * ks + 1], t0, t1, t2);
         const u32x4& h = ch[blk & 1];
         const v8i cv = v8i{(int)h[0], (int)h[1], (int)h[2], (int)t0, (int)t1, (int)t2, 0, 0};
-        const int e_c = ce[blk & 1];
+        const int e_c = ce[c];
         // plane-major: consecutive MFMAs accumulate into different tiles
         static_for<ND>([&](auto pc) {
           constexpr int p = decltype(pc)::value;
           constexpr int W = 2 + mx::plane_weight<ND, FD>(p);
           constexpr int dfp4 = (p == 0 ? DK0 : DK1) == kPlaneFP4;
+          constexpr int W1 = 0x0101 * ((W + 1) / 2), W0 = 0x0101 * (W / 2);  // added to both bytes
 #pragma unroll
           for (int t = 0; t < TD; ++t) {
             if constexpr (CA)
-              mma<0, dfp4>(acc[c][t], cv, dd[p][t], e_c + (W + 1) / 2, de[ks][t] + W / 2);
+              mma<0, dfp4, ks, ks>(acc[c][t], cv, dd[p][t], e_c + W1, de[t] + W0);
             else
-              mma<dfp4, 0>(acc[t][c], dd[p][t], cv, de[ks][t] + (W + 1) / 2, e_c + W / 2);
+              mma<dfp4, 0, ks, ks>(acc[t][c], dd[p][t], cv, de[t] + W1, e_c + W0);
           }
         });
         issue_after(blk, 2 * TC);
