@@ -41,6 +41,14 @@ def check_quantize(x: np.ndarray, axis: int, g: int, m: int, mode: str, seed: in
     output-row range (start, stop) to compare; default all."""
     t, st = gpu_quantize(x, axis, g, m, mode, seed)
     assert st == 0
+    q_o, E_o = check_tensor(t, x, axis, g, m, mode, seed, rows)
+    return t, q_o, E_o
+
+
+def check_tensor(t, x: np.ndarray, axis: int, g: int, m: int, mode: str, seed: int = 0, rows=None):
+    """A BFP tensor the library wrote (by any entry point) against the oracle's
+    conversion of x along ``axis``: exponents and mantissa bytes of the output
+    rows in ``rows`` (start, stop), default all.  Returns the oracle's (q, E)."""
     q_o, E_o, bad = oracle.quantize(x, axis=axis, g=g, m=m, mode=mode, seed=seed, threads=THREADS, rows=rows)
     assert bad == 0
     E = t.exp.cpu().numpy()
@@ -62,4 +70,4 @@ def check_quantize(x: np.ndarray, axis: int, g: int, m: int, mode: str, seed: in
         raise AssertionError("mantissas differ at %d positions, first %s: gpu %s oracle %s"
                              % (len(bad_idx), bad_idx[:3].tolist(), got_q[tuple(bad_idx[0])] if len(bad_idx) else None,
                                 q_o[tuple(bad_idx[0])] if len(bad_idx) else None))
-    return t, q_o, E_o
+    return q_o, E_o

@@ -12,7 +12,7 @@ import oracle
 import bfp_codec
 import paper_2110_15456_amd as fb
 from paper_2110_15456_amd import synth
-from gpu_util import announce, THREADS
+from gpu_util import announce, check_tensor, THREADS
 
 pytestmark = pytest.mark.gpu
 MODES = ("nearest", "stochastic", "truncate")
@@ -128,3 +128,48 @@ def test_dual_special_values():
             tr, tc = fb.quantize_dual(xt, m=m, rounding=mode, seed_rows=1, seed_cols=2)
             torch.cuda.synchronize()
             check_against_oracle(x, tr, tc, m, mode, 1, 2)
+
+
+@pytest.mark.parametrize("m", [2, 4, 6])
+def test_step_dy_full_size(m):
+    """dY of the FFN training step (8192 x 16384, the gradient distribution)
+    in both groupings with stochastic rounding, at the step's size and launch
+    configuration: byte for byte what the single-axis kernels write (those are
+    pinned to the oracle at full size by the quantize tests), and the first and
+    last 16 output rows of each grouping against the oracle directly."""
+    announce("dual full-size dY 8192x16384 m=%d stochastic" % m)
+    x = synth.draw("grads", (8192, 16384), 5400 + m)
+    xt = torch.from_numpy(x).cuda()
+    sr, sc = 1000 + 2 * m, 1001 + 2 * m
+    tr, tc = fb.quantize_dual(xt, g=16, m=m, rounding="stochastic", seed_rows=sr, seed_cols=sc)
+    ur = fb.quantize(xt, g=16, m=m, rounding="stochastic", seed=sr)
+    uc = fb.quantize(xt, group_axis=0, g=16, m=m, rounding="stochastic", seed=sc)
+    torch.cuda.synchronize()
+    assert torch.equal(tr.exp, ur.exp) and torch.equal(tr.mant, ur.mant), "row grouping differs from k_quantize_rows"
+    assert torch.equal(tc.exp, uc.exp) and torch.equal(tc.mant, uc.mant), "column grouping differs from k_quantize_cols"
+    for rows in ((0, 16), (8192 - 16, 8192)):
+        check_tensor(tr, x, -1, 16, m, "stochastic", sr, rows)
+    for rows in ((0, 16), (16384 - 16, 16384)):
+        check_tensor(tc, x, 0, 16, m, "stochastic", sc, rows)
+
+
+@pytest.mark.parametrize("m", [2, 4, 6])
+def test_step_weight_update_full_size(m):
+    """The step's weight update at full size (W 4096 x 16384, alpha = -1e-3),
+    in place as the step runs it: W' bit for bit the oracle's two FP32
+    roundings, and both groupings of W' byte for byte what the single-axis
+    kernels write for W'."""
+    announce("weight update full-size 4096x16384 m=%d" % m)
+    w = synth.draw("weights", (4096, 16384), 5500 + m)
+    dw = synth.draw("grads", (4096, 16384), 5600 + m)
+    wt, dwt = torch.from_numpy(w).cuda(), torch.from_numpy(dw).cuda()
+    w_out, tr, tc = fb.weight_update(wt, dwt, -1e-3, g=16, m=m, w_out=wt)
+    ur = fb.quantize(w_out, g=16, m=m)
+    uc = fb.quantize(w_out, group_axis=0, g=16, m=m)
+    torch.cuda.synchronize()
+    want = oracle.weight_update(w, dw, -1e-3)
+    assert np.array_equal(w_out.cpu().numpy().view(np.uint32), want.view(np.uint32)), "updated weights differ"
+    assert torch.equal(tr.exp, ur.exp) and torch.equal(tr.mant, ur.mant), "row grouping of W' differs"
+    assert torch.equal(tc.exp, uc.exp) and torch.equal(tc.mant, uc.mant), "column grouping of W' differs"
+    check_tensor(tr, want, -1, 16, m, "nearest", 0, (0, 16))
+    check_tensor(tc, want, 0, 16, m, "nearest", 0, (16384 - 16, 16384))
