@@ -249,7 +249,11 @@ def resnet_sweep(torch, fb, synth, dev, args):
     (C[M,N] = A[M,K] B[N,K]^T, g = 16 along K): half-normal activations, N(0, 0.02)
     weights, round to nearest.  These shapes are HBM-bound: the roofline time is
     max(2MNK / int8 MFMA peak, minimum bytes / HBM peak), with minimum bytes =
-    the BFP operands (codes + exponents) read once and the FP32 C written once."""
+    the BFP operands (codes + exponents) read once and the FP32 C written once.
+    The same GEMM with C converted to BFP in the epilogue (the next layer's
+    activations at the width of A, round to nearest) is timed beside it, with
+    its own minimum bytes (the BFP C instead of the FP32 C) and against the
+    unfused route (the FP32 GEMM, then a separate quantize of C)."""
     shapes = {"conv2_x": (256 * 56 * 56, 64, 576), "conv3_x": (256 * 28 * 28, 128, 1152),
               "conv4_x": (256 * 14 * 14, 256, 2304), "conv5_x": (256 * 7 * 7, 512, 4608)}
     pairs = [(2, 2), (2, 4), (4, 4)]
@@ -279,14 +283,38 @@ def resnet_sweep(torch, fb, synth, dev, args):
             nbytes = (M * K * code_bits(pa) + N * K * code_bits(pb)) / 8.0 + (M + N) * K / G + 4.0 * M * N
             gbs = nbytes / (ms * 1e-3) / 1e9
             floor_ms = max(2.0 * M * N * K / (PEAK_INT8_TOPS * 1e12), nbytes / (PEAK_HBM_GBS * 1e9)) * 1e3
+            # C converted to BFP in the epilogue, at A's width
+            T = fb.BFPTensor.empty(M, N, G, pa, dev)
+            fb.gemm_bfp(A, B, pa, out=T)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(reps):
+                fb.gemm_bfp(A, B, pa, out=T)
+            z.record()
+            torch.cuda.synchronize()
+            fms = a.elapsed_time(z) / reps
+            a.record()
+            for _ in range(reps):
+                fb.gemm(A, B, out=C)
+                fb.quantize(C, g=G, m=pa, out=T)
+            z.record()
+            torch.cuda.synchronize()
+            ums = a.elapsed_time(z) / reps
+            fbytes = nbytes - 4.0 * M * N + M * N * code_bits(pa) / 8.0 + M * N / G
+            ffloor_ms = max(2.0 * M * N * K / (PEAK_INT8_TOPS * 1e12), fbytes / (PEAK_HBM_GBS * 1e9)) * 1e3
             out["%s(%d,%d)" % (name, pa, pb)] = {
                 "M": M, "N": N, "K": K, "ms": round(ms, 4), "eff_tops": round(tops, 1),
                 "frac_int8_peak": round(tops / PEAK_INT8_TOPS, 4), "min_bytes": int(nbytes),
                 "GB_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
-                "roofline_ms": round(floor_ms, 4), "frac_roofline": round(floor_ms / ms, 4)}
-            log(args, "gemm %s (%d,%d): %.3f ms, %.0f eff TOPS, %.0f GB/s (%.0f%% of the roofline time)"
-                % (name, pa, pb, ms, tops, gbs, 100.0 * floor_ms / ms))
-            del A, B
+                "roofline_ms": round(floor_ms, 4), "frac_roofline": round(floor_ms / ms, 4),
+                "bfp_out": {"m": pa, "fused_ms": round(fms, 4), "unfused_ms": round(ums, 4),
+                            "speedup": round(ums / fms, 3), "min_bytes": int(fbytes),
+                            "GB_s": round(fbytes / (fms * 1e-3) / 1e9, 1), "roofline_ms": round(ffloor_ms, 4),
+                            "frac_roofline": round(ffloor_ms / fms, 4)}}
+            log(args, "gemm %s (%d,%d): %.3f ms, %.0f eff TOPS, %.0f GB/s (%.0f%% of the roofline time); "
+                "BFP output: %.3f ms fused, %.3f ms unfused (%.0f%% of its roofline time)"
+                % (name, pa, pb, ms, tops, gbs, 100.0 * floor_ms / ms, fms, ums, 100.0 * ffloor_ms / fms))
+            del A, B, T
         del C, wb
     del act
     return out

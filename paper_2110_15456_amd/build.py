@@ -20,7 +20,8 @@ LIB = os.path.join(HERE, "libfastbfp.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 SOURCES = ["quantize.hip", "packed.hip", "repack.hip", "gemm_mx.hip", "gemm_general.hip", "api.cpp"] + [
-    "gemm_mx_%s%s.hip" % (p, g) for g in ("", "_g32") for p in ("11", "12", "21", "22")] + ["gemm_mx_11n.hip"]
+    "gemm_mx_%s%s.hip" % (p, g) for g in ("", "_g32") for p in ("11", "12", "21", "22")] + [
+    "gemm_mx_11n_%d%d.hip" % (fa, fb) for fa in (0, 1) for fb in (0, 1)]
 # Per-source extra flags: the quantizers align values with ldexp and rely on
 # FP32 denormal flushing to read subnormal inputs as zero.
 SOURCE_FLAGS = {"quantize.hip": ["-fgpu-flush-denormals-to-zero"], "packed.hip": ["-fgpu-flush-denormals-to-zero"]}

@@ -1171,36 +1171,30 @@ hipError_t launch_mx_t(const uint8_t* a_mant, const uint8_t* a_exp, int64_t a_ps
   return launch_mx_v<CF, false>(a_mant, a_exp, a_ps, b_mant, b_exp, b_ps, M, N, ng, scale, C, ldc, qo, s);
 }
 
-// One chunk plane per operand, groups of 16, FP32 output, on a BM x BN tile
-// smaller than the default 256 x 256: for GEMMs with few columns (a 64-wide
-// tile wastes no MFMAs on padding when N = 64) or too few 256 x 256 tiles to
-// give every CU work (the ResNet im2col shapes: 98 to 196 tiles on 256 CUs).
+// One chunk plane per operand, groups of 16, on a BM x BN tile smaller than
+// the default 256 x 256: for GEMMs with few columns (a 64-wide tile wastes no
+// MFMAs on padding when N = 64) or too few 256 x 256 tiles to give every CU
+// work (the ResNet im2col shapes: 98 to 196 tiles on 256 CUs).  C in FP32, or
+// converted to BFP in the epilogue (qo).
 template <int BM, int BN, int FA, int FB>
 hipError_t launch_mx_11_tile(const uint8_t* a_mant, const uint8_t* a_exp, const uint8_t* b_mant,
                              const uint8_t* b_exp, int M, int N, int ng, float scale, float* C, int64_t ldc,
-                             hipStream_t s) {
+                             const OutBFP* qo, hipStream_t s) {
   using CF = mx::Cfg<BM, BN, 1, 1, FA, FB, 16>;
   auto al = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; };
   const bool ef = ng % mx::KG == 0 && al(a_exp, 4) && al(b_exp, 4);
-  const int tiles_m = (M + CF::BM - 1) / CF::BM, tiles_n = (N + CF::BN - 1) / CF::BN;
-  const dim3 grid((unsigned)(tiles_m * tiles_n));
-  if (ef)
-    hipLaunchKernelGGL((k_gemm_mx<CF, true, 0>), grid, dim3(CF::NT), 0, s, a_mant, a_exp,
-                       (int64_t)0, b_mant, b_exp, (int64_t)0, M, N, ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
-  else
-    hipLaunchKernelGGL((k_gemm_mx<CF, false, 0>), grid, dim3(CF::NT), 0, s, a_mant, a_exp,
-                       (int64_t)0, b_mant, b_exp, (int64_t)0, M, N, ng, scale, C, ldc, tiles_m, tiles_n, OutBFP{});
-  return hipGetLastError();
+  if (ef) return launch_mx_v<CF, true>(a_mant, a_exp, 0, b_mant, b_exp, 0, M, N, ng, scale, C, ldc, qo, s);
+  return launch_mx_v<CF, false>(a_mant, a_exp, 0, b_mant, b_exp, 0, M, N, ng, scale, C, ldc, qo, s);
 }
 
 #define FASTBFP_MX11_TILE_DECLARE(BM, BN, FA, FB)                                                              \
   extern template hipError_t launch_mx_11_tile<BM, BN, FA, FB>(const uint8_t*, const uint8_t*, const uint8_t*, \
                                                                const uint8_t*, int, int, int, float, float*,   \
-                                                               int64_t, hipStream_t);
+                                                               int64_t, const OutBFP*, hipStream_t);
 #define FASTBFP_MX11_TILE_INSTANTIATE(BM, BN, FA, FB)                                                         \
   template hipError_t launch_mx_11_tile<BM, BN, FA, FB>(const uint8_t*, const uint8_t*, const uint8_t*,       \
                                                         const uint8_t*, int, int, int, float, float*, int64_t, \
-                                                        hipStream_t);
+                                                        const OutBFP*, hipStream_t);
 
 #define FASTBFP_MX_DECLARE(NA, NB, FA, FB, G)                                                          \
   extern template hipError_t launch_mx_t<NA, NB, FA, FB, G>(const uint8_t*, const uint8_t*, int64_t,       \

@@ -62,11 +62,14 @@ FASTBFP_MX11_TILES_DECLARE(1, 1)
 //    slower), but 128x128 for N <= 128 or when 256x256 tiles are too few;
 //  * too few: fewer than 192 tiles leave over a quarter of the 256 CUs idle;
 //    then the next smaller tile, down to 128x64.
-static int gemm_mx11_tile(int64_t M, int64_t N, int fa) {
+// With C converted to BFP in the epilogue (converted), A in FP4 codes gets
+// the FP6 rule: there the 256x128 tile was the slower one (ffn_up (2,2) to
+// m = 2: 0.71 ms against 0.60-0.63 ms on 256x256).
+static int gemm_mx11_tile(int64_t M, int64_t N, int fa, bool converted) {
   constexpr int64_t MIN_TILES = 192;
   auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
   if (N <= 64) return 3;
-  if (fa) return tiles(256, 128) >= MIN_TILES ? 1 : 3;
+  if (fa && !converted) return tiles(256, 128) >= MIN_TILES ? 1 : 3;
   if (N > 128 && tiles(256, 256) >= MIN_TILES) return 0;
   return tiles(128, 128) >= MIN_TILES ? 4 : 3;
 }
@@ -74,11 +77,11 @@ static int gemm_mx11_tile(int64_t M, int64_t N, int fa) {
 template <int FA, int FB>
 static hipError_t launch_11_tile(int t, const uint8_t* a_mant, const uint8_t* a_exp, const uint8_t* b_mant,
                                  const uint8_t* b_exp, int M, int N, int ng, float scale, float* C, int64_t ldc,
-                                 hipStream_t s) {
-  if (t == 1) return launch_mx_11_tile<256, 128, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
-  if (t == 2) return launch_mx_11_tile<256, 64, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
-  if (t == 4) return launch_mx_11_tile<128, 128, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
-  return launch_mx_11_tile<128, 64, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, s);
+                                 const OutBFP* qo, hipStream_t s) {
+  if (t == 1) return launch_mx_11_tile<256, 128, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, qo, s);
+  if (t == 2) return launch_mx_11_tile<256, 64, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, qo, s);
+  if (t == 4) return launch_mx_11_tile<128, 128, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, qo, s);
+  return launch_mx_11_tile<128, 64, FA, FB>(a_mant, a_exp, b_mant, b_exp, M, N, ng, scale, C, ldc, qo, s);
 }
 
 template <int NA, int NB, int G>
@@ -104,13 +107,13 @@ static hipError_t launch_gemm_g(const uint8_t* a_mant, const uint8_t* a_exp, int
   const int fa = na == 1 ? plane0_fp4(a_m) : a_m <= 6, fb = nb == 1 ? plane0_fp4(b_m) : b_m <= 6;
   const float scale = ldexpf(1.0f, scale_log2);
   const int m = (int)M, n = (int)N;
-  if (G == 16 && na == 1 && nb == 1 && !qo) {
-    const int t = tile >= 0 ? tile : gemm_mx11_tile(M, N, fa);
+  if (G == 16 && na == 1 && nb == 1) {
+    const int t = tile >= 0 ? tile : gemm_mx11_tile(M, N, fa, qo != nullptr);
     if (t != 0) {
-      if (!fa && !fb) return launch_11_tile<0, 0>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, s);
-      if (!fa) return launch_11_tile<0, 1>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, s);
-      if (!fb) return launch_11_tile<1, 0>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, s);
-      return launch_11_tile<1, 1>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, s);
+      if (!fa && !fb) return launch_11_tile<0, 0>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, qo, s);
+      if (!fa) return launch_11_tile<0, 1>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, qo, s);
+      if (!fb) return launch_11_tile<1, 0>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, qo, s);
+      return launch_11_tile<1, 1>(t, a_mant, a_exp, b_mant, b_exp, m, n, ng, scale, C, ldc, qo, s);
     }
   }
   if (na == 1 && nb == 1)
@@ -144,7 +147,7 @@ hipError_t launch_gemm_mx_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a
                               uint32_t* status, hipStream_t s) {
   const OutBFP qo{c_mant, c_mant + M * (N / 16) * plane_group_bytes(16, c_m, 0), c_exp, status, c_m, mode,
                   c_m <= 4 ? plane0_fp4(c_m) : c_m <= 6, (uint32_t)seed, (uint32_t)(seed >> 32)};
-  return launch_gemm_any(a_mant, a_exp, a_m, na, b_mant, b_exp, b_m, nb, M, N, K, g, scale_log2, nullptr, N, &qo, 0, s);
+  return launch_gemm_any(a_mant, a_exp, a_m, na, b_mant, b_exp, b_m, nb, M, N, K, g, scale_log2, nullptr, N, &qo, -1, s);
 }
 
 }  // namespace fastbfp

@@ -121,6 +121,30 @@ def test_fused_full_size(m, mode):
     assert torch.equal(T.mant, R.mant)
 
 
+@pytest.mark.parametrize("name,shape", [("conv2_x", (802816, 64, 576)), ("conv3_x", (200704, 128, 1152)),
+                                        ("conv4_x", (50176, 256, 2304)), ("conv5_x", (12544, 512, 4608))])
+def test_fused_resnet_full_size(name, shape):
+    """The ResNet-18 im2col shapes at full size, in the bench's launch
+    configuration (the small tiles bfp_gemm picks for them): every exponent and
+    mantissa byte of the fused output equal to the separate GEMM and
+    conversion, for the one-chunk pairs the bench times and both rounding
+    modes."""
+    M, N, K = shape
+    g = torch.Generator(device="cuda").manual_seed(4400 + N)
+    x = torch.randn((M, K), generator=g, device="cuda").abs_()
+    w = torch.randn((N, K), generator=g, device="cuda").mul_(0.02)
+    for m_a, m_b in ((2, 2), (2, 4), (4, 4)):
+        A, B = fb.quantize(x, g=16, m=m_a), fb.quantize(w, g=16, m=m_b)
+        C = fb.gemm(A, B)
+        for mode in ("nearest", "stochastic"):
+            announce("gemm_bfp %s (%d,%d)->m%d %s" % (name, m_a, m_b, m_a, mode))
+            T = fb.gemm_bfp(A, B, m_a, rounding=mode, seed=9)
+            R = fb.quantize(C, g=16, m=m_a, rounding=mode, seed=9)
+            torch.cuda.synchronize()
+            assert torch.equal(T.exp, R.exp) and torch.equal(T.mant, R.mant)
+        del A, B, C
+
+
 def test_fused_with_g32_operands():
     """Operands grouped by 32 (the output is still grouped by 16 along N)."""
     M, N, K = 200, 208, 640
