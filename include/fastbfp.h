@@ -309,7 +309,9 @@ int bfp_gemm_tiled(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, co
  *                 BFP_E_UNSUPPORTED otherwise); the output is grouped by 16.
  *   c_m_bits    : 1..8.  round_mode, seed, status_word : as bfp_quantize.
  *   c_mant, c_exp : outputs sized by bfp_quantized_sizes(M, N, 16, c_m_bits).
- * N must be a multiple of 16 (BFP_E_SHAPE otherwise).
+ * N must be a multiple of 16 (BFP_E_SHAPE otherwise).  The workgroup tile
+ * follows bfp_gemm's choice from the shape (bfp_gemm_tiled), except that an
+ * A in FP4 codes is tiled like one in FP6 codes.
  */
 int bfp_gemm_bfp(const uint8_t* a_mant, const uint8_t* a_exp, int a_m_bits, const uint8_t* b_mant, const uint8_t* b_exp,
                  int b_m_bits, int64_t M, int64_t N, int64_t K, int g, int m_a, int m_b, int c_m_bits, int round_mode,
